@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Benchmark of the triangular multiplicative update on one MI355X.
+
+One step = one layer = the outgoing (Eq. 2) and the incoming (Eq. 3) update
+of a seeded N x N x 128 bf16 pair tensor resident in HBM (N = 4096 by
+default), each through the library's three kernels K1 projection -> K2
+contraction -> K3 epilogue (exactly the launches tri_mul_outgoing /
+tri_mul_incoming make), with HIP events between the kernels so that every
+kernel's duration is measured inside the timed region on the stream it runs
+on.
+
+Prints one JSON line.  `value` is the layer throughput in TFLOP/s
+(algorithmic flops of both directions / wall time of the step); the
+roofline object reports the contraction kernel against the bf16 MFMA peak.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def cpu_baseline(N, sample):
+    """The fp64 oracle (as it stands) timed on host cores on a bounded sample
+    of the same workload, extrapolated per stage to the whole layer.
+
+    Sample: one direction (outgoing) for a `sample` x `sample` block of output
+    pairs of the N = 4096 problem: the projections of 2 x sample x N pairs,
+    the contraction of sample^2 pairs over all N tokens and 128 channels, and
+    the epilogue of sample^2 pairs.  Each stage's measured cost per unit
+    (pair, pair x token) is scaled to the full layer (2 directions)."""
+    import ctypes
+
+    import numpy as np
+
+    import oracle
+    from paper_2603_14806_amd import perf, synth
+    try:   # keep freed heap memory mapped: first-touch page faults otherwise dominate numpy's temporaries
+        libc = ctypes.CDLL("libc.so.6")
+        libc.mallopt(-3, 1 << 30)    # M_MMAP_THRESHOLD
+        libc.mallopt(-1, 1 << 62)    # M_TRIM_THRESHOLD
+    except Exception:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    W = {k: oracle.f64(v) for k, v in synth.weights(dtype="bf16").items()}
+    rows = synth.pair_tensor(N, dtype="bf16", shape=(2 * sample, N, 128))  # stand-in z rows, same law
+    mask_rows = np.ones((2 * sample, N))
+    t0 = time.perf_counter()
+    a, _, _ = oracle.project(rows[:sample], mask_rows[:sample], W)
+    _, b, _ = oracle.project(rows[sample:], mask_rows[sample:], W)
+    t1 = time.perf_counter()
+    C = oracle.contract_outgoing(a, b)
+    t2 = time.perf_counter()
+    zb = oracle.f64(rows[:sample, :sample])
+    m = np.ones((sample, sample))
+    _, _, g = oracle.project(zb, m, W)
+    oracle.epilogue(C, g, m, W)
+    t3 = time.perf_counter()
+    per_pair_proj = (t1 - t0) / (2 * sample * N)
+    per_pair_token = (t2 - t1) / (sample * sample * N)
+    per_pair_epi = (t3 - t2) / (sample * sample)
+    # full direction: projections of N^2 pairs, contraction over N^3, epilogue N^2
+    t_dir = per_pair_proj * N * N + per_pair_token * N ** 3 + per_pair_epi * N * N
+    f = perf.flops(N)["total"]
+    return {"value": round(2 * f / (2 * t_dir) / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"outgoing update of a {sample}x{sample} block of output pairs at N={N} (c_z=c=128, fp64): "
+                       f"projections of {2 * sample}x{N} pairs, contraction over {N} tokens, epilogue; "
+                       f"measured {t3 - t0:.1f} s, per-stage cost extrapolated to both directions of the layer "
+                       f"({2 * t_dir:.0f} s per layer)"),
+            "sample_seconds": round(t3 - t0, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--N", type=int, default=4096)
+    ap.add_argument("--cpu-sample", type=int, default=128)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU path; "
+              "the per-device tile of a sharded run is measured by the block benchmark.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2603_14806_amd import perf, synth
+    from paper_2603_14806_amd import trimul as T
+
+    N = args.N
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print(f"[bench] N={N} steps={args.steps} warmup={args.warmup}", file=sys.stderr, flush=True)
+    layer = T.TriMul(synth.weights(dtype="bf16"), dtype="bf16", out_dtype="f32")
+    z = synth.pair_tensor(N, dtype="bf16", device=dev)
+    mask = synth.token_mask(N, 0, device=dev)
+    A = torch.empty((128, N, N), dtype=torch.bfloat16, device=dev)
+    B = torch.empty_like(A)
+    C = torch.empty((128, N, N), dtype=torch.float32, device=dev)
+    outs = [torch.empty((N, N, 128), dtype=torch.float32, device=dev) for _ in range(2)]
+    stream = torch.cuda.current_stream()
+    h = layer.h
+
+    def step(evs):
+        for d, direction in enumerate((T.TRI_MUL_OUTGOING, T.TRI_MUL_INCOMING)):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if evs is not None else None
+            if e: e[0].record(stream)
+            T.tri_mul_project(h, z, mask, N, direction, A, B, stream)
+            if e: e[1].record(stream)
+            T.tri_mul_contract(h, A, B, N, C, stream)
+            if e: e[2].record(stream)
+            T.tri_mul_epilogue(h, C, z, mask, N, outs[d], stream)
+            if e: e[3].record(stream)
+            if e: evs.append(e)
+
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    evs = []
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(evs)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    k_ms = {name: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / len(evs)
+            for i, name in enumerate(("project", "contract", "epilogue"))}
+    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/layer; per kernel {k_ms}", file=sys.stderr, flush=True)
+
+    # the full entry points (one call = the same three launches), outside the timed region
+    ws, need = layer.workspace(N)
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record(stream)
+    for _ in range(2):
+        T.tri_mul_outgoing(h, z, mask, N, outs[0], ws, need, stream)
+        T.tri_mul_incoming(h, z, mask, N, outs[1], ws, need, stream)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    full_ms = f0.elapsed_time(f1) / 2
+
+    fl = perf.flops(N)
+    by = perf.bytes_moved(N)
+    layer_flops = 2 * fl["total"]
+    contract_tflops = fl["contract"] / (k_ms["contract"] * 1e-3) / 1e12
+    result = {
+        "metric": "triangle-mult ms/layer + TFLOP/s at N=4096 bf16; % of MFMA bf16 peak",
+        "value": round(layer_flops / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"triangle multiplicative update, outgoing + incoming (one layer), N={N}, c_z=128, "
+                               f"c=128, bf16 storage / fp32 accumulation, fp32 output, all-ones mask, z~N(0,1)",
+                   "N": N, "c_z": 128, "c": 128, "parallelism": "none (one GPU)"},
+        "ms_per_layer": round(ms_step, 4),
+        "ms_per_layer_full_calls": round(full_ms, 4),
+        "contract_pct_of_bf16_peak": round(100 * contract_tflops / perf.PEAK_BF16_TFLOPS, 2),
+        "kernels": {
+            "project": {"ms": round(k_ms["project"], 4),
+                        "GB_per_s": round(by["project"] / (k_ms["project"] * 1e-3) / 1e9, 1),
+                        "TFLOP_per_s": round(fl["project"] / (k_ms["project"] * 1e-3) / 1e12, 2)},
+            "contract": {"ms": round(k_ms["contract"], 4), "TFLOP_per_s": round(contract_tflops, 2)},
+            "epilogue": {"ms": round(k_ms["epilogue"], 4),
+                         "GB_per_s": round(by["epilogue"] / (k_ms["epilogue"] * 1e-3) / 1e9, 1)},
+        },
+        "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "kernel": "k2_contract_mfma",
+                     "per_launch": f"2*N^3*c = {fl['contract']:.4e} flop (128 channels of one {N}^3 product)"},
+        "cpu_baseline": None,
+    }
+    del A, B, C, outs, z, ws
+    layer.close()
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(N, args.cpu_sample)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

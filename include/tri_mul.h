@@ -1,0 +1,189 @@
+/*
+ * tri_mul.h -- C ABI of the MI355X (gfx950) triangular multiplicative update.
+ *
+ * The operation (Fold-CP, Section 3.3, Eq. 2 outgoing and Eq. 3 incoming):
+ *
+ *   outgoing:  C[i][j][c] = sum_k a[i][k][c] * b[j][k][c]
+ *   incoming:  C[i][j][c] = sum_k a[k][i][c] * b[k][j][c]
+ *
+ * where a and b are gated projections of the pair representation z
+ * (Section 3.3: "projections" of z with "element-wise gating").  For every
+ * pair (i, j), with pair mask m_ij = m_i * m_j:
+ *
+ *   x_ij   = LN_in(z_ij)                              over c_z channels
+ *   a_ij   = m_ij * sigmoid(W_ga x_ij) * (W_a x_ij)   c channels
+ *   b_ij   = m_ij * sigmoid(W_gb x_ij) * (W_b x_ij)
+ *   out_ij = m_ij * sigmoid(W_g x_ij) * (W_o LN_out(C_ij))   c_z channels
+ *
+ * LN is LayerNorm with the biased variance and epsilon ln_eps.  The library
+ * returns the update out (the right-hand side of Eq. 2/3); the residual add
+ * z + out is the caller's.  Padded tokens (mask 0) contribute exactly zero to
+ * every sum and get exactly zero output.
+ *
+ * The paper shards z over a sqrt(P) x sqrt(P) grid (Section 2.1.1) and runs
+ * the contraction as a Cannon ring in which every step multiplies the resident
+ * row block of a with the column block of b and adds the product into the
+ * output block (Section 3.3, Fig. 2b).  tri_mul_block_accumulate() is one such
+ * step for one device's tile.
+ *
+ * Conventions for every call:
+ *   - Every tensor pointer is a DEVICE pointer (hipMalloc / torch CUDA
+ *     memory) unless stated otherwise; every struct pointer is a HOST pointer.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued asynchronously on it; device faults surface at the
+ *     caller's next synchronisation.
+ *   - Arguments are validated synchronously before anything is enqueued.
+ *     On failure nothing is launched and a negative status is returned;
+ *     tri_mul_last_error() then describes the failure (thread-local text).
+ *   - No C++ exception crosses this interface.
+ *   - One handle may be used from one stream at a time.
+ *   - Tensor pointers must be 16-byte aligned; row strides given in elements
+ *     must keep every row 16-byte aligned.
+ *   - Supported sizes: c_z = c = 128.  1 <= N <= 65536 (and N*N*c fits in
+ *     int64).
+ */
+#ifndef TRI_MUL_H
+#define TRI_MUL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define TRI_MUL_OK            0
+#define TRI_MUL_EINVAL       -1  /* null pointer, bad size, bad alignment, bad enum */
+#define TRI_MUL_EUNSUPPORTED -2  /* valid but unsupported configuration           */
+#define TRI_MUL_ENOMEM       -3  /* workspace too small or device allocation failed */
+#define TRI_MUL_EHIP         -4  /* the HIP runtime reported an error             */
+
+/* Storage types. */
+#define TRI_MUL_F32  0           /* float32 storage, float32 arithmetic           */
+#define TRI_MUL_BF16 1           /* bfloat16 storage, float32 accumulation        */
+
+/* Directions (Eq. 2 and Eq. 3). */
+#define TRI_MUL_OUTGOING 0
+#define TRI_MUL_INCOMING 1
+
+typedef struct tri_mul_handle_s* tri_mul_handle_t;
+
+/* Layer parameters.  All weight pointers are DEVICE pointers of type `dtype`,
+ * linear maps in [out][in] row-major layout (y = W x):
+ *   ln_in_w, ln_in_b   [c_z]        input LayerNorm gain and bias
+ *   w_a, w_ga          [c][c_z]     value / gate projection of a
+ *   w_b, w_gb          [c][c_z]     value / gate projection of b
+ *   w_g                [c_z][c_z]   output gate projection
+ *   ln_out_w, ln_out_b [c]          output LayerNorm gain and bias
+ *   w_o                [c_z][c]     output projection
+ * The library copies (and repacks) them during tri_mul_init; the caller may
+ * free its copies once tri_mul_init has returned. */
+typedef struct {
+    int32_t c_z;
+    int32_t c;
+    int32_t dtype;       /* TRI_MUL_F32 or TRI_MUL_BF16: z, weights, panels */
+    int32_t out_dtype;   /* TRI_MUL_F32 or TRI_MUL_BF16: out               */
+    float   ln_eps;      /* LayerNorm epsilon, e.g. 1e-5                    */
+    const void* ln_in_w;
+    const void* ln_in_b;
+    const void* w_a;
+    const void* w_ga;
+    const void* w_b;
+    const void* w_gb;
+    const void* w_g;
+    const void* ln_out_w;
+    const void* ln_out_b;
+    const void* w_o;
+} tri_mul_params_t;
+
+/* One device's tile of the 2-D pair grid and one k-panel of the ring
+ * (Section 2.1.1 tiling; Section 3.3 ring step).  Token indices are global:
+ *   output rows  i in [row0, row0 + rows),  columns j in [col0, col0 + cols),
+ *   k-panel      k in [k0, k0 + klen) of n_total tokens.
+ * ld_a / ld_b are the row strides (elements) of the a / b panels, >= klen,
+ * multiples of 8.  k_index / k_count number the panels of one tile: the call
+ * with k_index == 0 overwrites the accumulator, later calls add to it, and
+ * the call with k_index == k_count - 1 also runs the epilogue. */
+typedef struct {
+    int64_t n_total;
+    int64_t row0, col0;
+    int64_t rows, cols;
+    int64_t k0, klen;
+    int64_t ld_a, ld_b;
+    int32_t k_index, k_count;
+} tri_mul_block_view_t;
+
+/* Create a handle: validates `p`, allocates device buffers for the repacked
+ * weights and copies them (synchronously with respect to `stream`).
+ * Returns TRI_MUL_EUNSUPPORTED unless c_z == c == 128. */
+int tri_mul_init(tri_mul_handle_t* h, const tri_mul_params_t* p, void* stream);
+
+/* Free the handle's device buffers (after the device has finished with
+ * them).  Destroying NULL is a no-op returning TRI_MUL_OK. */
+int tri_mul_destroy(tri_mul_handle_t h);
+
+/* Text of the last failure on the calling thread ("" if none). */
+const char* tri_mul_last_error(void);
+
+/* Bytes of device workspace tri_mul_outgoing / tri_mul_incoming need for N
+ * tokens: the two channel-major panels A, B [c][N][N] (dtype) and the fp32
+ * contraction result [c][N][N], each 256-byte aligned.  *bytes is a HOST
+ * pointer. */
+int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
+
+/* The full update, Eq. 2 (outgoing) / Eq. 3 (incoming).
+ *   z     [N][N][c_z]  dtype, row-major pair tensor
+ *   mask  [N]          uint8 token mask (nonzero = real token); NULL = all real
+ *   out   [N][N][c_z]  out_dtype; receives the update; must not alias z or ws
+ *   ws    workspace of >= tri_mul_workspace_size(N) bytes, 256-byte aligned
+ * Returns TRI_MUL_ENOMEM if ws_bytes is too small. */
+int tri_mul_outgoing(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                     void* out, void* ws, size_t ws_bytes, void* stream);
+int tri_mul_incoming(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                     void* out, void* ws, size_t ws_bytes, void* stream);
+
+/* One ring step of one device tile (Section 3.3, Fig. 2b):
+ *   acc (+)= A_c * diag(m_k) * B_c^T   for every hidden channel c
+ *   a_panel  [c][rows][ld_a]  dtype, a_panel[c][i][k] = a at (row0+i, k0+k)
+ *   b_panel  [c][cols][ld_b]  dtype, b_panel[c][j][k] = b at (col0+j, k0+k)
+ *   acc      [c][rows][cols]  float32, caller-owned, overwritten when
+ *            k_index == 0 and accumulated into otherwise
+ *   mask     [n_total] uint8 token mask (NULL = all real): column k counts only
+ *            if mask[k0+k] != 0; rows/cols use mask[row0+i] * mask[col0+j]
+ *   z_tile   [rows][cols][c_z] dtype (read only when k_index == k_count-1):
+ *            the pair tensor of the tile, source of the output gate
+ *   out_tile [rows][cols][c_z] out_dtype (written only when k_index ==
+ *            k_count-1): the update of the tile
+ * The panels are direction-agnostic (for the incoming update the caller
+ * supplies the transposed operands). */
+int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v,
+                             const void* a_panel, const void* b_panel, float* acc,
+                             const uint8_t* mask, const void* z_tile, void* out_tile,
+                             void* stream);
+
+/* The three stages of tri_mul_outgoing / tri_mul_incoming, exposed so that
+ * callers can time or check them one by one.
+ *
+ * tri_mul_project: input LayerNorm, gated projections and pair mask.
+ *   Writes A, B [c][N][N] (dtype): outgoing A[c][i][k] = a[i][k][c],
+ *   incoming A[c][i][k] = a[k][i][c] (likewise B), so that either direction
+ *   becomes C[c] = A[c] * B[c]^T. */
+int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                    int32_t direction, void* a_panels, void* b_panels, void* stream);
+
+/* tri_mul_contract: C[c][i][j] = sum_k A[c][i][k] * B[c][j][k] for all c
+ * (A, B [c][N][N] dtype, C [c][N][N] float32, overwritten). */
+int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_panels,
+                     int64_t N, float* c_out, void* stream);
+
+/* tri_mul_epilogue: out[i][j] = m_ij * sigmoid(W_g LN_in(z_ij)) * W_o LN_out(C[:, i, j])
+ * (C [c][N][N] float32, z [N][N][c_z] dtype, out [N][N][c_z] out_dtype). */
+int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z,
+                     const uint8_t* mask, int64_t N, void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRI_MUL_H */

@@ -1,0 +1,350 @@
+// C ABI of the triangle-multiplication library: argument validation, the
+// handle with its repacked weights, and the sequencing of the three kernels
+// K1 (projection), K2 (contraction), K3 (epilogue) on the caller's stream.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/tri_mul.h"
+#include "kernels.h"
+
+using trimul::DeviceWeights;
+
+struct tri_mul_handle_s {
+    int c_z = 0, c = 0, dtype = 0, out_dtype = 0;
+    int device = 0;
+    DeviceWeights w;
+    std::vector<void*> allocations;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int ok() {
+    g_last_error.clear();
+    return TRI_MUL_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(TRI_MUL_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t esize(int dtype) { return dtype == TRI_MUL_BF16 ? 2 : 4; }
+
+size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+constexpr int64_t kMaxN = 65536;
+
+// Row stride of the workspace panels: rows start 16-byte aligned.
+int64_t panel_ld(int64_t N) { return (N + 7) & ~int64_t(7); }
+
+// Host conversion of one stored value to double (exact).
+double to_double(const unsigned char* p, int dtype) {
+    if (dtype == TRI_MUL_F32) {
+        float f;
+        memcpy(&f, p, 4);
+        return f;
+    }
+    uint16_t h;
+    memcpy(&h, p, 2);
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+uint16_t to_bf16_exact(double v) {   // v is already a bf16 value
+    float f = (float)v;
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    return (uint16_t)(u >> 16);
+}
+
+int check_n(int64_t N) {
+    if (N < 1 || N > kMaxN) return fail(TRI_MUL_EINVAL, "N = %lld outside [1, %lld]", (long long)N, (long long)kMaxN);
+    return TRI_MUL_OK;
+}
+
+int check_handle(tri_mul_handle_t h) {
+    if (!h) return fail(TRI_MUL_EINVAL, "null handle");
+    return TRI_MUL_OK;
+}
+
+template <typename T>
+int upload(tri_mul_handle_t h, T** dst, const std::vector<T>& src, hipStream_t s) {
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, src.size() * sizeof(T));
+    if (e != hipSuccess) return fail(TRI_MUL_ENOMEM, "hipMalloc of %zu bytes: %s", src.size() * sizeof(T), hipGetErrorString(e));
+    h->allocations.push_back(p);
+    e = hipMemcpyAsync(p, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "weight upload");
+    *dst = static_cast<T*>(p);
+    return TRI_MUL_OK;
+}
+
+void free_all(tri_mul_handle_t h) {
+    for (void* p : h->allocations) (void)hipFree(p);
+    h->allocations.clear();
+}
+
+int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, void* out, void* ws,
+             size_t ws_bytes, void* stream, int incoming) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!z || !out || !ws) return fail(TRI_MUL_EINVAL, "null z, out or workspace pointer");
+    if (!aligned16(z) || !aligned16(out)) return fail(TRI_MUL_EINVAL, "z and out must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
+    size_t need = 0;
+    if (int rc = tri_mul_workspace_size(h, N, &need)) return rc;
+    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed for N = %lld", ws_bytes, need, (long long)N);
+    const int64_t ld = panel_ld(N);
+    const size_t panel = (size_t)h->c * N * ld * esize(h->dtype);
+    char* base = static_cast<char*>(ws);
+    void* A = base;
+    void* B = base + round256(panel);
+    float* C = reinterpret_cast<float*>(base + 2 * round256(panel));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, ld, incoming, A, B, s);
+    if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
+    e = trimul::launch_contract(h->dtype, A, B, C, N, N, N, ld, ld, N, N * ld, N * ld, N * N, h->c, 0, nullptr, s);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    trimul::EpilogueArgs ea{C, N, N * N, z, mask, 0, 0, N, N, out};
+    e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
+    if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tri_mul_last_error(void) { return g_last_error.c_str(); }
+
+int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream) {
+    if (!out || !p) return fail(TRI_MUL_EINVAL, "null handle or params pointer");
+    *out = nullptr;
+    if (p->dtype != TRI_MUL_F32 && p->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EINVAL, "bad dtype %d", p->dtype);
+    if (p->out_dtype != TRI_MUL_F32 && p->out_dtype != TRI_MUL_BF16) return fail(TRI_MUL_EINVAL, "bad out_dtype %d", p->out_dtype);
+    if (p->c_z <= 0 || p->c <= 0) return fail(TRI_MUL_EINVAL, "c_z = %d, c = %d must be positive", p->c_z, p->c);
+    if (p->c_z != 128 || p->c != 128) return fail(TRI_MUL_EUNSUPPORTED, "only c_z = c = 128 is supported (got %d, %d)", p->c_z, p->c);
+    if (!(p->ln_eps > 0.f)) return fail(TRI_MUL_EINVAL, "ln_eps must be positive");
+    const void* ptrs[] = {p->ln_in_w, p->ln_in_b, p->w_a, p->w_ga, p->w_b, p->w_gb, p->w_g, p->ln_out_w, p->ln_out_b, p->w_o};
+    for (const void* q : ptrs)
+        if (!q) return fail(TRI_MUL_EINVAL, "null weight pointer");
+
+    tri_mul_handle_t h = new (std::nothrow) tri_mul_handle_s;
+    if (!h) return fail(TRI_MUL_ENOMEM, "host allocation failed");
+    h->c_z = p->c_z;
+    h->c = p->c;
+    h->dtype = p->dtype;
+    h->out_dtype = p->out_dtype;
+    h->w.eps = p->ln_eps;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipGetDevice(&h->device);
+    if (e != hipSuccess) {
+        delete h;
+        return hip_fail(e, "hipGetDevice");
+    }
+
+    const int cz = p->c_z, c = p->c;
+    const size_t es = esize(p->dtype);
+    auto fetch = [&](const void* src, size_t n, std::vector<double>& dst) -> int {
+        std::vector<unsigned char> raw(n * es);
+        hipError_t err = hipMemcpyAsync(raw.data(), src, n * es, hipMemcpyDeviceToHost, s);
+        if (err == hipSuccess) err = hipStreamSynchronize(s);
+        if (err != hipSuccess) return hip_fail(err, "weight download");
+        dst.resize(n);
+        for (size_t i = 0; i < n; ++i) dst[i] = to_double(raw.data() + i * es, p->dtype);
+        return TRI_MUL_OK;
+    };
+    std::vector<double> lnw, lnb, wa, wga, wb, wgb, wg, low, lob, wo;
+    int rc = TRI_MUL_OK;
+    if (!rc) rc = fetch(p->ln_in_w, cz, lnw);
+    if (!rc) rc = fetch(p->ln_in_b, cz, lnb);
+    if (!rc) rc = fetch(p->w_a, (size_t)c * cz, wa);
+    if (!rc) rc = fetch(p->w_ga, (size_t)c * cz, wga);
+    if (!rc) rc = fetch(p->w_b, (size_t)c * cz, wb);
+    if (!rc) rc = fetch(p->w_gb, (size_t)c * cz, wgb);
+    if (!rc) rc = fetch(p->w_g, (size_t)cz * cz, wg);
+    if (!rc) rc = fetch(p->ln_out_w, c, low);
+    if (!rc) rc = fetch(p->ln_out_b, c, lob);
+    if (!rc) rc = fetch(p->w_o, (size_t)cz * c, wo);
+    if (rc) {
+        delete h;
+        return rc;
+    }
+
+    // fp32 copies for the VALU kernels.
+    std::vector<float> f_lnw(lnw.begin(), lnw.end()), f_lnb(lnb.begin(), lnb.end());
+    std::vector<float> f_low(low.begin(), low.end()), f_lob(lob.begin(), lob.end());
+    std::vector<float> proj4((size_t)cz * c * 4), wo_t((size_t)c * cz), wg_t((size_t)cz * cz);
+    for (int d = 0; d < cz; ++d)
+        for (int ch = 0; ch < c; ++ch) {
+            float* q = &proj4[((size_t)d * c + ch) * 4];
+            q[0] = (float)wa[(size_t)ch * cz + d];
+            q[1] = (float)wga[(size_t)ch * cz + d];
+            q[2] = (float)wb[(size_t)ch * cz + d];
+            q[3] = (float)wgb[(size_t)ch * cz + d];
+        }
+    for (int d = 0; d < cz; ++d)
+        for (int ch = 0; ch < c; ++ch) wo_t[(size_t)ch * cz + d] = (float)wo[(size_t)d * c + ch];
+    for (int d = 0; d < cz; ++d)
+        for (int e2 = 0; e2 < cz; ++e2) wg_t[(size_t)e2 * cz + d] = (float)wg[(size_t)d * cz + e2];
+
+    if (!rc) rc = upload(h, &h->w.ln_in_w, f_lnw, s);
+    if (!rc) rc = upload(h, &h->w.ln_in_b, f_lnb, s);
+    if (!rc) rc = upload(h, &h->w.ln_out_w, f_low, s);
+    if (!rc) rc = upload(h, &h->w.ln_out_b, f_lob, s);
+    if (!rc) rc = upload(h, &h->w.proj4, proj4, s);
+    if (!rc) rc = upload(h, &h->w.wo_t, wo_t, s);
+    if (!rc) rc = upload(h, &h->w.wg_t, wg_t, s);
+
+    if (!rc && p->dtype == TRI_MUL_BF16) {
+        // MFMA operand copies: projection rows grouped per 32 hidden channels
+        // (W_a, W_ga, W_b, W_gb blocks), then W_o and W_g rows.
+        std::vector<uint16_t> pb((size_t)4 * c * cz), eb((size_t)2 * cz * 128);
+        for (int g = 0; g < c / 32; ++g)
+            for (int m = 0; m < 4; ++m)
+                for (int r = 0; r < 32; ++r) {
+                    const std::vector<double>& src = m == 0 ? wa : m == 1 ? wga : m == 2 ? wb : wgb;
+                    const size_t row = (size_t)g * 128 + m * 32 + r;
+                    for (int d = 0; d < cz; ++d) pb[row * cz + d] = to_bf16_exact(src[(size_t)(g * 32 + r) * cz + d]);
+                }
+        for (int d = 0; d < cz; ++d)
+            for (int k = 0; k < 128; ++k) {
+                eb[(size_t)d * 128 + k] = to_bf16_exact(wo[(size_t)d * c + k]);
+                eb[(size_t)(cz + d) * 128 + k] = to_bf16_exact(wg[(size_t)d * cz + k]);
+            }
+        if (!rc) rc = upload(h, &h->w.proj_bf, pb, s);
+        if (!rc) rc = upload(h, &h->w.epi_bf, eb, s);
+    }
+    if (!rc) {
+        e = hipStreamSynchronize(s);
+        if (e != hipSuccess) rc = hip_fail(e, "init synchronisation");
+    }
+    if (rc) {
+        free_all(h);
+        delete h;
+        return rc;
+    }
+    *out = h;
+    return ok();
+}
+
+int tri_mul_destroy(tri_mul_handle_t h) {
+    if (!h) return ok();
+    hipError_t e = hipDeviceSynchronize();
+    free_all(h);
+    delete h;
+    if (e != hipSuccess) return hip_fail(e, "destroy synchronisation");
+    return ok();
+}
+
+int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    const size_t panel = (size_t)h->c * N * panel_ld(N) * esize(h->dtype);
+    *bytes = 2 * round256(panel) + round256((size_t)h->c * N * N * 4);
+    return ok();
+}
+
+int tri_mul_outgoing(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, void* out, void* ws,
+                     size_t ws_bytes, void* stream) {
+    return run_full(h, z, mask, N, out, ws, ws_bytes, stream, 0);
+}
+
+int tri_mul_incoming(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, void* out, void* ws,
+                     size_t ws_bytes, void* stream) {
+    return run_full(h, z, mask, N, out, ws, ws_bytes, stream, 1);
+}
+
+int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, int32_t direction,
+                    void* a_panels, void* b_panels, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (direction != TRI_MUL_OUTGOING && direction != TRI_MUL_INCOMING) return fail(TRI_MUL_EINVAL, "bad direction %d", direction);
+    if (!z || !a_panels || !b_panels) return fail(TRI_MUL_EINVAL, "null z or panel pointer");
+    if (!aligned16(z) || !aligned16(a_panels) || !aligned16(b_panels)) return fail(TRI_MUL_EINVAL, "z and panels must be 16-byte aligned");
+    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, N, direction, a_panels, b_panels, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
+    return ok();
+}
+
+int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_panels, int64_t N, float* c_out,
+                     void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!a_panels || !b_panels || !c_out) return fail(TRI_MUL_EINVAL, "null panel or output pointer");
+    if (!aligned16(a_panels) || !aligned16(b_panels) || !aligned16(c_out)) return fail(TRI_MUL_EINVAL, "panels and output must be 16-byte aligned");
+    if (h->dtype == TRI_MUL_BF16 && (N % 8) != 0)
+        return fail(TRI_MUL_EINVAL, "bf16 contraction needs N %% 8 == 0 for 16-byte aligned rows (N = %lld)", (long long)N);
+    hipError_t e = trimul::launch_contract(h->dtype, a_panels, b_panels, c_out, N, N, N, N, N, N, N * N, N * N, N * N, h->c, 0,
+                                           nullptr, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    return ok();
+}
+
+int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z, const uint8_t* mask, int64_t N, void* out,
+                     void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!c_in || !z || !out) return fail(TRI_MUL_EINVAL, "null C, z or out pointer");
+    if (!aligned16(c_in) || !aligned16(z) || !aligned16(out)) return fail(TRI_MUL_EINVAL, "C, z and out must be 16-byte aligned");
+    trimul::EpilogueArgs ea{c_in, N, N * N, z, mask, 0, 0, N, N, out};
+    hipError_t e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    return ok();
+}
+
+int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                             const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                             void* out_tile, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (!v) return fail(TRI_MUL_EINVAL, "null view");
+    if (!a_panel || !b_panel || !acc) return fail(TRI_MUL_EINVAL, "null panel or accumulator pointer");
+    if (v->n_total < 1 || v->rows < 1 || v->cols < 1 || v->klen < 1) return fail(TRI_MUL_EINVAL, "empty or negative view sizes");
+    if (v->row0 < 0 || v->col0 < 0 || v->k0 < 0 || v->row0 + v->rows > v->n_total || v->col0 + v->cols > v->n_total ||
+        v->k0 + v->klen > v->n_total)
+        return fail(TRI_MUL_EINVAL, "view ranges exceed n_total = %lld", (long long)v->n_total);
+    if (v->rows > kMaxN || v->cols > kMaxN || v->klen > kMaxN)
+        return fail(TRI_MUL_EUNSUPPORTED, "tile sides and k-panel length are limited to %lld", (long long)kMaxN);
+    if (v->ld_a < v->klen || v->ld_b < v->klen || (v->ld_a % 8) || (v->ld_b % 8))
+        return fail(TRI_MUL_EINVAL, "ld_a / ld_b must be >= klen and multiples of 8");
+    if (v->k_count < 1 || v->k_index < 0 || v->k_index >= v->k_count) return fail(TRI_MUL_EINVAL, "bad k_index %d / k_count %d", v->k_index, v->k_count);
+    if (!aligned16(a_panel) || !aligned16(b_panel) || !aligned16(acc)) return fail(TRI_MUL_EINVAL, "panels and accumulator must be 16-byte aligned");
+    const bool last = v->k_index == v->k_count - 1;
+    if (last) {
+        if (!z_tile || !out_tile) return fail(TRI_MUL_EINVAL, "the last k-panel needs z_tile and out_tile");
+        if (!aligned16(z_tile) || !aligned16(out_tile)) return fail(TRI_MUL_EINVAL, "z_tile and out_tile must be 16-byte aligned");
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t sA = v->rows * v->ld_a, sB = v->cols * v->ld_b, sC = v->rows * v->cols;
+    hipError_t e = trimul::launch_contract(h->dtype, a_panel, b_panel, acc, v->rows, v->cols, v->klen, v->ld_a, v->ld_b,
+                                           v->cols, sA, sB, sC, h->c, v->k_index > 0, mask ? mask + v->k0 : nullptr, s);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    if (last) {
+        trimul::EpilogueArgs ea{acc, v->cols, sC, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
+        e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    }
+    return ok();
+}
+
+}  // extern "C"

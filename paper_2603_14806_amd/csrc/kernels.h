@@ -1,0 +1,54 @@
+// Host-side launchers of the triangle-multiplication kernels.  Each returns
+// hipSuccess or the error hipGetLastError() reported right after the launch.
+// Shapes are validated by the C-ABI layer before these are called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace trimul {
+
+// Repacked, device-resident layer parameters (owned by the handle).
+struct DeviceWeights {
+    // fp32 copies used by the VALU kernels (both storage types)
+    float* ln_in_w = nullptr;   // [c_z]
+    float* ln_in_b = nullptr;   // [c_z]
+    float* ln_out_w = nullptr;  // [c]
+    float* ln_out_b = nullptr;  // [c]
+    float* proj4 = nullptr;     // [c_z][c][4]: (W_a, W_ga, W_b, W_gb)[c][d] at [d][c][*]
+    float* wo_t = nullptr;      // [c][c_z]:   W_o[d][c] at [c][d]
+    float* wg_t = nullptr;      // [c_z][c_z]: W_g[d][e] at [e][d]
+    // bf16 copies used by the MFMA kernels (bf16 storage only)
+    uint16_t* proj_bf = nullptr;  // [4*c][c_z]: rows ordered per 32-channel group g:
+                                  // W_a[g], W_ga[g], W_b[g], W_gb[g] (32 rows each)
+    uint16_t* epi_bf = nullptr;   // [2*c_z][128]: W_o rows then W_g rows
+    float eps = 1e-5f;
+};
+
+struct EpilogueArgs {
+    const float* C;      // [c][rows][ldc] fp32 contraction result
+    int64_t ldc;         // row stride of C (elements)
+    int64_t sc;          // channel stride of C (elements)
+    const void* z;       // [rows][cols][c_z] pair tensor (same tile as C)
+    const uint8_t* mask; // token mask over global indices, or null
+    int64_t row0, col0;  // global token index of tile row 0 / column 0
+    int64_t rows, cols;
+    void* out;           // [rows][cols][c_z]
+};
+
+// K1: LN_in + gated projections + pair mask -> channel-major A, B [c][N][ld]
+// (row stride ld >= N elements; columns N..ld-1 are left untouched).
+hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
+                          int64_t N, int64_t ld, int incoming, void* A, void* B, hipStream_t s);
+
+// K2: C[b] (+)= A[b] * diag(kmask) * B[b]^T, A [b][M][lda], B [b][N][ldb], C [b][M][ldc].
+hipError_t launch_contract(int dtype, const void* A, const void* B, float* C, int64_t M, int64_t N,
+                           int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA, int64_t sB,
+                           int64_t sC, int batch, int accumulate, const uint8_t* kmask,
+                           hipStream_t s);
+
+// K3: LN_out + output projection + sigmoid gate + pair mask -> out [rows][cols][c_z].
+hipError_t launch_epilogue(int dtype, int out_dtype, const DeviceWeights& w, const EpilogueArgs& a,
+                           hipStream_t s);
+
+}  // namespace trimul

@@ -1,0 +1,222 @@
+"""Thin Python binding of libtrimul.so (the C ABI in include/tri_mul.h).
+
+Argument marshalling only: every step of the update runs in the library's HIP
+kernels.  PyTorch provides device memory and streams.  The functions keep the
+C names; TriMul is a small convenience wrapper that owns a handle.
+"""
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtrimul.so")
+
+TRI_MUL_OK, TRI_MUL_EINVAL, TRI_MUL_EUNSUPPORTED, TRI_MUL_ENOMEM, TRI_MUL_EHIP = 0, -1, -2, -3, -4
+TRI_MUL_F32, TRI_MUL_BF16 = 0, 1
+TRI_MUL_OUTGOING, TRI_MUL_INCOMING = 0, 1
+DTYPE_CODE = {"f32": TRI_MUL_F32, "bf16": TRI_MUL_BF16}
+TORCH_DTYPE = {TRI_MUL_F32: torch.float32, TRI_MUL_BF16: torch.bfloat16}
+WEIGHT_FIELDS = ("ln_in_w", "ln_in_b", "w_a", "w_ga", "w_b", "w_gb", "w_g", "ln_out_w", "ln_out_b", "w_o")
+
+_vp = ctypes.c_void_p
+_i32, _i64 = ctypes.c_int32, ctypes.c_int64
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("c_z", _i32), ("c", _i32), ("dtype", _i32), ("out_dtype", _i32), ("ln_eps", ctypes.c_float)] + \
+               [(name, _vp) for name in WEIGHT_FIELDS]
+
+
+class BlockView(ctypes.Structure):
+    _fields_ = [("n_total", _i64), ("row0", _i64), ("col0", _i64), ("rows", _i64), ("cols", _i64),
+                ("k0", _i64), ("klen", _i64), ("ld_a", _i64), ("ld_b", _i64),
+                ("k_index", _i32), ("k_count", _i32)]
+
+
+# name -> (restype, argtypes); the same order and meaning as include/tri_mul.h
+SIGNATURES = {
+    "tri_mul_init": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.POINTER(Params), _vp]),
+    "tri_mul_destroy": (ctypes.c_int, [_vp]),
+    "tri_mul_last_error": (ctypes.c_char_p, []),
+    "tri_mul_workspace_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_outgoing": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_incoming": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_block_accumulate": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
+    "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
+    "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
+}
+
+_lib = None
+
+
+class TriMulError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"tri_mul error {code}: {msg}")
+        self.code = code
+
+
+def lib():
+    """Load libtrimul.so from the package directory (it must have been built:
+    python -m paper_2603_14806_amd.build).  There is no fallback."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2603_14806_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def last_error():
+    return lib().tri_mul_last_error().decode()
+
+
+def _check(rc):
+    if rc != TRI_MUL_OK:
+        raise TriMulError(rc, last_error())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        return t                       # already an address (int) or None
+    if t.device.type != "cuda":
+        raise ValueError("tensors passed to the library must live on the GPU")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+# ---------------------------------------------------------------- C names
+
+def tri_mul_init(weights, dtype="bf16", out_dtype="f32", eps=1e-5, c_z=128, c=128, stream=None):
+    """weights: dict of device tensors (WEIGHT_FIELDS) in the storage dtype."""
+    p = Params(c_z, c, DTYPE_CODE[dtype], DTYPE_CODE[out_dtype], eps,
+               *[_ptr(weights[n]) for n in WEIGHT_FIELDS])
+    h = _vp()
+    _check(lib().tri_mul_init(ctypes.byref(h), ctypes.byref(p), _stream(stream)))
+    return h
+
+
+def tri_mul_destroy(h):
+    _check(lib().tri_mul_destroy(h))
+
+
+def tri_mul_workspace_size(h, N):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_workspace_size(h, N, ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_outgoing(h, z, mask, N, out, ws, ws_bytes, stream=None):
+    _check(lib().tri_mul_outgoing(h, _ptr(z), _ptr(mask), N, _ptr(out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def tri_mul_incoming(h, z, mask, N, out, ws, ws_bytes, stream=None):
+    _check(lib().tri_mul_incoming(h, _ptr(z), _ptr(mask), N, _ptr(out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def tri_mul_block_accumulate(h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream=None):
+    _check(lib().tri_mul_block_accumulate(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(acc),
+                                          _ptr(mask), _ptr(z_tile), _ptr(out_tile), _stream(stream)))
+
+
+def tri_mul_project(h, z, mask, N, direction, a_panels, b_panels, stream=None):
+    _check(lib().tri_mul_project(h, _ptr(z), _ptr(mask), N, direction, _ptr(a_panels), _ptr(b_panels),
+                                 _stream(stream)))
+
+
+def tri_mul_contract(h, a_panels, b_panels, N, c_out, stream=None):
+    _check(lib().tri_mul_contract(h, _ptr(a_panels), _ptr(b_panels), N, _ptr(c_out), _stream(stream)))
+
+
+def tri_mul_epilogue(h, c_in, z, mask, N, out, stream=None):
+    _check(lib().tri_mul_epilogue(h, _ptr(c_in), _ptr(z), _ptr(mask), N, _ptr(out), _stream(stream)))
+
+
+# ---------------------------------------------------------------- wrapper
+
+class TriMul:
+    """Owns a handle and allocates outputs / workspace with torch."""
+
+    def __init__(self, weights, dtype="bf16", out_dtype="f32", eps=1e-5, device="cuda", stream=None):
+        self.dtype, self.out_dtype = dtype, out_dtype
+        self.device = torch.device(device)
+        wd = {k: v.to(self.device, TORCH_DTYPE[DTYPE_CODE[dtype]]).contiguous() for k, v in weights.items()}
+        self.h = tri_mul_init(wd, dtype, out_dtype, eps, stream=stream)
+        torch.cuda.synchronize(self.device)
+        self._ws = None
+
+    def close(self):
+        if self.h:
+            tri_mul_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace(self, N):
+        need = tri_mul_workspace_size(self.h, N)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = None
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        return self._ws, need
+
+    def _out(self, N, out):
+        if out is None:
+            out = torch.empty((N, N, 128), dtype=TORCH_DTYPE[DTYPE_CODE[self.out_dtype]], device=self.device)
+        return out
+
+    def outgoing(self, z, mask=None, out=None, stream=None):
+        N = z.shape[0]
+        out = self._out(N, out)
+        ws, need = self.workspace(N)
+        tri_mul_outgoing(self.h, z, mask, N, out, ws, need, stream)
+        return out
+
+    def incoming(self, z, mask=None, out=None, stream=None):
+        N = z.shape[0]
+        out = self._out(N, out)
+        ws, need = self.workspace(N)
+        tri_mul_incoming(self.h, z, mask, N, out, ws, need, stream)
+        return out
+
+    def __call__(self, z, mask=None, direction="outgoing", out=None, stream=None):
+        return (self.outgoing if direction == "outgoing" else self.incoming)(z, mask, out, stream)
+
+    def project(self, z, mask=None, direction="outgoing", stream=None):
+        N = z.shape[0]
+        t = TORCH_DTYPE[DTYPE_CODE[self.dtype]]
+        A = torch.empty((128, N, N), dtype=t, device=self.device)
+        B = torch.empty((128, N, N), dtype=t, device=self.device)
+        tri_mul_project(self.h, z, mask, N, TRI_MUL_OUTGOING if direction == "outgoing" else TRI_MUL_INCOMING,
+                        A, B, stream)
+        return A, B
+
+    def contract(self, A, B, stream=None):
+        N = A.shape[1]
+        C = torch.empty((128, N, N), dtype=torch.float32, device=self.device)
+        tri_mul_contract(self.h, A, B, N, C, stream)
+        return C
+
+    def epilogue(self, C, z, mask=None, out=None, stream=None):
+        N = z.shape[0]
+        out = self._out(N, out)
+        tri_mul_epilogue(self.h, C, z, mask, N, out, stream)
+        return out
+
+    def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None):
+        tri_mul_block_accumulate(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream)

@@ -1,0 +1,241 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Sizes here let the oracle compute every output; they span several tiles of
+every kernel and ragged tails (N not a multiple of 8, 64 or 256)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_14806_amd import synth
+from paper_2603_14806_amd import trimul as T
+from tests.gpu_util import TOL, assert_close, errors, host, make_layer, needs_gpu, say
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+DIRS = ("outgoing", "incoming")
+
+
+# ------------------------------------------------------------ contraction
+
+@pytest.mark.parametrize("dtype,N", [("bf16", 64), ("bf16", 264), ("bf16", 520), ("f32", 65), ("f32", 130)])
+def test_contract_exact_on_integers(dtype, N):
+    """Small-integer operands make every product and partial sum exact in
+    fp32, so the kernel must match the fp64 contraction bit for bit (this also
+    pins the matrix-core operand and accumulator layouts)."""
+    say(f"contract exact dtype={dtype} N={N}")
+    layer, _ = make_layer(dtype)
+    g = torch.Generator().manual_seed(N)
+    A = torch.randint(-4, 5, (128, N, N), generator=g).to(synth.DTYPES[dtype])
+    B = torch.randint(-4, 5, (128, N, N), generator=g).to(synth.DTYPES[dtype])
+    C = layer.contract(A.cuda(), B.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.block_contract([host(A)], [host(B)], [np.ones(N)])    # [i][j][c]
+    np.testing.assert_array_equal(host(C).transpose(1, 2, 0), ref)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_block_accumulate_kmask_exact(dtype):
+    """Two k-panels with a token mask over k, ragged tile (300 x 200) and
+    panel lengths (130, 77) with padded row strides: overwrite on the first
+    panel, accumulate on the second, exact on integer data."""
+    say(f"block accumulate exact dtype={dtype}")
+    layer, W = make_layer(dtype)
+    rows, cols, n_total = 300, 200, 1000
+    g = torch.Generator().manual_seed(7)
+    mask = (torch.rand(n_total, generator=g) < 0.8).to(torch.uint8)
+    mask_d = mask.cuda()
+    acc = torch.full((128, rows, cols), float("nan"), device="cuda")
+    ks = [(100, 130), (500, 77)]
+    aps, bps = [], []
+    for idx, (k0, klen) in enumerate(ks):
+        ld = (klen + 7) // 8 * 8 + 8
+        ap = torch.randint(-4, 5, (128, rows, ld), generator=g).to(synth.DTYPES[dtype])
+        bp = torch.randint(-4, 5, (128, cols, ld), generator=g).to(synth.DTYPES[dtype])
+        # padding columns hold garbage the kernel must ignore
+        ap[:, :, klen:] = 1e4
+        bp[:, :, klen:] = float("nan")
+        aps.append(ap[:, :, :klen])
+        bps.append(bp[:, :, :klen])
+        v = T.BlockView(n_total, 700, 10, rows, cols, k0, klen, ld, ld, idx, 3)
+        layer.block_accumulate(v, ap.cuda(), bp.cuda(), acc, mask_d)
+    torch.cuda.synchronize()
+    ref = oracle.block_contract([host(a) for a in aps], [host(b) for b in bps],
+                                [host(mask[k0:k0 + kl]) for k0, kl in ks])
+    np.testing.assert_array_equal(host(acc).transpose(1, 2, 0), ref)
+
+
+# ------------------------------------------------------------- projection
+
+@pytest.mark.parametrize("dtype,N", [("bf16", 72), ("bf16", 300), ("f32", 65)])
+@pytest.mark.parametrize("direction", DIRS)
+def test_project_matches_oracle(dtype, N, direction):
+    say(f"project dtype={dtype} N={N} {direction}")
+    layer, W = make_layer(dtype, affine=True)
+    z = synth.pair_tensor(N, dtype=dtype)
+    mask = synth.random_mask(N, 0.85)
+    A, B = layer.project(z.cuda(), mask.cuda(), direction)
+    torch.cuda.synchronize()
+    rA, rB = oracle.projected_panels(z, mask, W, direction)
+    for got, ref, name in ((A, rA, "A"), (B, rB, "B")):
+        got = host(got)
+        if dtype == "f32":
+            mx, rel = errors(got, ref)
+            say(f"  {name}: max_abs={mx:.2e} rel_fro={rel:.2e}")
+            assert rel <= 1e-6
+        else:
+            # one rounding to bf16 (half an ulp, <= 2^-8 relative) plus fp32 error
+            bound = 2.0 ** -8 * np.abs(ref) + 1e-5
+            bad = np.abs(got - ref) > bound
+            assert not bad.any(), f"{name}: {bad.sum()} elements beyond one bf16 rounding"
+        # masked pairs are exact zeros
+        m = oracle.pair_mask(mask)
+        mm = m if direction == "outgoing" else m.T
+        assert np.all(got[:, mm == 0] == 0)
+
+
+# --------------------------------------------------------------- epilogue
+
+@pytest.mark.parametrize("dtype,out_dtype,N", [("bf16", "f32", 100), ("bf16", "bf16", 64), ("f32", "f32", 65)])
+def test_epilogue_matches_oracle(dtype, out_dtype, N):
+    say(f"epilogue dtype={dtype} out={out_dtype} N={N}")
+    layer, W = make_layer(dtype, out_dtype, affine=True)
+    z = synth.pair_tensor(N, dtype=dtype)
+    mask = synth.random_mask(N, 0.85, sub=3)
+    # contraction-like input: sums of ~N unit products have scale sqrt(N)
+    C = (torch.randn((128, N, N), generator=torch.Generator().manual_seed(5)) * np.sqrt(N)).float()
+    out = layer.epilogue(C.cuda(), z.cuda(), mask.cuda())
+    torch.cuda.synchronize()
+    m = oracle.pair_mask(mask)
+    _, _, gate = oracle.project(z, m, W)
+    ref = oracle.epilogue(host(C).transpose(1, 2, 0), gate, m, W)
+    tol_dtype = "f32" if (dtype == "f32" and out_dtype == "f32") else "bf16"
+    assert_close(host(out), ref, tol_dtype, "epilogue")
+    assert np.all(host(out)[m == 0] == 0)
+
+
+# ------------------------------------------------------- whole update, full
+
+def run_full(dtype, N, mask, direction, out_dtype="f32", affine=False, scale=None):
+    layer, W = make_layer(dtype, out_dtype, affine=affine)
+    z = synth.pair_tensor(N, dtype=dtype, scale=scale)
+    out = layer(z.cuda(), None if mask is None else mask.cuda(), direction)
+    torch.cuda.synchronize()
+    ref = oracle.tri_mul(z, np.ones(N) if mask is None else mask, W, direction)
+    return host(out), ref, layer, W, z
+
+
+@pytest.mark.parametrize("direction", DIRS)
+def test_config1_fp32_n64(direction):
+    say(f"config 1: fp32 N=64 {direction}")
+    got, ref, *_ = run_full("f32", 64, None, direction)
+    assert_close(got, ref, "f32", "c1")
+
+
+@pytest.mark.parametrize("direction", DIRS)
+def test_config2_bf16_n512_pad51(direction):
+    say(f"config 2: bf16 N=512, last 51 tokens padded, {direction}")
+    mask = synth.token_mask(512, 51)
+    got, ref, *_ = run_full("bf16", 512, mask, direction)
+    assert_close(got[:461, :461], ref[:461, :461], "bf16", "c2 unmasked block")
+    assert np.all(got[461:] == 0) and np.all(got[:, 461:] == 0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("N", [1, 2, 17, 63, 65, 257, 300])
+def test_ragged_sizes(dtype, N):
+    for direction in DIRS:
+        say(f"ragged dtype={dtype} N={N} {direction}")
+        mask = synth.random_mask(N, 0.8, sub=N)
+        if N > 1:
+            mask[0] = 1
+        got, ref, *_ = run_full(dtype, N, mask, direction, affine=True)
+        if not np.any(ref):
+            assert not np.any(got)
+        else:
+            assert_close(got, ref, dtype, f"N={N}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_all_masked_gives_zero(dtype):
+    N = 40
+    got, ref, *_ = run_full(dtype, N, torch.zeros(N, dtype=torch.uint8), "outgoing")
+    assert not np.any(got)
+
+
+def test_bf16_output_dtype():
+    say("bf16 output N=256")
+    got, ref, *_ = run_full("bf16", 256, None, "incoming", out_dtype="bf16")
+    assert_close(got, ref, "bf16", "bf16 out")
+
+
+# ------------------------------------------------------------ invariants
+
+@pytest.mark.parametrize("direction", DIRS)
+def test_padding_invariance_bitwise(direction):
+    N, n_real = 200, 170
+    layer, W = make_layer("bf16")
+    mask = synth.token_mask(N, N - n_real).cuda()
+    z = synth.pair_tensor(N, dtype="bf16").cuda()
+    z2 = z.clone()
+    z2[n_real:] = 100 * synth.pair_tensor(N, dtype="bf16", seed=5)[n_real:].cuda()
+    z2[:, n_real:] = -30 * synth.pair_tensor(N, dtype="bf16", seed=6)[:, n_real:].cuda()
+    o1 = layer(z, mask, direction).clone()
+    o2 = layer(z2, mask, direction)
+    torch.cuda.synchronize()
+    assert torch.equal(o1[:n_real, :n_real], o2[:n_real, :n_real])
+    assert not o2[n_real:].any() and not o2[:, n_real:].any()
+
+
+def test_deterministic_bitwise():
+    layer, W = make_layer("bf16")
+    z = synth.pair_tensor(320, dtype="bf16").cuda()
+    o1 = layer(z, None, "outgoing").clone()
+    o2 = layer(z, None, "outgoing")
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+
+
+def test_incoming_equals_transposed_outgoing_with_swapped_weights():
+    N = 192
+    Wt = synth.weights(128, 128, dtype="bf16")
+    Ws = dict(Wt, w_a=Wt["w_b"], w_ga=Wt["w_gb"], w_b=Wt["w_a"], w_gb=Wt["w_ga"])
+    la = T.TriMul(Wt, "bf16", "f32")
+    lb = T.TriMul(Ws, "bf16", "f32")
+    z = synth.pair_tensor(N, dtype="bf16").cuda()
+    inc = la.incoming(z)
+    out_t = lb.outgoing(z.transpose(0, 1).contiguous()).transpose(0, 1)
+    torch.cuda.synchronize()
+    mx, rel = errors(host(inc), host(out_t))
+    say(f"  swap relation: max_abs={mx:.2e} rel={rel:.2e}")
+    assert rel <= 1e-6
+
+
+# ------------------------------------------------------------- ABI errors
+
+def test_abi_errors_on_device():
+    layer, _ = make_layer("bf16")
+    N = 64
+    z = torch.zeros((N, N, 128), dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros((N, N, 128), dtype=torch.float32, device="cuda")
+    need = T.tri_mul_workspace_size(layer.h, N)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    L = T.lib()
+    s = torch.cuda.current_stream().cuda_stream
+    assert L.tri_mul_outgoing(layer.h, z.data_ptr(), None, N, out.data_ptr(), ws.data_ptr(), need - 1, s) == T.TRI_MUL_ENOMEM
+    assert L.tri_mul_outgoing(layer.h, z.data_ptr() + 2, None, N, out.data_ptr(), ws.data_ptr(), need, s) == T.TRI_MUL_EINVAL
+    assert L.tri_mul_outgoing(layer.h, z.data_ptr(), None, 0, out.data_ptr(), ws.data_ptr(), need, s) == T.TRI_MUL_EINVAL
+    assert L.tri_mul_outgoing(layer.h, z.data_ptr(), None, -5, out.data_ptr(), ws.data_ptr(), need, s) == T.TRI_MUL_EINVAL
+    assert L.tri_mul_project(layer.h, z.data_ptr(), None, N, 7, ws.data_ptr(), ws.data_ptr(), s) == T.TRI_MUL_EINVAL
+    v = T.BlockView(100, 90, 0, 20, 10, 0, 10, 16, 16, 0, 1)      # rows exceed n_total
+    assert L.tri_mul_block_accumulate(layer.h, v, ws.data_ptr(), ws.data_ptr(), ws.data_ptr(), None,
+                                      z.data_ptr(), out.data_ptr(), s) == T.TRI_MUL_EINVAL
+    v = T.BlockView(100, 0, 0, 20, 10, 0, 10, 12, 16, 0, 1)       # ld_a not a multiple of 8
+    assert L.tri_mul_block_accumulate(layer.h, v, ws.data_ptr(), ws.data_ptr(), ws.data_ptr(), None,
+                                      z.data_ptr(), out.data_ptr(), s) == T.TRI_MUL_EINVAL
+    v = T.BlockView(100, 0, 0, 20, 10, 0, 10, 16, 16, 0, 1)       # last panel without z_tile
+    assert L.tri_mul_block_accumulate(layer.h, v, ws.data_ptr(), ws.data_ptr(), ws.data_ptr(), None,
+                                      None, out.data_ptr(), s) == T.TRI_MUL_EINVAL
+    assert "z_tile" in T.last_error()
+    torch.cuda.synchronize()
+    layer.close()
+    layer.close()
