@@ -119,31 +119,48 @@ def epilogue(C, g, m_pairs, W, eps=EPS):
     return f64(m_pairs)[..., None] * f64(g) * y
 
 
+def take_pairs(z, rows=None, cols=None):
+    """z[rows][:, cols] as float64, converting only the selected pairs (z may be
+    a numpy array or a torch tensor, also on a device)."""
+    if hasattr(z, "detach"):
+        import torch
+        if rows is not None:
+            z = z[torch.as_tensor(rows, device=z.device)]
+        if cols is not None:
+            z = z[:, torch.as_tensor(cols, device=z.device)]
+        return f64(z)
+    z = np.asarray(z)
+    if rows is not None:
+        z = z[rows]
+    if cols is not None:
+        z = z[:, cols]
+    return f64(z)
+
+
 def tri_mul(z, mask, W, direction, rows=None, cols=None, eps=EPS):
     """The whole update for one pair tensor z [N][N][c_z] and token mask [N].
 
     direction: "outgoing" (Eq. 2) or "incoming" (Eq. 3).  rows / cols select
     the output pairs (index arrays; default all), so large N can be checked on
     a sample.  Returns out[len(rows)][len(cols)][c_z] in float64."""
-    z = f64(z)
     mask = f64(mask)
     N = z.shape[0]
     rows = np.arange(N) if rows is None else np.asarray(rows)
     cols = np.arange(N) if cols is None else np.asarray(cols)
     if direction == "outgoing":
         # a[i, k] for i in rows, all k; b[j, k] for j in cols, all k.
-        a, _, _ = project(z[rows], pair_mask(mask[rows], mask), W, eps)
-        _, b, _ = project(z[cols], pair_mask(mask[cols], mask), W, eps)
+        a, _, _ = project(take_pairs(z, rows), pair_mask(mask[rows], mask), W, eps)
+        _, b, _ = project(take_pairs(z, cols), pair_mask(mask[cols], mask), W, eps)
         C = contract_outgoing(a, b)
     elif direction == "incoming":
         # a[k, i] for i in rows, all k; b[k, j] for j in cols, all k.
-        a, _, _ = project(z[:, rows], pair_mask(mask, mask[rows]), W, eps)
-        _, b, _ = project(z[:, cols], pair_mask(mask, mask[cols]), W, eps)
+        a, _, _ = project(take_pairs(z, None, rows), pair_mask(mask, mask[rows]), W, eps)
+        _, b, _ = project(take_pairs(z, None, cols), pair_mask(mask, mask[cols]), W, eps)
         C = contract_incoming(a, b)
     else:
         raise ValueError(f"direction must be 'outgoing' or 'incoming', got {direction!r}")
     m_out = pair_mask(mask[rows], mask[cols])
-    _, _, g = project(z[np.ix_(rows, cols)], m_out, W, eps)
+    _, _, g = project(take_pairs(z, rows, cols), m_out, W, eps)
     return epilogue(C, g, m_out, W, eps)
 
 

@@ -157,9 +157,10 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
     h->w.eps = p->ln_eps;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = hipGetDevice(&h->device);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&h->w.cus, hipDeviceAttributeMultiprocessorCount, h->device);
     if (e != hipSuccess) {
         delete h;
-        return hip_fail(e, "hipGetDevice");
+        return hip_fail(e, "device query");
     }
 
     const int cz = p->c_z, c = p->c;

@@ -91,11 +91,218 @@ __global__ __launch_bounds__(256) void k3_epilogue_valu(
     }
 }
 
+
+// ------------------------------------------------------------ bf16 MFMA
+//
+// Persistent kernel, 4 waves, work unit = 32 consecutive pairs of one output
+// row.  Wave w owns output channels [32 w, 32 w + 32) of both W_o and W_g,
+// kept in VGPRs as the MFMA B operand; the activations (LN_out(C) split into
+// bf16 hi + lo, and bf16 LN_in(z) for the gate) are the A operand, so a lane
+// ends up holding 32 consecutive output channels of a pair and the stores are
+// 128-byte rows.
+constexpr int kP3 = 32;
+constexpr int kCsRow = kP3 + 4;     // C staging row stride (floats): conflict-free column reads
+constexpr int kYRow = 256;          // bytes of one bf16 activation row [128]
+
+__device__ __forceinline__ uint32_t yoff(int p, int chunk) {
+    return (uint32_t)(p * kYRow + ((chunk ^ (p & 15)) << 4));
+}
+
+template <typename TO, bool VEC_C>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
+void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* __restrict__ wepi,
+                      const float* __restrict__ lnin_w, const float* __restrict__ lnin_b,
+                      const float* __restrict__ lnout_w, const float* __restrict__ lnout_b, float eps) {
+    __shared__ __attribute__((aligned(16))) float cs[kCh * kCsRow];          // C as [c][p]
+    __shared__ __attribute__((aligned(16))) char ys[3][kP3 * kYRow];         // y_hi, y_lo, x_hi
+    __shared__ __attribute__((aligned(16))) float prm[4][128];               // LN gains and biases
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int lp = t >> 3, lq = t & 7;     // LayerNorms: pair lp, 8 lanes per pair
+    const bf16_t* z = static_cast<const bf16_t*>(a.z);
+    TO* out = static_cast<TO*>(a.out);
+
+    bf16x8_t wo[8], wg[8];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+        const size_t col = (size_t)ks * 16 + 8 * (lane >> 5);
+        wo[ks] = *reinterpret_cast<const bf16x8_t*>(wepi + (size_t)(w * 32 + (lane & 31)) * 128 + col);
+        wg[ks] = *reinterpret_cast<const bf16x8_t*>(wepi + (size_t)(128 + w * 32 + (lane & 31)) * 128 + col);
+    }
+    if (t < 128) {
+        prm[0][t] = lnout_w[t];
+        prm[1][t] = lnout_b[t];
+        prm[2][t] = lnin_w[t];
+        prm[3][t] = lnin_b[t];
+    }
+
+    // C loads: thread moves floats [4 cj, 4 cj + 4) of channel rows (t >> 3) + 32 s.
+    const int cj = t & 7;
+    auto load_c = [&](int64_t u, float4 (&cv)[4], uint4& z0, uint4& z1) {
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) cv[s2] = make_float4(0.f, 0.f, 0.f, 0.f);
+        z0 = z1 = make_uint4(0, 0, 0, 0);
+        if (u >= nunits) return;
+        const int64_t i = u / nchunk, j0 = (u - i * nchunk) * kP3;
+        const int np = (int)min<int64_t>(kP3, a.cols - j0);
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+            const float* src = a.C + (int64_t)((t >> 3) + 32 * s2) * a.sc + i * a.ldc + j0 + 4 * cj;
+            if (VEC_C && 4 * cj + 4 <= np) {
+                cv[s2] = *reinterpret_cast<const float4*>(src);
+            } else {
+                float e[4] = {0.f, 0.f, 0.f, 0.f};
+                for (int k = 0; k < 4; ++k)
+                    if (4 * cj + k < np) e[k] = src[k];
+                cv[s2] = make_float4(e[0], e[1], e[2], e[3]);
+            }
+        }
+        if (lp < np) {
+            const uint4* zs = reinterpret_cast<const uint4*>(z + ((i * a.cols) + j0 + lp) * kCz + 16 * lq);
+            z0 = zs[0];
+            z1 = zs[1];
+        }
+    };
+
+    float4 cc[4];
+    uint4 zc0, zc1;
+    load_c(blockIdx.x, cc, zc0, zc1);
+    for (int64_t u = blockIdx.x; u < nunits; u += gridDim.x) {
+        float4 cn[4];
+        uint4 zn0, zn1;
+        load_c(u + gridDim.x, cn, zn0, zn1);      // prefetch the next unit
+
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2)
+            *reinterpret_cast<float4*>(&cs[((t >> 3) + 32 * s2) * kCsRow + 4 * cj]) = cc[s2];
+        __syncthreads();
+
+        {   // LN_out over the 128 hidden channels of pair lp: lane lq holds c = lq + 8 i
+            float v[16];
+            float s1 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                v[i] = cs[(lq + 8 * i) * kCsRow + lp];
+                s1 += v[i];
+            }
+            s1 += __shfl_xor(s1, 1);
+            s1 += __shfl_xor(s1, 2);
+            s1 += __shfl_xor(s1, 4);
+            const float mu = s1 * (1.0f / kCh);
+            float q2 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                v[i] -= mu;
+                q2 += v[i] * v[i];
+            }
+            q2 += __shfl_xor(q2, 1);
+            q2 += __shfl_xor(q2, 2);
+            q2 += __shfl_xor(q2, 4);
+            const float rs = rsqrtf(q2 * (1.0f / kCh) + eps);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int c = lq + 8 * i;
+                const float y = v[i] * rs * prm[0][c] + prm[1][c];
+                const bf16_t h = f2bf(y);
+                const uint32_t o = yoff(lp, c >> 3) + 2 * (c & 7);
+                *reinterpret_cast<bf16_t*>(ys[0] + o) = h;
+                *reinterpret_cast<bf16_t*>(ys[1] + o) = f2bf(y - bf2f(h));
+            }
+        }
+        {   // LN_in over the 128 pair channels of pair lp: lane lq holds 16 lq .. 16 lq + 15
+            float v[16];
+            const uint32_t uu[8] = {zc0.x, zc0.y, zc0.z, zc0.w, zc1.x, zc1.y, zc1.z, zc1.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                v[2 * i] = __uint_as_float(uu[i] << 16);
+                v[2 * i + 1] = __uint_as_float(uu[i] & 0xffff0000u);
+            }
+            float s1 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s1 += v[i];
+            s1 += __shfl_xor(s1, 1);
+            s1 += __shfl_xor(s1, 2);
+            s1 += __shfl_xor(s1, 4);
+            const float mu = s1 * (1.0f / kCz);
+            float q2 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                v[i] -= mu;
+                q2 += v[i] * v[i];
+            }
+            q2 += __shfl_xor(q2, 1);
+            q2 += __shfl_xor(q2, 2);
+            q2 += __shfl_xor(q2, 4);
+            const float rs = rsqrtf(q2 * (1.0f / kCz) + eps);
+            uint32_t hx[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = 16 * lq + 2 * i;
+                const float x0 = v[2 * i] * rs * prm[2][c] + prm[3][c];
+                const float x1 = v[2 * i + 1] * rs * prm[2][c + 1] + prm[3][c + 1];
+                hx[i] = (uint32_t)f2bf(x0) | ((uint32_t)f2bf(x1) << 16);
+            }
+            *reinterpret_cast<uint4*>(ys[2] + yoff(lp, 2 * lq)) = make_uint4(hx[0], hx[1], hx[2], hx[3]);
+            *reinterpret_cast<uint4*>(ys[2] + yoff(lp, 2 * lq + 1)) = make_uint4(hx[4], hx[5], hx[6], hx[7]);
+        }
+        __syncthreads();
+
+        f32x16_t ay, ag;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ay[r] = ag[r] = 0.f;
+        const int ap = lane & 31;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            const uint32_t o = yoff(ap, 2 * ks + (lane >> 5));
+            const bf16x8_t yh = *reinterpret_cast<const bf16x8_t*>(ys[0] + o);
+            const bf16x8_t yl = *reinterpret_cast<const bf16x8_t*>(ys[1] + o);
+            const bf16x8_t xh = *reinterpret_cast<const bf16x8_t*>(ys[2] + o);
+            ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yh, wo[ks], ay, 0, 0, 0);
+            ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yl, wo[ks], ay, 0, 0, 0);
+            ag = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, wg[ks], ag, 0, 0, 0);
+        }
+
+        // Lane holds output channel 32 w + (lane & 31); register r holds pair
+        // 8 (r / 4) + 4 (lane / 32) + r % 4.
+        const int64_t i = u / nchunk, j0 = (u - i * nchunk) * kP3;
+        const int np = (int)min<int64_t>(kP3, a.cols - j0);
+        const bool mi = a.mask ? a.mask[a.row0 + i] != 0 : true;
+        const int d = w * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int p = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (p < np) {
+                const bool m = mi && (a.mask ? a.mask[a.col0 + j0 + p] != 0 : true);
+                Store<TO>::st(out + ((i * a.cols) + j0 + p) * kCz + d, m ? sigmoidf_(ag[r]) * ay[r] : 0.f);
+            }
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) cc[s2] = cn[s2];
+        zc0 = zn0;
+        zc1 = zn1;
+    }
+}
+
 template <typename T, typename TO>
 hipError_t launch_valu(const DeviceWeights& w, const EpilogueArgs& a, hipStream_t s) {
     const int64_t nchunk = (a.cols + kPairs - 1) / kPairs;
     hipLaunchKernelGGL((k3_epilogue_valu<T, TO>), dim3((unsigned)(a.rows * nchunk)), dim3(256), 0, s, a,
                        nchunk, w.wo_t, w.wg_t, w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
+    return hipGetLastError();
+}
+
+template <typename TO>
+hipError_t launch_mfma(const DeviceWeights& w, const EpilogueArgs& a, hipStream_t s) {
+    const int nchunk = (int)((a.cols + kP3 - 1) / kP3);
+    const int64_t nunits = a.rows * nchunk;
+    const int64_t cap = 2 * (int64_t)w.cus;
+    const unsigned g = (unsigned)(nunits < cap ? nunits : cap);
+    const bool vec = (a.ldc % 4) == 0 && (a.sc % 4) == 0 && (reinterpret_cast<uintptr_t>(a.C) & 15u) == 0;
+    if (vec)
+        hipLaunchKernelGGL((k3_epilogue_mfma<TO, true>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
+                           w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
+    else
+        hipLaunchKernelGGL((k3_epilogue_mfma<TO, false>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
+                           w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
     return hipGetLastError();
 }
 
@@ -105,7 +312,7 @@ hipError_t launch_epilogue(int dtype, int out_dtype, const DeviceWeights& w, con
                            hipStream_t s) {
     if (dtype == 0)
         return out_dtype == 0 ? launch_valu<float, float>(w, a, s) : launch_valu<float, bf16_t>(w, a, s);
-    return out_dtype == 0 ? launch_valu<bf16_t, float>(w, a, s) : launch_valu<bf16_t, bf16_t>(w, a, s);
+    return out_dtype == 0 ? launch_mfma<float>(w, a, s) : launch_mfma<bf16_t>(w, a, s);
 }
 
 }  // namespace trimul

@@ -23,6 +23,7 @@ struct DeviceWeights {
                                   // W_a[g], W_ga[g], W_b[g], W_gb[g] (32 rows each)
     uint16_t* epi_bf = nullptr;   // [2*c_z][128]: W_o rows then W_g rows
     float eps = 1e-5f;
+    int cus = 256;                // compute units of the device (persistent grids)
 };
 
 struct EpilogueArgs {

@@ -86,6 +86,180 @@ __global__ __launch_bounds__(256) void k1_project_valu(
     }
 }
 
+
+// ------------------------------------------------------------ bf16 MFMA
+//
+// Persistent kernel, 4 waves, work unit = line of 32 pairs.  Wave g owns
+// hidden channels [32 g, 32 g + 32): its 128 weight rows (W_a, W_ga, W_b,
+// W_gb of those channels) stay in VGPRs for the whole kernel as the MFMA A
+// operand, so the 4 x 32 outputs of a channel land in the same lane and
+// register and the gating is element-wise in registers.
+//
+// Precision: the LayerNormed input x (fp32) is split into x_hi = bf16(x) and
+// x_lo = bf16(x - x_hi); with exact bf16 weights W x_hi + W x_lo carries ~16
+// mantissa bits, so a and b see one bf16 rounding only (their store).
+constexpr int kP1 = 32;             // pairs per line
+constexpr int kXRow = kCz * 2;      // bytes of one bf16 x row (256)
+
+// x rows [p][128] bf16: 16-byte chunk q of row p lives at slot q ^ (p & 15).
+__device__ __forceinline__ uint32_t xoff(int p, int chunk) {
+    return (uint32_t)(p * kXRow + ((chunk ^ (p & 15)) << 4));
+}
+
+template <bool INCOMING>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
+void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ mask, int N, int64_t ld,
+                     int nchunk, int64_t nlines, const bf16_t* __restrict__ wproj,
+                     const float* __restrict__ lnw, const float* __restrict__ lnb, float eps,
+                     bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
+    __shared__ __attribute__((aligned(16))) char xs[2][kP1 * kXRow];   // x_hi, x_lo
+    __shared__ __attribute__((aligned(16))) float os[2][kCh][kP1];      // a, b as [c][p]
+    __shared__ __attribute__((aligned(16))) float gb[2][kCz];           // LayerNorm gain, bias
+    const int t = threadIdx.x, lane = t & 63, g = t >> 6;
+    const int lp = t >> 3, lq = t & 7;     // LayerNorm: pair lp, channels 16 lq .. 16 lq + 15
+
+    bf16x8_t w[4][8];
+#pragma unroll
+    for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks)
+            w[ob][ks] = *reinterpret_cast<const bf16x8_t*>(
+                wproj + (size_t)(g * 128 + ob * 32 + (lane & 31)) * kCz + ks * 16 + 8 * (lane >> 5));
+    if (t < kCz) {
+        gb[0][t] = lnw[t];
+        gb[1][t] = lnb[t];
+    }
+    __syncthreads();
+
+    auto pair_of = [&](int64_t line, int p, int64_t& r, int64_t& k0) -> int64_t {
+        r = line / nchunk;
+        k0 = (line - r * nchunk) * kP1;
+        return INCOMING ? (k0 + p) * N + r : r * N + k0 + p;
+    };
+    auto load_z = [&](int64_t line, uint4& z0, uint4& z1) {
+        z0 = z1 = make_uint4(0, 0, 0, 0);
+        if (line < nlines) {
+            int64_t r, k0;
+            const int64_t pr = pair_of(line, lp, r, k0);
+            if (k0 + lp < N) {
+                const uint4* src = reinterpret_cast<const uint4*>(z + pr * kCz + 16 * lq);
+                z0 = src[0];
+                z1 = src[1];
+            }
+        }
+    };
+
+    uint4 zc0, zc1;
+    load_z(blockIdx.x, zc0, zc1);
+    for (int64_t line = blockIdx.x; line < nlines; line += gridDim.x) {
+        uint4 zn0, zn1;
+        load_z(line + gridDim.x, zn0, zn1);      // prefetch the next line
+
+        // LayerNorm of pair lp over 128 channels (8 lanes x 16 channels).
+        float v[16];
+        {
+            const uint32_t u[8] = {zc0.x, zc0.y, zc0.z, zc0.w, zc1.x, zc1.y, zc1.z, zc1.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                v[2 * i] = __uint_as_float(u[i] << 16);
+                v[2 * i + 1] = __uint_as_float(u[i] & 0xffff0000u);
+            }
+        }
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s += v[i];
+        s += __shfl_xor(s, 1);
+        s += __shfl_xor(s, 2);
+        s += __shfl_xor(s, 4);
+        const float mu = s * (1.0f / kCz);
+        float q2 = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            v[i] -= mu;
+            q2 += v[i] * v[i];
+        }
+        q2 += __shfl_xor(q2, 1);
+        q2 += __shfl_xor(q2, 2);
+        q2 += __shfl_xor(q2, 4);
+        const float rs = rsqrtf(q2 * (1.0f / kCz) + eps);
+        float gam[16], bet[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float4 a4 = *reinterpret_cast<const float4*>(&gb[0][16 * lq + 4 * i]);
+            const float4 b4 = *reinterpret_cast<const float4*>(&gb[1][16 * lq + 4 * i]);
+            gam[4 * i] = a4.x; gam[4 * i + 1] = a4.y; gam[4 * i + 2] = a4.z; gam[4 * i + 3] = a4.w;
+            bet[4 * i] = b4.x; bet[4 * i + 1] = b4.y; bet[4 * i + 2] = b4.z; bet[4 * i + 3] = b4.w;
+        }
+        uint32_t hi[8], lo[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float x0 = v[2 * i] * rs * gam[2 * i] + bet[2 * i];
+            const float x1 = v[2 * i + 1] * rs * gam[2 * i + 1] + bet[2 * i + 1];
+            const bf16_t h0 = f2bf(x0), h1 = f2bf(x1);
+            hi[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            lo[i] = (uint32_t)f2bf(x0 - bf2f(h0)) | ((uint32_t)f2bf(x1 - bf2f(h1)) << 16);
+        }
+        *reinterpret_cast<uint4*>(xs[0] + xoff(lp, 2 * lq)) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        *reinterpret_cast<uint4*>(xs[0] + xoff(lp, 2 * lq + 1)) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+        *reinterpret_cast<uint4*>(xs[1] + xoff(lp, 2 * lq)) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+        *reinterpret_cast<uint4*>(xs[1] + xoff(lp, 2 * lq + 1)) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+        __syncthreads();
+
+        // [W_a; W_ga; W_b; W_gb](32 channels) x [x_hi + x_lo](32 pairs)
+        f32x16_t acc[4];
+#pragma unroll
+        for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[ob][r] = 0.f;
+        const int bp = lane & 31;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            const bf16x8_t xh = *reinterpret_cast<const bf16x8_t*>(xs[0] + xoff(bp, 2 * ks + (lane >> 5)));
+            const bf16x8_t xl = *reinterpret_cast<const bf16x8_t*>(xs[1] + xoff(bp, 2 * ks + (lane >> 5)));
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob) {
+                acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xh, acc[ob], 0, 0, 0);
+                acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xl, acc[ob], 0, 0, 0);
+            }
+        }
+
+        // Gate, mask, stage as [c][p] fp32.  Lane holds pair (lane & 31); in
+        // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.
+        int64_t r0, k0;
+        (void)pair_of(line, 0, r0, k0);
+        const int np = (int)min<int64_t>(kP1, N - k0);
+        const bool mrow = mask ? mask[r0] != 0 : true;
+        const bool mp = bp < np && mrow && (mask ? mask[k0 + bp] != 0 : true);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int c = g * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            os[0][c][bp] = mp ? sigmoidf_(acc[1][r]) * acc[0][r] : 0.f;
+            os[1][c][bp] = mp ? sigmoidf_(acc[3][r]) * acc[2][r] : 0.f;
+        }
+        __syncthreads();
+
+        // Channel-major stores: 8 lanes write the 32 pairs (64 bytes) of one row.
+        const int j = t & 7;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int R = (t >> 3) + 32 * i, ab = R >> 7, c = R & 127;
+            const float4 f = *reinterpret_cast<const float4*>(&os[ab][c][4 * j]);
+            bf16_t* dst = (ab ? B : A) + ((int64_t)c * N + r0) * ld + k0 + 4 * j;
+            if (4 * j + 4 <= np) {
+                const uint32_t lo2 = (uint32_t)f2bf(f.x) | ((uint32_t)f2bf(f.y) << 16);
+                const uint32_t hi2 = (uint32_t)f2bf(f.z) | ((uint32_t)f2bf(f.w) << 16);
+                *reinterpret_cast<uint2*>(dst) = make_uint2(lo2, hi2);
+            } else {
+                const float e[4] = {f.x, f.y, f.z, f.w};
+                for (int u = 0; u < 4; ++u)
+                    if (4 * j + u < np) dst[u] = f2bf(e[u]);
+            }
+        }
+        zc0 = zn0;
+        zc1 = zn1;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
@@ -101,12 +275,15 @@ hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, cons
             hipLaunchKernelGGL((k1_project_valu<float, false>), grid, block, 0, s, (const float*)z, mask, N,
                                ld, nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
     } else {
+        const int nch = (int)((N + kP1 - 1) / kP1);
+        const int64_t nlines = N * nch;
+        const unsigned g = (unsigned)(nlines < 2 * (int64_t)w.cus ? nlines : 2 * (int64_t)w.cus);
         if (incoming)
-            hipLaunchKernelGGL((k1_project_valu<bf16_t, true>), grid, block, 0, s, (const bf16_t*)z, mask, N,
-                               ld, nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
+            hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N, ld,
+                               nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
         else
-            hipLaunchKernelGGL((k1_project_valu<bf16_t, false>), grid, block, 0, s, (const bf16_t*)z, mask, N,
-                               ld, nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
+            hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N, ld,
+                               nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
     }
     return hipGetLastError();
 }

@@ -1,0 +1,147 @@
+"""GPU parity at the benchmark table's full sizes (N = 2048, N = 4096, and one
+3750 x 3750 tile of an 8 x 8 grid at N = 30000), checked on sampled outputs
+the oracle computes one by one, plus the block decomposition of the full
+update (each tile accumulated over k-panels equals the full result)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_14806_amd import synth
+from paper_2603_14806_amd import trimul as T
+from tests.gpu_util import assert_close, errors, host, make_layer, needs_gpu, say
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+DIRS = ("outgoing", "incoming")
+
+
+def sample_index(N, n_rand, seed, extra=()):
+    """Sorted unique indices: n_rand random ones plus edges and tile seams."""
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, 31, 32, 63, 64, 255, 256, N // 2, N - 2, N - 1] + list(extra)
+    idx = set(int(i) for i in fixed if 0 <= i < N)
+    idx |= set(rng.choice(N, size=n_rand, replace=False).tolist())
+    return np.array(sorted(idx))
+
+
+@pytest.mark.parametrize("direction", DIRS)
+def test_config3_bf16_n2048_channel_scaled(direction):
+    N = 2048
+    say(f"config 3: bf16 N={N}, per-channel scale U(0.5,2), {direction}")
+    layer, W = make_layer("bf16")
+    z = synth.pair_tensor(N, dtype="bf16", scale=synth.channel_scale(), device="cuda")
+    out = layer(z, None, direction)
+    torch.cuda.synchronize()
+    I, J = sample_index(N, 110, 1), sample_index(N, 110, 2)
+    ref = oracle.tri_mul(z, np.ones(N), W, direction, I, J)
+    got = host(out[torch.as_tensor(I, device="cuda")][:, torch.as_tensor(J, device="cuda")])
+    assert_close(got, ref, "bf16", f"c3 {len(I)}x{len(J)} sampled pairs")
+    # four full output rows
+    R = np.array([0, 777, 1500, N - 1])
+    ref_r = oracle.tri_mul(z, np.ones(N), W, direction, R, None)
+    assert_close(host(out[torch.as_tensor(R, device="cuda")]), ref_r, "bf16", "c3 full rows")
+
+
+@pytest.mark.parametrize("direction", DIRS)
+def test_config4_bf16_n4096(direction):
+    N = 4096
+    say(f"config 4: bf16 N={N}, {direction}")
+    layer, W = make_layer("bf16")
+    z = synth.pair_tensor(N, dtype="bf16", device="cuda")
+    out = layer(z, None, direction)
+    torch.cuda.synchronize()
+    I, J = sample_index(N, 117, 3), sample_index(N, 117, 4)
+    ref = oracle.tri_mul(z, np.ones(N), W, direction, I, J)
+    got = host(out[torch.as_tensor(I, device="cuda")][:, torch.as_tensor(J, device="cuda")])
+    assert_close(got, ref, "bf16", f"c4 {len(I)}x{len(J)} sampled pairs")
+    R = np.array([0, 2049, N - 1])
+    ref_r = oracle.tri_mul(z, np.ones(N), W, direction, R, None)
+    assert_close(host(out[torch.as_tensor(R, device="cuda")]), ref_r, "bf16", "c4 full rows")
+    del out, z
+    layer.close()
+    torch.cuda.empty_cache()
+
+
+def test_config5_tile_of_8x8_grid_n30000():
+    """Tile (7, 7) of an 8 x 8 grid at N = 30000: 3750 x 3750 outputs, 8
+    k-panels of 3750 tokens, the last 300 tokens padded (rows, columns and the
+    last k-panel).  Panels ~ N(0,1) bf16 generated on the device."""
+    n_total, g = 30000, 8
+    b = n_total // g
+    row0 = col0 = 7 * b
+    ld = (b + 7) // 8 * 8
+    say(f"config 5: tile ({row0},{col0}) {b}x{b}, 8 k-panels, ld={ld}")
+    layer, W = make_layer("bf16")
+    mask = synth.token_mask(n_total, 300, device="cuda")
+    aps, bps = [], []
+    for p in range(g):
+        aps.append(synth.pair_tensor(0, dtype="bf16", device="cuda", name="a_panel", seed=synth.SEED + p,
+                                     shape=(128, b, ld)))
+        bps.append(synth.pair_tensor(0, dtype="bf16", device="cuda", name="b_panel", seed=synth.SEED + p,
+                                     shape=(128, b, ld)))
+    z_tile = synth.pair_tensor(0, dtype="bf16", device="cuda", name="z_tile", shape=(b, b, 128))
+    acc = torch.empty((128, b, b), dtype=torch.float32, device="cuda")
+    out = torch.empty((b, b, 128), dtype=torch.float32, device="cuda")
+    for p in range(g):
+        v = T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g)
+        layer.block_accumulate(v, aps[p], bps[p], acc, mask, z_tile, out)
+    torch.cuda.synchronize()
+    say("  device run done")
+    I = sample_index(b, 114, 5, extra=(3449, 3450, 3451, 3700, 3748))
+    J = sample_index(b, 114, 6, extra=(3449, 3450, 3451, 3700, 3748))
+    It, Jt = torch.as_tensor(I, device="cuda"), torch.as_tensor(J, device="cuda")
+    mask_h = host(mask)
+    ref_C = oracle.block_contract([host(a[:, It, :b]) for a in aps], [host(bb[:, Jt, :b]) for bb in bps],
+                                  [mask_h[p * b:(p + 1) * b] for p in range(g)])
+    got_C = host(acc[:, It][:, :, Jt]).transpose(1, 2, 0)
+    mx, rel = errors(got_C, ref_C)
+    say(f"  accumulator: max_abs={mx:.3e} rel_fro={rel:.3e}")
+    assert rel <= 1e-5
+    ref = oracle.block_epilogue(ref_C, oracle.take_pairs(z_tile, I, J), mask_h[row0 + I], mask_h[col0 + J], W)
+    got = host(out[It][:, Jt])
+    valid = (mask_h[row0 + I] != 0)[:, None] & (mask_h[col0 + J] != 0)[None, :]
+    assert_close(got[valid], ref[valid], "bf16", "c5 sampled valid pairs")
+    assert np.all(got[~valid] == 0)
+
+
+@pytest.mark.parametrize("direction", DIRS)
+@pytest.mark.parametrize("N,g", [(1024, 2), (1024, 4), (1000, 4)])
+def test_block_decomposition_matches_full(direction, N, g):
+    """The one-GPU stand-in for the paper's ring: split the full problem into
+    a g x g grid of tiles, run each tile as g block_accumulate calls (one per
+    k-panel, as in the Cannon ring) from the same projected panels, and compare
+    with the single-call contraction and update."""
+    say(f"block == full: N={N} g={g} {direction}")
+    layer, W = make_layer("bf16")
+    z = synth.pair_tensor(N, dtype="bf16", device="cuda")
+    mask = synth.random_mask(N, 0.9, sub=g).cuda()
+    A, B = layer.project(z, mask, direction)
+    C_full = layer.contract(A, B)
+    out_full = layer.epilogue(C_full, z, mask)
+    out_dir = layer(z, mask, direction)
+    torch.cuda.synchronize()
+    assert torch.equal(out_full, out_dir), "stage calls differ from the one-call entry point"
+    bsz = N // g
+    ld = (bsz + 7) // 8 * 8
+    out_blk = torch.zeros_like(out_full)
+    for r in range(g):
+        for c in range(g):
+            r0, c0 = r * bsz, c * bsz
+            acc = torch.empty((128, bsz, bsz), dtype=torch.float32, device="cuda")
+            z_tile = z[r0:r0 + bsz, c0:c0 + bsz].contiguous()
+            o_tile = torch.empty((bsz, bsz, 128), dtype=torch.float32, device="cuda")
+            for p in range(g):
+                k0 = p * bsz
+                ap = torch.zeros((128, bsz, ld), dtype=torch.bfloat16, device="cuda")
+                bp = torch.zeros((128, bsz, ld), dtype=torch.bfloat16, device="cuda")
+                ap[:, :, :bsz] = A[:, r0:r0 + bsz, k0:k0 + bsz]
+                bp[:, :, :bsz] = B[:, c0:c0 + bsz, k0:k0 + bsz]
+                v = T.BlockView(N, r0, c0, bsz, bsz, k0, bsz, ld, ld, p, g)
+                layer.block_accumulate(v, ap, bp, acc, mask, z_tile, o_tile)
+            mx, rel = errors(host(acc), host(C_full[:, r0:r0 + bsz, c0:c0 + bsz]))
+            assert rel <= 1e-5, (r, c, rel)
+            out_blk[r0:r0 + bsz, c0:c0 + bsz] = o_tile
+    torch.cuda.synchronize()
+    mx, rel = errors(host(out_blk), host(out_full))
+    say(f"  tiles vs full: max_abs={mx:.2e} rel_fro={rel:.2e}")
+    assert rel <= 1e-5 and mx <= 1e-3

@@ -290,3 +290,13 @@ def test_block_kmask_drops_masked_k():
             for c in range(3):
                 s = sum(ap[0][c, i, k] * bp[0][c, j, k] for k in (0, 2, 3)) + ap[1][c, i, 5] * bp[1][c, j, 5]
                 assert abs(C[i, j, c] - s) < 1e-12
+
+
+def test_sampling_from_torch_input_matches_numpy():
+    N = 10
+    W = rand_weights(8, 8, seed=34)
+    z = rand_z(N, 8, seed=35)
+    rows, cols = np.array([9, 0, 4]), np.array([2, 7])
+    for d in DIRS:
+        np.testing.assert_array_equal(oracle.tri_mul(torch.from_numpy(z), np.ones(N), W, d, rows, cols),
+                                      oracle.tri_mul(z, np.ones(N), W, d, rows, cols))
