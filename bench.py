@@ -86,6 +86,8 @@ def main():
     ap.add_argument("--N", type=int, default=4096)
     ap.add_argument("--cpu-sample", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=float, default=0.0,
+                    help="GiB moved by one plain device-to-device copy before the run (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU path; "
@@ -100,6 +102,14 @@ def main():
     N = args.N
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration > 0:
+        n = int(args.copy_calibration * (1 << 30)) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy of {4 * n} bytes done", file=sys.stderr, flush=True)
+        del src, dst
     print(f"[bench] N={N} steps={args.steps} warmup={args.warmup}", file=sys.stderr, flush=True)
     layer = T.TriMul(synth.weights(dtype="bf16"), dtype="bf16", out_dtype="f32")
     z = synth.pair_tensor(N, dtype="bf16", device=dev)

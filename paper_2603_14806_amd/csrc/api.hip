@@ -122,7 +122,7 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, ld, incoming, A, B, s);
     if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
-    e = trimul::launch_contract(h->dtype, A, B, C, N, N, N, ld, ld, N, N * ld, N * ld, N * N, h->c, 0, nullptr, s);
+    e = trimul::launch_contract(h->dtype, A, B, C, N, N, N, ld, ld, N, N * ld, N * ld, N * N, h->c, 0, nullptr, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     trimul::EpilogueArgs ea{C, N, N * N, z, mask, 0, 0, N, N, out};
     e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
@@ -216,6 +216,10 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
     if (!rc) rc = upload(h, &h->w.wo_t, wo_t, s);
     if (!rc) rc = upload(h, &h->w.wg_t, wg_t, s);
 
+    if (!rc) {
+        std::vector<uint8_t> zeros((size_t)trimul::kMaxKPanel + 64, 0);
+        rc = upload(h, &h->w.kmask_pad, zeros, s);
+    }
     if (!rc && p->dtype == TRI_MUL_BF16) {
         // MFMA operand copies: projection rows grouped per 32 hidden channels
         // (W_a, W_ga, W_b, W_gb blocks), then W_o and W_g rows.
@@ -297,7 +301,7 @@ int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_pan
     if (h->dtype == TRI_MUL_BF16 && (N % 8) != 0)
         return fail(TRI_MUL_EINVAL, "bf16 contraction needs N %% 8 == 0 for 16-byte aligned rows (N = %lld)", (long long)N);
     hipError_t e = trimul::launch_contract(h->dtype, a_panels, b_panels, c_out, N, N, N, N, N, N, N * N, N * N, N * N, h->c, 0,
-                                           nullptr, static_cast<hipStream_t>(stream));
+                                           nullptr, h->w.cus, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     return ok();
 }
@@ -324,7 +328,7 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
     if (v->row0 < 0 || v->col0 < 0 || v->k0 < 0 || v->row0 + v->rows > v->n_total || v->col0 + v->cols > v->n_total ||
         v->k0 + v->klen > v->n_total)
         return fail(TRI_MUL_EINVAL, "view ranges exceed n_total = %lld", (long long)v->n_total);
-    if (v->rows > kMaxN || v->cols > kMaxN || v->klen > kMaxN)
+    if (v->rows > kMaxN || v->cols > kMaxN || v->klen > trimul::kMaxKPanel)
         return fail(TRI_MUL_EUNSUPPORTED, "tile sides and k-panel length are limited to %lld", (long long)kMaxN);
     if (v->ld_a < v->klen || v->ld_b < v->klen || (v->ld_a % 8) || (v->ld_b % 8))
         return fail(TRI_MUL_EINVAL, "ld_a / ld_b must be >= klen and multiples of 8");
@@ -337,8 +341,15 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int64_t sA = v->rows * v->ld_a, sB = v->cols * v->ld_b, sC = v->rows * v->cols;
-    hipError_t e = trimul::launch_contract(h->dtype, a_panel, b_panel, acc, v->rows, v->cols, v->klen, v->ld_a, v->ld_b,
-                                           v->cols, sA, sB, sC, h->c, v->k_index > 0, mask ? mask + v->k0 : nullptr, s);
+    hipError_t e = hipSuccess;
+    const uint8_t* kmask = nullptr;
+    if (mask) {   // the kernels read the k-range of the mask as a zero-padded 0/1 copy
+        e = trimul::launch_stage_kmask(mask + v->k0, v->klen, h->w.kmask_pad, s);
+        if (e != hipSuccess) return hip_fail(e, "mask staging kernel launch");
+        kmask = h->w.kmask_pad;
+    }
+    e = trimul::launch_contract(h->dtype, a_panel, b_panel, acc, v->rows, v->cols, v->klen, v->ld_a, v->ld_b,
+                                v->cols, sA, sB, sC, h->c, v->k_index > 0, kmask, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     if (last) {
         trimul::EpilogueArgs ea{acc, v->cols, sC, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};

@@ -16,40 +16,71 @@ namespace {
 
 // ---------------------------------------------------------------- bf16 MFMA
 //
-// Macro tile 256 x 256, k-tile 64, 256 threads = 4 waves in a 2 x 2 grid,
-// each wave owns a 128 x 128 sub-tile = 4 x 4 MFMA blocks of 32 x 32.
-// Two LDS stages of (A 256x64 + B 256x64) bf16 = 128 KB.  Each LDS row holds
-// 64 k-values = 8 chunks of 16 bytes; chunk q of row r is stored at slot
-// q ^ (r & 7) so that the 32 rows a wave reads at one k-chunk hit distinct
-// banks.
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int ROW_BYTES = BK * 2;               // 128
-constexpr int A_BYTES = BM * ROW_BYTES;         // 32 KB
-constexpr int B_BYTES = BN * ROW_BYTES;         // 32 KB
-constexpr int STAGE_BYTES = A_BYTES + B_BYTES;  // 64 KB
+// Persistent kernel: one work-group (4 waves) per CU, each looping over
+// 256 x 256 output tiles; a wave owns a 128 x 128 sub-tile = 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16.  The k loop runs in steps of 32 through a
+// 4-stage LDS ring (32 KB per stage) filled by direct-to-LDS buffer loads
+// (no VGPR staging), three steps ahead of the step being multiplied.  The
+// ring flows straight from one output tile into the next.
+//
+// Tile order: in round r the work-groups on XCD x take 32 consecutive
+// logical tiles, i.e. a 4 x 8 block of one channel, so the A row panels and B
+// column panels of a block are fetched once into that XCD's L2 and served to
+// the 32 CUs that share it.
+//
+// LDS layout of a stage: 256 A rows then 256 B rows of 32 bf16 (64 bytes =
+// 4 chunks of 16 bytes); chunk q of row r sits at slot q ^ ((r >> 2) & 3).
+// gfx950's LDS has 64 banks and serves a 16-byte-per-lane read 16 lanes per
+// cycle; the 16 rows those lanes read then cover all 64 banks.
+constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
+constexpr int ROWB = BK * 2;                    // 64 bytes per row per stage
+constexpr int A_ST = BM * ROWB;                 // 16 KB
+constexpr int B_ST = BN * ROWB;                 // 16 KB
+constexpr int MASK_ST = 4 * 256;                // per-wave k-mask bytes (KMASK only)
+constexpr int ST_BYTES = A_ST + B_ST + MASK_ST; // 33 KB
 
-__device__ __forceinline__ uint32_t lane_keep(bool v) { return v ? 0xffffu : 0u; }
+typedef int v4i_t __attribute__((ext_vector_type(4)));
 
-// Zero the bf16 elements of a 16-byte chunk whose k (k_base + e) is >= K or,
-// with a token mask, masked out.
-template <bool KMASK>
-__device__ __forceinline__ uint4 chunk_keep_mask(int k_base, int K, const uint8_t* __restrict__ kmask) {
-    uint32_t m[4];
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-        const int k = k_base + 2 * h;
-        bool v0 = k < K, v1 = k + 1 < K;
-        if (KMASK) {
-            v0 = v0 && kmask[k] != 0;
-            v1 = v1 && kmask[k + 1] != 0;
-        }
-        m[h] = lane_keep(v0) | (lane_keep(v1) << 16);
-    }
-    return make_uint4(m[0], m[1], m[2], m[3]);
+// Raw buffer descriptor (gfx9): base, stride 0, num_records = bytes, 32-bit
+// untyped access.  Loads at byte offsets >= bytes return zero.
+__device__ __forceinline__ v4i_t buffer_desc(const void* p, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    v4i_t r;
+    r.x = (int)(uint32_t)a;
+    r.y = (int)(uint32_t)(a >> 32);
+    r.z = (int)bytes;
+    r.w = 0x00020000;
+    return r;
 }
 
-__device__ __forceinline__ uint4 and4(uint4 a, uint4 b) {
-    return make_uint4(a.x & b.x, a.y & b.y, a.z & b.z, a.w & b.w);
+// Direct-to-LDS load: lane i writes `size` bytes at LDS address lds + size * i.
+// Issued as inline assembly so that the compiler does not serialise every
+// later LDS read behind it; the kernel waits on vmcnt itself.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_load16(v4i_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    lds = __builtin_amdgcn_readfirstlane(lds);
+    soff = __builtin_amdgcn_readfirstlane(soff);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+__device__ __forceinline__ void lds_load4(v4i_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    lds = __builtin_amdgcn_readfirstlane(lds);
+    soff = __builtin_amdgcn_readfirstlane(soff);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(p));
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
 template <bool KMASK>
@@ -58,132 +89,157 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
                       int M, int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB,
                       int64_t sC, int tiles_m, int tiles_n, int total, int accumulate,
                       const uint8_t* __restrict__ kmask) {
-    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_BYTES];
+    __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
+    constexpr int LOADS = 8 + (KMASK ? 1 : 0);  // buffer loads per wave per step
 
-    // Work-group -> tile.  Work-groups are dealt round-robin to the 8 XCDs;
-    // give each XCD a contiguous range of logical tiles so that the tiles
-    // sharing A row-panels and B column-panels meet in the same L2.
-    const int bid = blockIdx.x;
-    const int per = total >> 3;
-    const int logical = bid < (per << 3) ? (bid & 7) * per + (bid >> 3) : bid;
-    const int tiles = tiles_m * tiles_n;
-    const int ch = logical / tiles;
-    const int rem = logical - ch * tiles;
-    constexpr int G = 4;   // tile rows per group: 4 x tiles_n tiles walk down 4 A row-panels
-    const int gid = rem / (G * tiles_n);
-    const int first_m = gid * G;
-    const int gsz = min(tiles_m - first_m, G);
-    const int in_g = rem - gid * G * tiles_n;
-    const int tm = first_m + in_g % gsz;
-    const int tn = in_g / gsz;
-    const int m0 = tm * BM, n0 = tn * BN;
-
-    const bf16_t* Ab = A + ch * sA + (int64_t)m0 * lda;
-    const bf16_t* Bb = B + ch * sB + (int64_t)n0 * ldb;
-    // Rows past M (N) fall outside the resource and load as zero.
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(Ab, (uint32_t)(min(BM, M - m0) * lda * 2));
-    const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bb, (uint32_t)(min(BN, N - n0) * ldb * 2));
-
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-
-    // Global -> LDS copy: thread t moves chunk kc = t & 7 of rows (t >> 3) + 32 s.
-    const int row_l = t >> 3, kc = t & 7;
-    const uint32_t ga_off = (uint32_t)(row_l * lda + kc * 8) * 2;
-    const uint32_t gb_off = (uint32_t)(row_l * ldb + kc * 8) * 2;
-    const uint32_t ga_step = (uint32_t)(32 * lda * 2), gb_step = (uint32_t)(32 * ldb * 2);
-    const uint32_t lds_w = row_l * ROW_BYTES + ((kc ^ (row_l & 7)) << 4);
-
-    // LDS -> MFMA operands: lane reads row (lane & 31) of its 32-row block at
-    // k-chunk 2 s + (lane >> 5) of the k-tile.
-    uint32_t a_rd[4], b_rd[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        const uint32_t x = ((2 * s + (lane >> 5)) ^ (lane & 7)) << 4;
-        a_rd[s] = (wm * 128 + (lane & 31)) * ROW_BYTES + x;
-        b_rd[s] = A_BYTES + (wn * 128 + (lane & 31)) * ROW_BYTES + x;
-    }
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    uint4 sa[8], sb[8];
+    const int G = gridDim.x, wg = blockIdx.x;
+    const int perm = (G & 7) == 0 ? (wg & 7) * (G >> 3) + (wg >> 3) : wg;
+    const int my_tiles = perm < total ? (total - 1 - perm) / G + 1 : 0;
     const int nk = (K + BK - 1) / BK;
+    const int steps = my_tiles * nk;
+    const int tiles = tiles_m * tiles_n;
 
-    auto gload = [&](int kt) {
-        const uint32_t kb = (uint32_t)kt * ROW_BYTES;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            sa[s] = buf_load16(ra, ga_off + s * ga_step + kb);
-            sb[s] = buf_load16(rb, gb_off + s * gb_step + kb);
-        }
-        if (KMASK || kt * BK + BK > K) {
-            const uint4 keep = chunk_keep_mask<KMASK>(kt * BK + kc * 8, K, kmask);
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                sa[s] = and4(sa[s], keep);
-                sb[s] = and4(sb[s], keep);
-            }
-        }
-    };
-    auto lstore = [&](int stage) {
-        char* base = smem + stage * STAGE_BYTES + lds_w;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            *reinterpret_cast<uint4*>(base + s * 32 * ROW_BYTES) = sa[s];
-            *reinterpret_cast<uint4*>(base + A_BYTES + s * 32 * ROW_BYTES) = sb[s];
-        }
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // uniform per wave
+    const int wm = wave >> 1, wn = wave & 1;
+    const int rl = lane & 31, hi = lane >> 5;
+
+    auto decode = [&](int it, int& ch, int& m0, int& n0) {
+        const int L = it * G + perm;
+        ch = L / tiles;
+        const int rem = L - ch * tiles;
+        constexpr int GR = 4;   // tile rows per group: 32 consecutive tiles form a 4 x 8 block
+        const int gid = rem / (GR * tiles_n);
+        const int first_m = gid * GR;
+        const int gsz = min(tiles_m - first_m, GR);
+        const int in_g = rem - gid * GR * tiles_n;
+        m0 = (first_m + in_g % gsz) * BM;
+        n0 = (in_g / gsz) * BN;
     };
 
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
-        const char* st = smem + cur * STAGE_BYTES;
+    // Direct-to-LDS: lane i of a load writes 16 bytes at (instruction base + 16 i),
+    // i.e. row (i >> 2) of the 16 rows the instruction covers, slot (i & 3);
+    // it therefore fetches chunk (i & 3) ^ ((row >> 2) & 3) of that row.
+    const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
+    const uint32_t va = (uint32_t)(((wave * 64 + (lane >> 2)) * lda + lkc * 8) * 2);
+    const uint32_t vb = (uint32_t)(((wave * 64 + (lane >> 2)) * ldb + lkc * 8) * 2);
+    const uint32_t a_j = (uint32_t)(16 * lda * 2), b_j = (uint32_t)(16 * ldb * 2);
+    // kmask is the staged copy: 0/1 bytes, zero-padded to a multiple of 32
+    const v4i_t rmask = buffer_desc(kmask, KMASK ? (uint32_t)((K + 31) / 32 * 32) : 0u);
+
+    const uint32_t lds_base = lds_addr(smem);
+    auto issue = [&](int s) {
+        const int it = s / nk, kt = s - it * nk;
+        int ch, m0, n0;
+        decode(it, ch, m0, n0);
+        const v4i_t ra = buffer_desc(A + ch * sA + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 2));
+        const v4i_t rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
+        const uint32_t st = lds_base + (uint32_t)((s % STAGES) * ST_BYTES);
+        const uint32_t kb = (uint32_t)kt * ROWB;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            bf16x8_t af[4], bfr[4];
+        for (int j = 0; j < 4; ++j) lds_load16(ra, va, j * a_j + kb, st + (wave * 64 + 16 * j) * ROWB);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(st + a_rd[s] + i * 32 * ROW_BYTES);
+        for (int j = 0; j < 4; ++j) lds_load16(rb, vb, j * b_j + kb, st + A_ST + (wave * 64 + 16 * j) * ROWB);
+        if (KMASK)   // bytes [kt*32, kt*32 + 256) of the staged k-mask; past its end reads as 0
+            lds_load4(rmask, (uint32_t)lane * 4, (uint32_t)kt * BK, st + A_ST + B_ST + wave * 256);
+    };
+
+    const int q = (rl >> 2) & 3;
+    uint32_t rdA[2], rdB[2];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(st + b_rd[s] + j * 32 * ROW_BYTES);
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-        }
-        if (kt + 1 < nk) lstore(cur ^ 1);
-        __syncthreads();
+    for (int sub = 0; sub < 2; ++sub) {
+        const uint32_t x = (uint32_t)(((2 * sub + hi) ^ q) << 4);
+        rdA[sub] = (wm * 128 + rl) * ROWB + x;
+        rdB[sub] = A_ST + (wn * 128 + rl) * ROWB + x;
     }
 
-    // 32x32 accumulator layout: lane holds column (lane & 31) and, in register
-    // r, row 8 (r / 4) + 4 (lane / 32) + r % 4.
-    float* Cb = C + ch * sC;
-    const int lrow = 4 * (lane >> 5), lcol = lane & 31;
+    const int pro = min(STAGES - 1, steps);
+    for (int s = 0; s < pro; ++s) issue(s);
+
+    for (int it = 0; it < my_tiles; ++it) {
+        f32x16_t acc[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int col = n0 + wn * 128 + j * 32 + lcol;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + lrow + (r & 3);
-                if (row < M && col < N) {
-                    float* p = Cb + (int64_t)row * ldc + col;
-                    float v = acc[i][j][r];
-                    if (accumulate) v += *p;
-                    *p = v;
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+        for (int kt = 0; kt < nk; ++kt) {
+            const int s = it * nk + kt;
+            const int ahead = min(STAGES - 2, steps - 1 - s);   // later steps already in flight
+            if (ahead >= 2) wait_vmcnt<2 * LOADS>();
+            else if (ahead == 1) wait_vmcnt<LOADS>();
+            else wait_vmcnt<0>();
+            __syncthreads();
+            if (s + STAGES - 1 < steps) issue(s + STAGES - 1);
+
+            const char* st = smem + (s % STAGES) * ST_BYTES;
+            const bool tail = (kt == nk - 1) && (K % BK) != 0;
+#pragma unroll
+            for (int sub = 0; sub < 2; ++sub) {
+                bf16x8_t af[4], bfr[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(st + rdA[sub] + i * 32 * ROWB);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(st + rdB[sub] + j * 32 * ROWB);
+                if (KMASK || tail) {
+                    // zero the operands of k past K or masked out (0 * garbage must not reach the sum)
+                    const int kl = sub * 16 + hi * 8;   // lane's first k within the step
+                    uint32_t keep[4];
+                    if (KMASK) {
+                        const uint2 mb = *reinterpret_cast<const uint2*>(st + A_ST + B_ST + wave * 256 + kl);
+#pragma unroll
+                        for (int h = 0; h < 4; ++h) {
+                            const uint32_t b2 = h < 2 ? (mb.x >> (16 * h)) : (mb.y >> (16 * (h - 2)));
+                            keep[h] = ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
+                        }
+                    } else {
+                        const int kk = kt * BK + kl;
+#pragma unroll
+                        for (int h = 0; h < 4; ++h)
+                            keep[h] = (kk + 2 * h < K ? 0xffffu : 0u) | (kk + 2 * h + 1 < K ? 0xffff0000u : 0u);
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        uint4 u = __builtin_bit_cast(uint4, af[i]);
+                        u.x &= keep[0]; u.y &= keep[1]; u.z &= keep[2]; u.w &= keep[3];
+                        af[i] = __builtin_bit_cast(bf16x8_t, u);
+                        uint4 v = __builtin_bit_cast(uint4, bfr[i]);
+                        v.x &= keep[0]; v.y &= keep[1]; v.z &= keep[2]; v.w &= keep[3];
+                        bfr[i] = __builtin_bit_cast(bf16x8_t, v);
+                    }
                 }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
             }
         }
+
+        // 32x32 accumulator layout: lane holds column (lane & 31) and, in
+        // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.
+        int ch, m0, n0;
+        decode(it, ch, m0, n0);
+        const int row0 = m0 + wm * 128 + 4 * hi, col0 = n0 + wn * 128 + rl;
+        float* Cb = C + ch * sC + (int64_t)row0 * ldc + col0;
+        const bool full = m0 + BM <= M && n0 + BN <= N;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
+                    float* p = Cb + (int64_t)dr * ldc + j * 32;
+                    if (full || (row0 + dr < M && col0 + j * 32 < N)) {
+                        float v = acc[i][j][r];
+                        if (accumulate) v += *p;
+                        *p = v;
+                    }
+                }
+    }
 }
 
 // ---------------------------------------------------------------- fp32 VALU
@@ -237,11 +293,22 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
         }
 }
 
+__global__ void k_stage_kmask(const uint8_t* __restrict__ mask, int klen, int padded, uint8_t* __restrict__ dst) {
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < padded) dst[k] = (k < klen && mask[k] != 0) ? 1 : 0;
+}
+
 }  // namespace
+
+hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s) {
+    const int padded = (int)((klen + 31) / 32 * 32);
+    hipLaunchKernelGGL(k_stage_kmask, dim3((padded + 255) / 256), dim3(256), 0, s, mask, (int)klen, padded, dst);
+    return hipGetLastError();
+}
 
 hipError_t launch_contract(int dtype, const void* A, const void* B, float* C, int64_t M, int64_t N,
                            int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA, int64_t sB,
-                           int64_t sC, int batch, int accumulate, const uint8_t* kmask,
+                           int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,
                            hipStream_t s) {
     if (dtype == 0) {
         const dim3 grid((unsigned)((M + 63) / 64), (unsigned)((N + 63) / 64), (unsigned)batch);
@@ -251,12 +318,13 @@ hipError_t launch_contract(int dtype, const void* A, const void* B, float* C, in
     }
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
+    const int grid = total < cus ? total : cus;
     if (kmask)
-        hipLaunchKernelGGL((k2_contract_mfma<true>), dim3(total), dim3(256), 0, s, (const bf16_t*)A,
+        hipLaunchKernelGGL((k2_contract_mfma<true>), dim3(grid), dim3(256), 0, s, (const bf16_t*)A,
                            (const bf16_t*)B, C, (int)M, (int)N, (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC,
                            tm, tn, total, accumulate, kmask);
     else
-        hipLaunchKernelGGL((k2_contract_mfma<false>), dim3(total), dim3(256), 0, s, (const bf16_t*)A,
+        hipLaunchKernelGGL((k2_contract_mfma<false>), dim3(grid), dim3(256), 0, s, (const bf16_t*)A,
                            (const bf16_t*)B, C, (int)M, (int)N, (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC,
                            tm, tn, total, accumulate, kmask);
     return hipGetLastError();

@@ -24,7 +24,14 @@ struct DeviceWeights {
     uint16_t* epi_bf = nullptr;   // [2*c_z][128]: W_o rows then W_g rows
     float eps = 1e-5f;
     int cus = 256;                // compute units of the device (persistent grids)
+    uint8_t* kmask_pad = nullptr; // staging of a k-panel token mask, kMaxKPanel + 64 bytes
 };
+
+constexpr int64_t kMaxKPanel = 65536;   // longest k-panel of one block call
+
+// Copies mask[0, klen) into dst as 0/1 bytes and zero-fills dst up to the next
+// multiple of 32 (so the contraction can read whole 4-byte words of it).
+hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s);
 
 struct EpilogueArgs {
     const float* C;      // [c][rows][ldc] fp32 contraction result
@@ -45,7 +52,7 @@ hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, cons
 // K2: C[b] (+)= A[b] * diag(kmask) * B[b]^T, A [b][M][lda], B [b][N][ldb], C [b][M][ldc].
 hipError_t launch_contract(int dtype, const void* A, const void* B, float* C, int64_t M, int64_t N,
                            int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA, int64_t sB,
-                           int64_t sC, int batch, int accumulate, const uint8_t* kmask,
+                           int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,
                            hipStream_t s);
 
 // K3: LN_out + output projection + sigmoid gate + pair mask -> out [rows][cols][c_z].
