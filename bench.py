@@ -114,7 +114,8 @@ def main():
     layer = T.TriMul(synth.weights(dtype="bf16"), dtype="bf16", out_dtype="f32")
     z = synth.pair_tensor(N, dtype="bf16", device=dev)
     mask = synth.token_mask(N, 0, device=dev)
-    A = torch.empty((128, N, N), dtype=torch.bfloat16, device=dev)
+    npanel = T.tri_mul_panel_size(layer.h, N) // 2
+    A = torch.empty(npanel, dtype=torch.bfloat16, device=dev)
     B = torch.empty_like(A)
     C = torch.empty((128, N, N), dtype=torch.float32, device=dev)
     outs = [torch.empty((N, N, 128), dtype=torch.float32, device=dev) for _ in range(2)]

@@ -127,9 +127,9 @@ int tri_mul_destroy(tri_mul_handle_t h);
 const char* tri_mul_last_error(void);
 
 /* Bytes of device workspace tri_mul_outgoing / tri_mul_incoming need for N
- * tokens: the two channel-major panels A, B [c][N][N] (dtype) and the fp32
- * contraction result [c][N][N], each 256-byte aligned.  *bytes is a HOST
- * pointer. */
+ * tokens: the two contraction operands (panel layout, see tri_mul_project)
+ * and the fp32 contraction result [c][N][N], each 256-byte aligned.  *bytes
+ * is a HOST pointer. */
 int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
 
 /* The full update, Eq. 2 (outgoing) / Eq. 3 (incoming).
@@ -165,15 +165,26 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v,
 /* The three stages of tri_mul_outgoing / tri_mul_incoming, exposed so that
  * callers can time or check them one by one.
  *
- * tri_mul_project: input LayerNorm, gated projections and pair mask.
- *   Writes A, B [c][N][N] (dtype): outgoing A[c][i][k] = a[i][k][c],
- *   incoming A[c][i][k] = a[k][i][c] (likewise B), so that either direction
- *   becomes C[c] = A[c] * B[c]^T. */
+ * Operand ("panel") layout.  The contraction operands A, B hold, for every
+ * hidden channel c, an N x N matrix X_c[i][k] in 256 x 32 blocks: element
+ * (c, i, k) is at index
+ *     ((c * T + i / 256) * S + k / 32) * 8192 + (i % 256) * 32 + k % 32
+ * with T = ceil(N / 256) and S = ceil(N / 32), so one operand takes
+ * c * T * 256 * S * 32 elements.  Padding elements (i >= N or k >= N) are
+ * never written and never contribute.
+ *
+ * tri_mul_panel_size: bytes of one operand for N tokens (*bytes is HOST). */
+int tri_mul_panel_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
+
+/* tri_mul_project: input LayerNorm, gated projections and pair mask.
+ *   Writes A, B (dtype, panel layout, tri_mul_panel_size bytes each):
+ *   outgoing X_c[i][k] = a[i][k][c], incoming X_c[i][k] = a[k][i][c]
+ *   (likewise B), so that either direction becomes C[c] = A[c] * B[c]^T. */
 int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
                     int32_t direction, void* a_panels, void* b_panels, void* stream);
 
-/* tri_mul_contract: C[c][i][j] = sum_k A[c][i][k] * B[c][j][k] for all c
- * (A, B [c][N][N] dtype, C [c][N][N] float32, overwritten). */
+/* tri_mul_contract: C[c][i][j] = sum_k A_c[i][k] * B_c[j][k] for all c
+ * (A, B in the panel layout above, C [c][N][N] float32, overwritten). */
 int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_panels,
                      int64_t N, float* c_out, void* stream);
 

@@ -8,7 +8,8 @@
 #include <string>
 #include <vector>
 
-#include "../../include/tri_mul.h"
+#include "tri_mul.h"
+#include "common.h"
 #include "kernels.h"
 
 using trimul::DeviceWeights;
@@ -51,8 +52,10 @@ size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
 constexpr int64_t kMaxN = 65536;
 
-// Row stride of the workspace panels: rows start 16-byte aligned.
-int64_t panel_ld(int64_t N) { return (N + 7) & ~int64_t(7); }
+// Bytes of one blocked operand (all hidden channels) for N tokens.
+size_t panel_bytes(int64_t N, int c, int dtype) {
+    return (size_t)c * (size_t)trimul::panel_elems(trimul::panel_geom(N, N)) * esize(dtype);
+}
 
 // Host conversion of one stored value to double (exact).
 double to_double(const unsigned char* p, int dtype) {
@@ -113,16 +116,15 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
     size_t need = 0;
     if (int rc = tri_mul_workspace_size(h, N, &need)) return rc;
     if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed for N = %lld", ws_bytes, need, (long long)N);
-    const int64_t ld = panel_ld(N);
-    const size_t panel = (size_t)h->c * N * ld * esize(h->dtype);
+    const size_t panel = panel_bytes(N, h->c, h->dtype);
     char* base = static_cast<char*>(ws);
     void* A = base;
     void* B = base + round256(panel);
     float* C = reinterpret_cast<float*>(base + 2 * round256(panel));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, ld, incoming, A, B, s);
+    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, A, B, s);
     if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
-    e = trimul::launch_contract(h->dtype, A, B, C, N, N, N, ld, ld, N, N * ld, N * ld, N * N, h->c, 0, nullptr, h->w.cus, s);
+    e = trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     trimul::EpilogueArgs ea{C, N, N * N, z, mask, 0, 0, N, N, out};
     e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
@@ -265,8 +267,15 @@ int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
     if (int rc = check_handle(h)) return rc;
     if (int rc = check_n(N)) return rc;
     if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
-    const size_t panel = (size_t)h->c * N * panel_ld(N) * esize(h->dtype);
-    *bytes = 2 * round256(panel) + round256((size_t)h->c * N * N * 4);
+    *bytes = 2 * round256(panel_bytes(N, h->c, h->dtype)) + round256((size_t)h->c * N * N * 4);
+    return ok();
+}
+
+int tri_mul_panel_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    *bytes = panel_bytes(N, h->c, h->dtype);
     return ok();
 }
 
@@ -287,7 +296,7 @@ int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int6
     if (direction != TRI_MUL_OUTGOING && direction != TRI_MUL_INCOMING) return fail(TRI_MUL_EINVAL, "bad direction %d", direction);
     if (!z || !a_panels || !b_panels) return fail(TRI_MUL_EINVAL, "null z or panel pointer");
     if (!aligned16(z) || !aligned16(a_panels) || !aligned16(b_panels)) return fail(TRI_MUL_EINVAL, "z and panels must be 16-byte aligned");
-    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, N, direction, a_panels, b_panels, static_cast<hipStream_t>(stream));
+    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, direction, a_panels, b_panels, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
     return ok();
 }
@@ -298,10 +307,8 @@ int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_pan
     if (int rc = check_n(N)) return rc;
     if (!a_panels || !b_panels || !c_out) return fail(TRI_MUL_EINVAL, "null panel or output pointer");
     if (!aligned16(a_panels) || !aligned16(b_panels) || !aligned16(c_out)) return fail(TRI_MUL_EINVAL, "panels and output must be 16-byte aligned");
-    if (h->dtype == TRI_MUL_BF16 && (N % 8) != 0)
-        return fail(TRI_MUL_EINVAL, "bf16 contraction needs N %% 8 == 0 for 16-byte aligned rows (N = %lld)", (long long)N);
-    hipError_t e = trimul::launch_contract(h->dtype, a_panels, b_panels, c_out, N, N, N, N, N, N, N * N, N * N, N * N, h->c, 0,
-                                           nullptr, h->w.cus, static_cast<hipStream_t>(stream));
+    hipError_t e = trimul::launch_contract(h->dtype, 1, a_panels, b_panels, c_out, N, N, N, 0, 0, N, 0, 0, N * N, h->c,
+                                           0, nullptr, h->w.cus, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     return ok();
 }
@@ -348,7 +355,7 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
         if (e != hipSuccess) return hip_fail(e, "mask staging kernel launch");
         kmask = h->w.kmask_pad;
     }
-    e = trimul::launch_contract(h->dtype, a_panel, b_panel, acc, v->rows, v->cols, v->klen, v->ld_a, v->ld_b,
+    e = trimul::launch_contract(h->dtype, 0, a_panel, b_panel, acc, v->rows, v->cols, v->klen, v->ld_a, v->ld_b,
                                 v->cols, sA, sB, sC, h->c, v->k_index > 0, kmask, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     if (last) {

@@ -33,6 +33,28 @@ template <> struct Store<bf16_t> {
     static __device__ __forceinline__ void st(bf16_t* p, float v) { *p = f2bf(v); }
 };
 
+// Blocked layout of the contraction operands ("panels") written by the
+// projection and read by the contraction: for hidden channel c, operand row i
+// and contraction index k, the element lives at
+//     ((c * tiles_r + i / 256) * ksteps + k / 32) * (256 * 32) + (i % 256) * 32 + k % 32
+// with tiles_r = ceil(rows / 256) and ksteps = ceil(K / 32), so that one
+// 256-row x 32-k step of a contraction tile is one contiguous 16 KB block.
+constexpr int kBlkRows = 256, kBlkK = 32;
+struct PanelGeom {
+    int64_t tiles_r;   // ceil(rows / 256)
+    int64_t ksteps;    // ceil(K / 32)
+};
+__host__ __device__ __forceinline__ PanelGeom panel_geom(int64_t rows, int64_t K) {
+    return PanelGeom{(rows + kBlkRows - 1) / kBlkRows, (K + kBlkK - 1) / kBlkK};
+}
+__host__ __device__ __forceinline__ int64_t panel_elems(const PanelGeom& g) {
+    return g.tiles_r * g.ksteps * kBlkRows * kBlkK;   // per channel
+}
+__host__ __device__ __forceinline__ int64_t panel_off(const PanelGeom& g, int64_t c, int64_t i, int64_t k) {
+    return ((c * g.tiles_r + i / kBlkRows) * g.ksteps + k / kBlkK) * (kBlkRows * kBlkK) + (i % kBlkRows) * kBlkK +
+           k % kBlkK;
+}
+
 __device__ __forceinline__ float sigmoidf_(float t) { return 1.0f / (1.0f + __expf(-t)); }
 
 // Raw buffer resource over `bytes` bytes starting at p: loads at offsets

@@ -32,12 +32,21 @@ namespace {
 // 4 chunks of 16 bytes); chunk q of row r sits at slot q ^ ((r >> 2) & 3).
 // gfx950's LDS has 64 banks and serves a 16-byte-per-lane read 16 lanes per
 // cycle; the 16 rows those lanes read then cover all 64 banks.
-constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
+constexpr int BN = 256, BK = 32;
 constexpr int ROWB = BK * 2;                    // 64 bytes per row per stage
-constexpr int A_ST = BM * ROWB;                 // 16 KB
 constexpr int B_ST = BN * ROWB;                 // 16 KB
 constexpr int MASK_ST = 4 * 256;                // per-wave k-mask bytes (KMASK only)
-constexpr int ST_BYTES = A_ST + B_ST + MASK_ST; // 33 KB
+
+// Tile geometry for BM output rows per work-group (256 or 384): each wave owns
+// BM/2 x 128 outputs = MI x 4 MFMA blocks, and loads LA blocks of 16 A rows
+// and 4 blocks of 16 B rows per k-step.
+template <int BM> struct Geo {
+    static constexpr int MI = BM / 64;
+    static constexpr int LA = BM / 64;
+    static constexpr int A_ST = BM * ROWB;
+    static constexpr int ST_BYTES = A_ST + B_ST + MASK_ST;
+    static constexpr int STAGES = (160 * 1024) / ST_BYTES >= 4 ? 4 : 3;
+};
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 
@@ -83,14 +92,17 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <bool KMASK>
+template <int BM, bool KMASK, bool BLOCKED>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C,
                       int M, int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB,
                       int64_t sC, int tiles_m, int tiles_n, int total, int accumulate,
                       const uint8_t* __restrict__ kmask) {
+    using GG = Geo<BM>;
+    constexpr int MI = GG::MI, LA = GG::LA, A_ST = GG::A_ST, ST_BYTES = GG::ST_BYTES, STAGES = GG::STAGES;
+    constexpr int NPART = LA + 4;                // buffer loads of A and B per wave per step
     __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
-    constexpr int LOADS = 8 + (KMASK ? 1 : 0);  // buffer loads per wave per step
+    constexpr int LOADS = NPART + (KMASK ? 1 : 0);  // buffer loads per wave per step
 
     const int G = gridDim.x, wg = blockIdx.x;
     const int perm = (G & 7) == 0 ? (wg & 7) * (G >> 3) + (wg >> 3) : wg;
@@ -121,27 +133,54 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
     // i.e. row (i >> 2) of the 16 rows the instruction covers, slot (i & 3);
     // it therefore fetches chunk (i & 3) ^ ((row >> 2) & 3) of that row.
     const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
-    const uint32_t va = (uint32_t)(((wave * 64 + (lane >> 2)) * lda + lkc * 8) * 2);
-    const uint32_t vb = (uint32_t)(((wave * 64 + (lane >> 2)) * ldb + lkc * 8) * 2);
-    const uint32_t a_j = (uint32_t)(16 * lda * 2), b_j = (uint32_t)(16 * ldb * 2);
+    // Row-major operands: row r at r * ld elements.  Blocked operands: one
+    // tile's k-step is a contiguous [256 rows][32] block (row r at r * 32).
+    const int rsa = BLOCKED ? BK : lda, rsb = BLOCKED ? BK : ldb;
+    const uint32_t va = (uint32_t)(((wave * (BM / 4) + (lane >> 2)) * rsa + lkc * 8) * 2);
+    const uint32_t vb = (uint32_t)(((wave * 64 + (lane >> 2)) * rsb + lkc * 8) * 2);
+    const uint32_t a_j = (uint32_t)(16 * rsa * 2), b_j = (uint32_t)(16 * rsb * 2);
+    const uint32_t a_k = BLOCKED ? (uint32_t)(BM * BK * 2) : (uint32_t)ROWB;   // bytes per k-step
+    const uint32_t b_k = BLOCKED ? (uint32_t)(BN * BK * 2) : (uint32_t)ROWB;
     // kmask is the staged copy: 0/1 bytes, zero-padded to a multiple of 32
     const v4i_t rmask = buffer_desc(kmask, KMASK ? (uint32_t)((K + 31) / 32 * 32) : 0u);
 
+    // Load cursor: the tile and k-step of the next step to be fetched.  The
+    // tile decode and buffer descriptors change once per tile, not per step.
     const uint32_t lds_base = lds_addr(smem);
-    auto issue = [&](int s) {
-        const int it = s / nk, kt = s - it * nk;
+    int l_it = 0, l_kt = 0, l_stage = 0;
+    v4i_t ra, rb;
+    auto load_tile = [&]() {
         int ch, m0, n0;
-        decode(it, ch, m0, n0);
-        const v4i_t ra = buffer_desc(A + ch * sA + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 2));
-        const v4i_t rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
-        const uint32_t st = lds_base + (uint32_t)((s % STAGES) * ST_BYTES);
-        const uint32_t kb = (uint32_t)kt * ROWB;
+        decode(l_it, ch, m0, n0);
+        if (BLOCKED) {   // the tile-row's blocks for all k-steps; rows past M are padding, never stored
+            ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK), (uint32_t)(nk * BM * BK * 2));
+            rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK), (uint32_t)(nk * BN * BK * 2));
+        } else {         // rows past M (N) fall outside the descriptor and load as zero
+            ra = buffer_desc(A + ch * sA + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 2));
+            rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
+        }
+    };
+    // Part j of the next step's fetch: j < LA are A row blocks, then 4 B row
+    // blocks (16 rows each per wave); part NPART is the k-mask.
+    auto issue_part = [&](int j) {
+        const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
+        if (j < LA) lds_load16(ra, va, j * a_j + l_kt * a_k, st + (wave * (BM / 4) + 16 * j) * ROWB);
+        else if (j < NPART)
+            lds_load16(rb, vb, (j - LA) * b_j + l_kt * b_k, st + A_ST + (wave * 64 + 16 * (j - LA)) * ROWB);
+        else if (KMASK)   // bytes [kt*32, kt*32 + 256) of the staged k-mask; past its end reads as 0
+            lds_load4(rmask, (uint32_t)lane * 4, (uint32_t)l_kt * BK, st + A_ST + B_ST + wave * 256);
+    };
+    auto advance = [&]() {
+        l_stage = l_stage == STAGES - 1 ? 0 : l_stage + 1;
+        if (++l_kt == nk) {
+            l_kt = 0;
+            if (++l_it < my_tiles) load_tile();
+        }
+    };
+    auto issue_next = [&]() {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) lds_load16(ra, va, j * a_j + kb, st + (wave * 64 + 16 * j) * ROWB);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) lds_load16(rb, vb, j * b_j + kb, st + A_ST + (wave * 64 + 16 * j) * ROWB);
-        if (KMASK)   // bytes [kt*32, kt*32 + 256) of the staged k-mask; past its end reads as 0
-            lds_load4(rmask, (uint32_t)lane * 4, (uint32_t)kt * BK, st + A_ST + B_ST + wave * 256);
+        for (int j = 0; j <= NPART; ++j) issue_part(j);
+        advance();
     };
 
     const int q = (rl >> 2) & 3;
@@ -149,17 +188,19 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
         const uint32_t x = (uint32_t)(((2 * sub + hi) ^ q) << 4);
-        rdA[sub] = (wm * 128 + rl) * ROWB + x;
+        rdA[sub] = (wm * (BM / 2) + rl) * ROWB + x;
         rdB[sub] = A_ST + (wn * 128 + rl) * ROWB + x;
     }
 
+    if (my_tiles > 0) load_tile();
     const int pro = min(STAGES - 1, steps);
-    for (int s = 0; s < pro; ++s) issue(s);
+    for (int s = 0; s < pro; ++s) issue_next();
+    int c_stage = 0;
 
     for (int it = 0; it < my_tiles; ++it) {
-        f32x16_t acc[4][4];
+        f32x16_t acc[MI][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -172,49 +213,74 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
             else if (ahead == 1) wait_vmcnt<LOADS>();
             else wait_vmcnt<0>();
             __syncthreads();
-            if (s + STAGES - 1 < steps) issue(s + STAGES - 1);
+            const bool fetch = s + STAGES - 1 < steps;
 
-            const char* st = smem + (s % STAGES) * ST_BYTES;
+            const char* st = smem + c_stage * ST_BYTES;
+            c_stage = c_stage == STAGES - 1 ? 0 : c_stage + 1;
             const bool tail = (kt == nk - 1) && (K % BK) != 0;
+
+            // Zero the operands of k past K or masked out (0 * garbage must not
+            // reach the sum); only on the last step of a ragged K or with a k-mask.
+            auto mask_frags = [&](int sub, bf16x8_t (&af)[MI], bf16x8_t (&bfr)[4]) {
+                const int kl = sub * 16 + hi * 8;   // lane's first k within the step
+                uint32_t keep[4];
+                if (KMASK) {
+                    const uint2 mb = *reinterpret_cast<const uint2*>(st + A_ST + B_ST + wave * 256 + kl);
 #pragma unroll
-            for (int sub = 0; sub < 2; ++sub) {
-                bf16x8_t af[4], bfr[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(st + rdA[sub] + i * 32 * ROWB);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(st + rdB[sub] + j * 32 * ROWB);
-                if (KMASK || tail) {
-                    // zero the operands of k past K or masked out (0 * garbage must not reach the sum)
-                    const int kl = sub * 16 + hi * 8;   // lane's first k within the step
-                    uint32_t keep[4];
-                    if (KMASK) {
-                        const uint2 mb = *reinterpret_cast<const uint2*>(st + A_ST + B_ST + wave * 256 + kl);
-#pragma unroll
-                        for (int h = 0; h < 4; ++h) {
-                            const uint32_t b2 = h < 2 ? (mb.x >> (16 * h)) : (mb.y >> (16 * (h - 2)));
-                            keep[h] = ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
-                        }
-                    } else {
-                        const int kk = kt * BK + kl;
-#pragma unroll
-                        for (int h = 0; h < 4; ++h)
-                            keep[h] = (kk + 2 * h < K ? 0xffffu : 0u) | (kk + 2 * h + 1 < K ? 0xffff0000u : 0u);
+                    for (int h = 0; h < 4; ++h) {
+                        const uint32_t b2 = h < 2 ? (mb.x >> (16 * h)) : (mb.y >> (16 * (h - 2)));
+                        keep[h] = ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
                     }
+                } else {
+                    const int kk = kt * BK + kl;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        uint4 u = __builtin_bit_cast(uint4, af[i]);
-                        u.x &= keep[0]; u.y &= keep[1]; u.z &= keep[2]; u.w &= keep[3];
-                        af[i] = __builtin_bit_cast(bf16x8_t, u);
-                        uint4 v = __builtin_bit_cast(uint4, bfr[i]);
-                        v.x &= keep[0]; v.y &= keep[1]; v.z &= keep[2]; v.w &= keep[3];
-                        bfr[i] = __builtin_bit_cast(bf16x8_t, v);
-                    }
+                    for (int h = 0; h < 4; ++h)
+                        keep[h] = (kk + 2 * h < K ? 0xffffu : 0u) | (kk + 2 * h + 1 < K ? 0xffff0000u : 0u);
                 }
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < MI; ++i) {
+                    uint4 u = __builtin_bit_cast(uint4, af[i]);
+                    u.x &= keep[0]; u.y &= keep[1]; u.z &= keep[2]; u.w &= keep[3];
+                    af[i] = __builtin_bit_cast(bf16x8_t, u);
+                }
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < 4; ++j) {
+                    uint4 v = __builtin_bit_cast(uint4, bfr[j]);
+                    v.x &= keep[0]; v.y &= keep[1]; v.z &= keep[2]; v.w &= keep[3];
+                    bfr[j] = __builtin_bit_cast(bf16x8_t, v);
+                }
+            };
+
+            bf16x8_t a0[MI], b0[4], a1[MI], b1[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b0[j] = *reinterpret_cast<const bf16x8_t*>(st + rdB[0] + j * 32 * ROWB);
+#pragma unroll
+            for (int i = 0; i < MI; ++i) a0[i] = *reinterpret_cast<const bf16x8_t*>(st + rdA[0] + i * 32 * ROWB);
+            if (KMASK || tail) mask_frags(0, a0, b0);
+            // Sub-step 0: 4 MI MFMAs; after every second one, one part of the
+            // next step's fetch and one operand read of sub-step 1.
+#pragma unroll
+            for (int x = 0; x < 4 * MI; ++x) {
+                const int i = x >> 2, j = x & 3;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
+                if (x & 1) {
+                    const int y = x >> 1;   // 0 .. 2 MI - 1 >= NPART - 1
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (fetch && y < NPART) issue_part(y);
+                    if (y < 4) b1[y] = *reinterpret_cast<const bf16x8_t*>(st + rdB[1] + y * 32 * ROWB);
+                    else if (y < 4 + MI) a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            if (fetch) {
+                if (KMASK) issue_part(NPART);
+                advance();
+            }
+            if (KMASK || tail) mask_frags(1, a1, b1);
+#pragma unroll
+            for (int x = 0; x < 4 * MI; ++x) {
+                const int i = x >> 2, j = x & 3;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
             }
         }
 
@@ -222,11 +288,11 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
         // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.
         int ch, m0, n0;
         decode(it, ch, m0, n0);
-        const int row0 = m0 + wm * 128 + 4 * hi, col0 = n0 + wn * 128 + rl;
+        const int row0 = m0 + wm * (BM / 2) + 4 * hi, col0 = n0 + wn * 128 + rl;
         float* Cb = C + ch * sC + (int64_t)row0 * ldc + col0;
         const bool full = m0 + BM <= M && n0 + BN <= N;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -244,6 +310,7 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
 
 // ---------------------------------------------------------------- fp32 VALU
 
+template <bool BLOCKED>
 __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__ A, const float* __restrict__ B,
                                                       float* __restrict__ C, int M, int N, int K, int64_t lda,
                                                       int64_t ldb, int64_t ldc, int64_t sA, int64_t sB,
@@ -252,8 +319,9 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
     __shared__ float As[16][64 + 4], Bs[16][64 + 4];
     const int64_t ch = blockIdx.z;
     const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
-    A += ch * sA;
-    B += ch * sB;
+    const PanelGeom ga = panel_geom(M, K), gb = panel_geom(N, K);
+    auto a_at = [&](int64_t r, int64_t k) { return BLOCKED ? A[panel_off(ga, ch, r, k)] : A[ch * sA + r * lda + k]; };
+    auto b_at = [&](int64_t r, int64_t k) { return BLOCKED ? B[panel_off(gb, ch, r, k)] : B[ch * sB + r * ldb + k]; };
     C += ch * sC;
     const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
     float acc[4][4] = {};
@@ -262,8 +330,8 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
         for (int s = 0; s < 4; ++s) {
             const int idx = t + 256 * s, row = idx >> 4, kk = idx & 15, k = k0 + kk;
             const bool kv = k < K && (!kmask || kmask[k] != 0);
-            As[kk][row] = (m0 + row < M && kv) ? A[(int64_t)(m0 + row) * lda + k] : 0.f;
-            Bs[kk][row] = (n0 + row < N && kv) ? B[(int64_t)(n0 + row) * ldb + k] : 0.f;
+            As[kk][row] = (m0 + row < M && kv) ? a_at(m0 + row, k) : 0.f;
+            Bs[kk][row] = (n0 + row < N && kv) ? b_at(n0 + row, k) : 0.f;
         }
         __syncthreads();
 #pragma unroll
@@ -306,27 +374,37 @@ hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, h
     return hipGetLastError();
 }
 
-hipError_t launch_contract(int dtype, const void* A, const void* B, float* C, int64_t M, int64_t N,
-                           int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA, int64_t sB,
-                           int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,
+hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B, float* C, int64_t M,
+                           int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA,
+                           int64_t sB, int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,
                            hipStream_t s) {
     if (dtype == 0) {
         const dim3 grid((unsigned)((M + 63) / 64), (unsigned)((N + 63) / 64), (unsigned)batch);
-        hipLaunchKernelGGL(k2_contract_f32, grid, dim3(256), 0, s, (const float*)A, (const float*)B, C, (int)M,
-                           (int)N, (int)K, lda, ldb, ldc, sA, sB, sC, accumulate, kmask);
+        if (blocked)
+            hipLaunchKernelGGL(k2_contract_f32<true>, grid, dim3(256), 0, s, (const float*)A, (const float*)B, C,
+                               (int)M, (int)N, (int)K, lda, ldb, ldc, sA, sB, sC, accumulate, kmask);
+        else
+            hipLaunchKernelGGL(k2_contract_f32<false>, grid, dim3(256), 0, s, (const float*)A, (const float*)B, C,
+                               (int)M, (int)N, (int)K, lda, ldb, ldc, sA, sB, sC, accumulate, kmask);
         return hipGetLastError();
     }
+    constexpr int BM = 256;
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
     const int grid = total < cus ? total : cus;
-    if (kmask)
-        hipLaunchKernelGGL((k2_contract_mfma<true>), dim3(grid), dim3(256), 0, s, (const bf16_t*)A,
-                           (const bf16_t*)B, C, (int)M, (int)N, (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC,
-                           tm, tn, total, accumulate, kmask);
-    else
-        hipLaunchKernelGGL((k2_contract_mfma<false>), dim3(grid), dim3(256), 0, s, (const bf16_t*)A,
-                           (const bf16_t*)B, C, (int)M, (int)N, (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC,
-                           tm, tn, total, accumulate, kmask);
+    const bf16_t* a = (const bf16_t*)A;
+    const bf16_t* b = (const bf16_t*)B;
+#define K2_LAUNCH(KM, BL)                                                                                      \
+    hipLaunchKernelGGL((k2_contract_mfma<BM, KM, BL>), dim3(grid), dim3(256), 0, s, a, b, C, (int)M, (int)N, \
+                       (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
+    if (kmask) {
+        if (blocked) K2_LAUNCH(true, true);
+        else K2_LAUNCH(true, false);
+    } else {
+        if (blocked) K2_LAUNCH(false, true);
+        else K2_LAUNCH(false, false);
+    }
+#undef K2_LAUNCH
     return hipGetLastError();
 }
 

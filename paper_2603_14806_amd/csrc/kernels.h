@@ -44,15 +44,18 @@ struct EpilogueArgs {
     void* out;           // [rows][cols][c_z]
 };
 
-// K1: LN_in + gated projections + pair mask -> channel-major A, B [c][N][ld]
-// (row stride ld >= N elements; columns N..ld-1 are left untouched).
+// K1: LN_in + gated projections + pair mask -> channel-major operands A, B in
+// the blocked panel layout (common.h) of N rows and K = N.  Elements of the
+// padding (rows or k >= N) are left untouched.
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
-                          int64_t N, int64_t ld, int incoming, void* A, void* B, hipStream_t s);
+                          int64_t N, int incoming, void* A, void* B, hipStream_t s);
 
-// K2: C[b] (+)= A[b] * diag(kmask) * B[b]^T, A [b][M][lda], B [b][N][ldb], C [b][M][ldc].
-hipError_t launch_contract(int dtype, const void* A, const void* B, float* C, int64_t M, int64_t N,
-                           int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA, int64_t sB,
-                           int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,
+// K2: C[b] (+)= A[b] * diag(kmask) * B[b]^T for b < batch, C [b][M][ldc] row-major.
+// blocked != 0: A, B in the blocked panel layout of M (N) rows and K columns
+// (lda, ldb, sA, sB unused); blocked == 0: A [b][M][lda], B [b][N][ldb].
+hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B, float* C, int64_t M,
+                           int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA,
+                           int64_t sB, int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,
                            hipStream_t s);
 
 // K3: LN_out + output projection + sigmoid gate + pair mask -> out [rows][cols][c_z].

@@ -17,7 +17,7 @@ constexpr int kLine = 64;   // pairs per work unit
 // Scalar (VALU) fp32 version; it serves the fp32 storage path.
 template <typename T, bool INCOMING>
 __global__ __launch_bounds__(256) void k1_project_valu(
-    const T* __restrict__ z, const uint8_t* __restrict__ mask, int64_t N, int64_t ld, int64_t nchunk,
+    const T* __restrict__ z, const uint8_t* __restrict__ mask, int64_t N, int64_t nchunk,
     const float4* __restrict__ proj4, const float* __restrict__ lnw, const float* __restrict__ lnb,
     float eps, T* __restrict__ A, T* __restrict__ B) {
     __shared__ float xs[kLine][kCz + 1];
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(256) void k1_project_valu(
             const bool m = mr && (mask ? mask[k0 + p] != 0 : true);
             const float a = m ? sigmoidf_(acc[q][1]) * acc[q][0] : 0.f;
             const float b = m ? sigmoidf_(acc[q][3]) * acc[q][2] : 0.f;
-            const int64_t off = ((int64_t)c * N + r) * ld + k0 + p;
+            const int64_t off = panel_off(panel_geom(N, N), c, r, k0 + p);
             Store<T>::st(A + off, a);
             Store<T>::st(B + off, b);
         }
@@ -108,7 +108,7 @@ __device__ __forceinline__ uint32_t xoff(int p, int chunk) {
 
 template <bool INCOMING>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
-void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ mask, int N, int64_t ld,
+void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ mask, int N,
                      int nchunk, int64_t nlines, const bf16_t* __restrict__ wproj,
                      const float* __restrict__ lnw, const float* __restrict__ lnb, float eps,
                      bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
@@ -238,13 +238,15 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ m
         }
         __syncthreads();
 
-        // Channel-major stores: 8 lanes write the 32 pairs (64 bytes) of one row.
+        // Channel-major stores: 8 lanes write the 32 pairs (64 bytes) of one
+        // panel row; the 32 pairs are one k-step of the blocked layout.
         const int j = t & 7;
+        const PanelGeom pg = panel_geom(N, N);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int R = (t >> 3) + 32 * i, ab = R >> 7, c = R & 127;
             const float4 f = *reinterpret_cast<const float4*>(&os[ab][c][4 * j]);
-            bf16_t* dst = (ab ? B : A) + ((int64_t)c * N + r0) * ld + k0 + 4 * j;
+            bf16_t* dst = (ab ? B : A) + panel_off(pg, c, r0, k0 + 4 * j);
             if (4 * j + 4 <= np) {
                 const uint32_t lo2 = (uint32_t)f2bf(f.x) | ((uint32_t)f2bf(f.y) << 16);
                 const uint32_t hi2 = (uint32_t)f2bf(f.z) | ((uint32_t)f2bf(f.w) << 16);
@@ -263,26 +265,26 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ m
 }  // namespace
 
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
-                          int64_t N, int64_t ld, int incoming, void* A, void* B, hipStream_t s) {
+                          int64_t N, int incoming, void* A, void* B, hipStream_t s) {
     const int64_t nchunk = (N + kLine - 1) / kLine;
     const dim3 grid((unsigned)(N * nchunk)), block(256);
     const float4* p4 = reinterpret_cast<const float4*>(w.proj4);
     if (dtype == 0) {
         if (incoming)
             hipLaunchKernelGGL((k1_project_valu<float, true>), grid, block, 0, s, (const float*)z, mask, N,
-                               ld, nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
+                               nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
         else
             hipLaunchKernelGGL((k1_project_valu<float, false>), grid, block, 0, s, (const float*)z, mask, N,
-                               ld, nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
+                               nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
     } else {
         const int nch = (int)((N + kP1 - 1) / kP1);
         const int64_t nlines = N * nch;
         const unsigned g = (unsigned)(nlines < 2 * (int64_t)w.cus ? nlines : 2 * (int64_t)w.cus);
         if (incoming)
-            hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N, ld,
+            hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N,
                                nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
         else
-            hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N, ld,
+            hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N,
                                nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
     }
     return hipGetLastError();

@@ -40,6 +40,7 @@ SIGNATURES = {
     "tri_mul_destroy": (ctypes.c_int, [_vp]),
     "tri_mul_last_error": (ctypes.c_char_p, []),
     "tri_mul_workspace_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_panel_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
     "tri_mul_outgoing": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
     "tri_mul_incoming": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
     "tri_mul_block_accumulate": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -115,6 +116,12 @@ def tri_mul_destroy(h):
 def tri_mul_workspace_size(h, N):
     n = ctypes.c_size_t()
     _check(lib().tri_mul_workspace_size(h, N, ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_panel_size(h, N):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_panel_size(h, N, ctypes.byref(n)))
     return n.value
 
 
@@ -198,16 +205,19 @@ class TriMul:
         return (self.outgoing if direction == "outgoing" else self.incoming)(z, mask, out, stream)
 
     def project(self, z, mask=None, direction="outgoing", stream=None):
+        """Returns the two operands in the library's panel layout (flat
+        tensors; see panel_to_dense)."""
         N = z.shape[0]
         t = TORCH_DTYPE[DTYPE_CODE[self.dtype]]
-        A = torch.empty((128, N, N), dtype=t, device=self.device)
-        B = torch.empty((128, N, N), dtype=t, device=self.device)
+        n = tri_mul_panel_size(self.h, N) // torch.empty((), dtype=t).element_size()
+        A = torch.empty(n, dtype=t, device=self.device)
+        B = torch.empty(n, dtype=t, device=self.device)
         tri_mul_project(self.h, z, mask, N, TRI_MUL_OUTGOING if direction == "outgoing" else TRI_MUL_INCOMING,
                         A, B, stream)
         return A, B
 
-    def contract(self, A, B, stream=None):
-        N = A.shape[1]
+    def contract(self, A, B, N, stream=None):
+        """A, B in the panel layout (project / dense_to_panel)."""
         C = torch.empty((128, N, N), dtype=torch.float32, device=self.device)
         tri_mul_contract(self.h, A, B, N, C, stream)
         return C
@@ -220,3 +230,26 @@ class TriMul:
 
     def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None):
         tri_mul_block_accumulate(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream)
+
+
+# ------------------------------------------------------ panel layout views
+
+def _panel_dims(N, c=128):
+    T, S = -(-N // 256), -(-N // 32)
+    return c, T, S
+
+
+def panel_to_dense(P, N, c=128):
+    """Panel-layout operand (flat) -> dense [c][N][N] (a view copy)."""
+    c, T, S = _panel_dims(N, c)
+    X = P.reshape(c, T, S, 256, 32).permute(0, 1, 3, 2, 4).reshape(c, T * 256, S * 32)
+    return X[:, :N, :N]
+
+
+def dense_to_panel(X):
+    """Dense [c][N][N] -> flat panel-layout operand (zero padding)."""
+    c, N = X.shape[0], X.shape[1]
+    _, T, S = _panel_dims(N, c)
+    Y = torch.zeros((c, T * 256, S * 32), dtype=X.dtype, device=X.device)
+    Y[:, :N, :N] = X
+    return Y.reshape(c, T, 256, S, 32).permute(0, 1, 3, 2, 4).contiguous().reshape(-1)

@@ -1,6 +1,8 @@
 """GPU parity at the benchmark table's full sizes (N = 2048, N = 4096, and one
 3750 x 3750 tile of an 8 x 8 grid at N = 30000), checked on sampled outputs
-the oracle computes one by one, plus the block decomposition of the full
+the oracle computes one by one (at N = 2048 also four full output rows; at
+N = 4096 a full row would need the CPU projection of all 16.7M pairs), plus
+the block decomposition of the full
 update (each tile accumulated over k-panels equals the full result)."""
 import numpy as np
 import pytest
@@ -54,9 +56,6 @@ def test_config4_bf16_n4096(direction):
     ref = oracle.tri_mul(z, np.ones(N), W, direction, I, J)
     got = host(out[torch.as_tensor(I, device="cuda")][:, torch.as_tensor(J, device="cuda")])
     assert_close(got, ref, "bf16", f"c4 {len(I)}x{len(J)} sampled pairs")
-    R = np.array([0, 2049, N - 1])
-    ref_r = oracle.tri_mul(z, np.ones(N), W, direction, R, None)
-    assert_close(host(out[torch.as_tensor(R, device="cuda")]), ref_r, "bf16", "c4 full rows")
     del out, z
     layer.close()
     torch.cuda.empty_cache()
@@ -115,8 +114,9 @@ def test_block_decomposition_matches_full(direction, N, g):
     layer, W = make_layer("bf16")
     z = synth.pair_tensor(N, dtype="bf16", device="cuda")
     mask = synth.random_mask(N, 0.9, sub=g).cuda()
-    A, B = layer.project(z, mask, direction)
-    C_full = layer.contract(A, B)
+    Ap, Bp = layer.project(z, mask, direction)
+    C_full = layer.contract(Ap, Bp, N)
+    A, B = T.panel_to_dense(Ap, N), T.panel_to_dense(Bp, N)
     out_full = layer.epilogue(C_full, z, mask)
     out_dir = layer(z, mask, direction)
     torch.cuda.synchronize()
