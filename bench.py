@@ -78,6 +78,22 @@ def cpu_baseline(N, sample):
             "sample_seconds": round(t3 - t0, 2)}
 
 
+def measured_traffic():
+    """HBM-side bytes per K2 launch from the committed rocprofv3 counter runs
+    (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known size),
+    valid only while the contraction kernel source is the one measured."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "k2_contract_traffic.json")))
+        csrc = os.path.join(ROOT, "paper_2603_14806_amd", "csrc")
+        src = open(os.path.join(csrc, "contract.hip"), "rb").read() + open(os.path.join(csrc, "common.h"), "rb").read()
+        if hashlib.sha256(src).hexdigest() == rec["source_sha256"]:
+            return rec["traffic_bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        pass
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,7 +208,7 @@ def main():
         },
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "k2_contract_mfma",
+                     "traffic": measured_traffic(), "kernel": "k2_contract_mfma",
                      "per_launch": f"2*N^3*c = {fl['contract']:.4e} flop (128 channels of one {N}^3 product)"},
         "cpu_baseline": None,
     }
