@@ -133,7 +133,7 @@ def main():
     npanel = T.tri_mul_panel_size(layer.h, N) // 2
     A = torch.empty(npanel, dtype=torch.bfloat16, device=dev)
     B = torch.empty_like(A)
-    C = torch.empty((128, N, N), dtype=torch.float32, device=dev)
+    C = torch.empty(N * (-(-N // 32) * 32) * 128, dtype=torch.float32, device=dev)   # result layout
     outs = [torch.empty((N, N, 128), dtype=torch.float32, device=dev) for _ in range(2)]
     stream = torch.cuda.current_stream()
     h = layer.h

@@ -128,8 +128,8 @@ const char* tri_mul_last_error(void);
 
 /* Bytes of device workspace tri_mul_outgoing / tri_mul_incoming need for N
  * tokens: the two contraction operands (panel layout, see tri_mul_project)
- * and the fp32 contraction result [c][N][N], each 256-byte aligned.  *bytes
- * is a HOST pointer. */
+ * and the fp32 contraction result (result layout, see tri_mul_contract), each
+ * 256-byte aligned.  *bytes is a HOST pointer. */
 int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
 
 /* The full update, Eq. 2 (outgoing) / Eq. 3 (incoming).
@@ -183,13 +183,17 @@ int tri_mul_panel_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
 int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
                     int32_t direction, void* a_panels, void* b_panels, void* stream);
 
-/* tri_mul_contract: C[c][i][j] = sum_k A_c[i][k] * B_c[j][k] for all c
- * (A, B in the panel layout above, C [c][N][N] float32, overwritten). */
+/* tri_mul_contract: C_c[i][j] = sum_k A_c[i][k] * B_c[j][k] for all c.
+ *   A, B in the panel layout above.  C (float32, overwritten) in the result
+ *   layout: element (channel ch, i, j) at ((i * J + j / 32) * c + ch) * 32 +
+ *   j % 32 with J = ceil(N / 32) -- the c channels of 32 consecutive pairs of
+ *   a row are one contiguous block; C takes N * J * 32 * c floats. */
 int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_panels,
                      int64_t N, float* c_out, void* stream);
 
-/* tri_mul_epilogue: out[i][j] = m_ij * sigmoid(W_g LN_in(z_ij)) * W_o LN_out(C[:, i, j])
- * (C [c][N][N] float32, z [N][N][c_z] dtype, out [N][N][c_z] out_dtype). */
+/* tri_mul_epilogue: out[i][j] = m_ij * sigmoid(W_g LN_in(z_ij)) * W_o LN_out(C_.[i][j])
+ * (C float32 in the result layout of tri_mul_contract, z [N][N][c_z] dtype,
+ * out [N][N][c_z] out_dtype). */
 int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z,
                      const uint8_t* mask, int64_t N, void* out, void* stream);
 

@@ -52,6 +52,9 @@ size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
 constexpr int64_t kMaxN = 65536;
 
+// Bytes of the fp32 contraction result in the pair-blocked layout.
+size_t result_bytes(int64_t N, int c) { return (size_t)N * (size_t)((N + 31) / 32 * 32) * (size_t)c * 4; }
+
 // Bytes of one blocked operand (all hidden channels) for N tokens.
 size_t panel_bytes(int64_t N, int c, int dtype) {
     return (size_t)c * (size_t)trimul::panel_elems(trimul::panel_geom(N, N)) * esize(dtype);
@@ -126,7 +129,7 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
     if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
     e = trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
-    trimul::EpilogueArgs ea{C, N, N * N, z, mask, 0, 0, N, N, out};
+    trimul::EpilogueArgs ea{C, 1, 0, 0, z, mask, 0, 0, N, N, out};
     e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
     if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
     return ok();
@@ -267,7 +270,7 @@ int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
     if (int rc = check_handle(h)) return rc;
     if (int rc = check_n(N)) return rc;
     if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
-    *bytes = 2 * round256(panel_bytes(N, h->c, h->dtype)) + round256((size_t)h->c * N * N * 4);
+    *bytes = 2 * round256(panel_bytes(N, h->c, h->dtype)) + round256(result_bytes(N, h->c));
     return ok();
 }
 
@@ -319,7 +322,7 @@ int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z, const
     if (int rc = check_n(N)) return rc;
     if (!c_in || !z || !out) return fail(TRI_MUL_EINVAL, "null C, z or out pointer");
     if (!aligned16(c_in) || !aligned16(z) || !aligned16(out)) return fail(TRI_MUL_EINVAL, "C, z and out must be 16-byte aligned");
-    trimul::EpilogueArgs ea{c_in, N, N * N, z, mask, 0, 0, N, N, out};
+    trimul::EpilogueArgs ea{c_in, 1, 0, 0, z, mask, 0, 0, N, N, out};
     hipError_t e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
     return ok();
@@ -359,7 +362,7 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
                                 v->cols, sA, sB, sC, h->c, v->k_index > 0, kmask, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     if (last) {
-        trimul::EpilogueArgs ea{acc, v->cols, sC, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
+        trimul::EpilogueArgs ea{acc, 0, v->cols, sC, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
         e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
         if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
     }

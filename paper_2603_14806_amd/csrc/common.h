@@ -55,6 +55,17 @@ __host__ __device__ __forceinline__ int64_t panel_off(const PanelGeom& g, int64_
            k % kBlkK;
 }
 
+// Pair-blocked layout of the fp32 contraction result C written by the
+// contraction and read by the epilogue (full update and stage calls): element
+// (channel c, row i, column j) of nch channels lives at
+//     ((i * ceil(cols / 32) + j / 32) * nch + c) * 32 + j % 32
+// so that the 128 channels of 32 consecutive pairs of a row are one
+// contiguous 16 KB block.
+constexpr int kResJ = 32;
+__host__ __device__ __forceinline__ int64_t result_off(int64_t jblocks, int nch, int64_t c, int64_t i, int64_t j) {
+    return ((i * jblocks + j / kResJ) * nch + c) * kResJ + j % kResJ;
+}
+
 __device__ __forceinline__ float sigmoidf_(float t) { return 1.0f / (1.0f + __expf(-t)); }
 
 // Raw buffer resource over `bytes` bytes starting at p: loads at offsets

@@ -110,6 +110,7 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
     const int nk = (K + BK - 1) / BK;
     const int steps = my_tiles * nk;
     const int tiles = tiles_m * tiles_n;
+    const int nchan = total / tiles;
 
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // uniform per wave
@@ -285,12 +286,16 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
         }
 
         // 32x32 accumulator layout: lane holds column (lane & 31) and, in
-        // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.
+        // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.  Either layout
+        // of C gets 32 consecutive floats (128 bytes) per half-wave store.
         int ch, m0, n0;
         decode(it, ch, m0, n0);
         const int row0 = m0 + wm * (BM / 2) + 4 * hi, col0 = n0 + wn * 128 + rl;
-        float* Cb = C + ch * sC + (int64_t)row0 * ldc + col0;
         const bool full = m0 + BM <= M && n0 + BN <= N;
+        const int64_t jblocks = (N + kResJ - 1) / kResJ;
+        float* Cb = BLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0)
+                            : C + ch * sC + (int64_t)row0 * ldc + col0;
+        const int64_t row_step = BLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -298,7 +303,8 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
-                    float* p = Cb + (int64_t)dr * ldc + j * 32;
+                    // column block j*32 of a blocked C is (j * nchan * 32) floats further on
+                    float* p = Cb + (int64_t)dr * row_step + (BLOCKED ? (int64_t)j * nchan * kResJ : j * 32);
                     if (full || (row0 + dr < M && col0 + j * 32 < N)) {
                         float v = acc[i][j][r];
                         if (accumulate) v += *p;
@@ -322,7 +328,7 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
     const PanelGeom ga = panel_geom(M, K), gb = panel_geom(N, K);
     auto a_at = [&](int64_t r, int64_t k) { return BLOCKED ? A[panel_off(ga, ch, r, k)] : A[ch * sA + r * lda + k]; };
     auto b_at = [&](int64_t r, int64_t k) { return BLOCKED ? B[panel_off(gb, ch, r, k)] : B[ch * sB + r * ldb + k]; };
-    C += ch * sC;
+    float* Cr = C + ch * sC;
     const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
     float acc[4][4] = {};
     for (int k0 = 0; k0 < K; k0 += 16) {
@@ -349,13 +355,14 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
         }
         __syncthreads();
     }
+    const int64_t jblocks = (N + kResJ - 1) / kResJ;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int row = m0 + ty * 4 + i, col = n0 + tx * 4 + j;
             if (row < M && col < N) {
-                float* p = C + (int64_t)row * ldc + col;
+                float* p = BLOCKED ? C + result_off(jblocks, (int)gridDim.z, ch, row, col) : Cr + (int64_t)row * ldc + col;
                 *p = accumulate ? *p + acc[i][j] : acc[i][j];
             }
         }

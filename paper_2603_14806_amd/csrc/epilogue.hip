@@ -25,9 +25,11 @@ __global__ __launch_bounds__(256) void k3_epilogue_valu(
     const int np = (int)min<int64_t>(kPairs, a.cols - j0);
     const T* z = static_cast<const T*>(a.z);
 
+    const int64_t jblocks = (a.cols + kResJ - 1) / kResJ;
     for (int idx = t; idx < kPairs * kCh; idx += 256) {
         const int c = idx / kPairs, p = idx % kPairs;
-        cs[p][c] = p < np ? a.C[c * a.sc + i * a.ldc + j0 + p] : 0.f;
+        cs[p][c] = p < np ? (a.cblocked ? a.C[result_off(jblocks, kCh, c, i, j0 + p)] : a.C[c * a.sc + i * a.ldc + j0 + p])
+                          : 0.f;
     }
     for (int idx = t; idx < kPairs * kCz; idx += 256) {
         const int p = idx / kCz, d = idx % kCz;
@@ -103,12 +105,13 @@ __global__ __launch_bounds__(256) void k3_epilogue_valu(
 constexpr int kP3 = 32;
 constexpr int kCsRow = kP3 + 4;     // C staging row stride (floats): conflict-free column reads
 constexpr int kYRow = 256;          // bytes of one bf16 activation row [128]
+constexpr int kOsRow = kCz + 8;     // output staging row stride (floats): the two half-waves hit disjoint banks
 
 __device__ __forceinline__ uint32_t yoff(int p, int chunk) {
     return (uint32_t)(p * kYRow + ((chunk ^ (p & 15)) << 4));
 }
 
-template <typename TO, bool VEC_C>
+template <typename TO, bool VEC_C, bool CBLK>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
 void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* __restrict__ wepi,
                       const float* __restrict__ lnin_w, const float* __restrict__ lnin_b,
@@ -116,6 +119,7 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
     __shared__ __attribute__((aligned(16))) float cs[kCh * kCsRow];          // C as [c][p]
     __shared__ __attribute__((aligned(16))) char ys[3][kP3 * kYRow];         // y_hi, y_lo, x_hi
     __shared__ __attribute__((aligned(16))) float prm[4][128];               // LN gains and biases
+    __shared__ __attribute__((aligned(16))) float os[kP3 * kOsRow];          // outputs as [p][d]
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const int lp = t >> 3, lq = t & 7;     // LayerNorms: pair lp, 8 lanes per pair
     const bf16_t* z = static_cast<const bf16_t*>(a.z);
@@ -144,8 +148,22 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
         if (u >= nunits) return;
         const int64_t i = u / nchunk, j0 = (u - i * nchunk) * kP3;
         const int np = (int)min<int64_t>(kP3, a.cols - j0);
+        if (CBLK) {   // the unit's 128 channels x 32 pairs are one contiguous block
+            const float4* blk = reinterpret_cast<const float4*>(a.C + result_off(nchunk, kCh, 0, i, j0));
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2) {
+            for (int s2 = 0; s2 < 4; ++s2) {
+                float4 v = blk[t + 256 * s2];
+                if (4 * cj + 4 > np) {   // pairs past the end of the row are padding
+                    if (4 * cj + 0 >= np) v.x = 0.f;
+                    if (4 * cj + 1 >= np) v.y = 0.f;
+                    if (4 * cj + 2 >= np) v.z = 0.f;
+                    if (4 * cj + 3 >= np) v.w = 0.f;
+                }
+                cv[s2] = v;
+            }
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < 4 && !CBLK; ++s2) {
             const float* src = a.C + (int64_t)((t >> 3) + 32 * s2) * a.sc + i * a.ldc + j0 + 4 * cj;
             if (VEC_C && 4 * cj + 4 <= np) {
                 cv[s2] = *reinterpret_cast<const float4*>(src);
@@ -262,7 +280,8 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
         }
 
         // Lane holds output channel 32 w + (lane & 31); register r holds pair
-        // 8 (r / 4) + 4 (lane / 32) + r % 4.
+        // 8 (r / 4) + 4 (lane / 32) + r % 4.  Stage the unit's outputs in LDS,
+        // then write its contiguous [32 pairs][128] block with 16-byte stores.
         const int64_t i = u / nchunk, j0 = (u - i * nchunk) * kP3;
         const int np = (int)min<int64_t>(kP3, a.cols - j0);
         const bool mi = a.mask ? a.mask[a.row0 + i] != 0 : true;
@@ -270,9 +289,33 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int p = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            if (p < np) {
-                const bool m = mi && (a.mask ? a.mask[a.col0 + j0 + p] != 0 : true);
-                Store<TO>::st(out + ((i * a.cols) + j0 + p) * kCz + d, m ? sigmoidf_(ag[r]) * ay[r] : 0.f);
+            const bool m = p < np && mi && (a.mask ? a.mask[a.col0 + j0 + p] != 0 : true);
+            os[p * kOsRow + d] = m ? sigmoidf_(ag[r]) * ay[r] : 0.f;
+        }
+        __syncthreads();
+        TO* ob = out + ((i * a.cols) + j0) * kCz;
+        if (sizeof(TO) == 4) {
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2) {
+                const int q = t + 256 * s2, p = q >> 5, d4 = (q & 31) * 4;
+                if (p < np)
+                    *reinterpret_cast<float4*>(reinterpret_cast<float*>(ob) + p * kCz + d4) =
+                        *reinterpret_cast<const float4*>(&os[p * kOsRow + d4]);
+            }
+        } else {
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                const int q = t + 256 * s2, p = q >> 4, d8 = (q & 15) * 8;
+                if (p < np) {
+                    const float4 f0 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8]);
+                    const float4 f1 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8 + 4]);
+                    uint4 pk;
+                    pk.x = (uint32_t)f2bf(f0.x) | ((uint32_t)f2bf(f0.y) << 16);
+                    pk.y = (uint32_t)f2bf(f0.z) | ((uint32_t)f2bf(f0.w) << 16);
+                    pk.z = (uint32_t)f2bf(f1.x) | ((uint32_t)f2bf(f1.y) << 16);
+                    pk.w = (uint32_t)f2bf(f1.z) | ((uint32_t)f2bf(f1.w) << 16);
+                    *reinterpret_cast<uint4*>(reinterpret_cast<bf16_t*>(ob) + p * kCz + d8) = pk;
+                }
             }
         }
 #pragma unroll
@@ -297,11 +340,14 @@ hipError_t launch_mfma(const DeviceWeights& w, const EpilogueArgs& a, hipStream_
     const int64_t cap = 2 * (int64_t)w.cus;
     const unsigned g = (unsigned)(nunits < cap ? nunits : cap);
     const bool vec = (a.ldc % 4) == 0 && (a.sc % 4) == 0 && (reinterpret_cast<uintptr_t>(a.C) & 15u) == 0;
-    if (vec)
-        hipLaunchKernelGGL((k3_epilogue_mfma<TO, true>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
+    if (a.cblocked)
+        hipLaunchKernelGGL((k3_epilogue_mfma<TO, true, true>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
+                           w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
+    else if (vec)
+        hipLaunchKernelGGL((k3_epilogue_mfma<TO, true, false>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
                            w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
     else
-        hipLaunchKernelGGL((k3_epilogue_mfma<TO, false>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
+        hipLaunchKernelGGL((k3_epilogue_mfma<TO, false, false>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
                            w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
     return hipGetLastError();
 }

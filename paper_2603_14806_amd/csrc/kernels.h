@@ -34,9 +34,10 @@ constexpr int64_t kMaxKPanel = 65536;   // longest k-panel of one block call
 hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s);
 
 struct EpilogueArgs {
-    const float* C;      // [c][rows][ldc] fp32 contraction result
-    int64_t ldc;         // row stride of C (elements)
-    int64_t sc;          // channel stride of C (elements)
+    const float* C;      // fp32 contraction result: pair-blocked (cblocked) or [c][rows][ldc]
+    int cblocked;        // C in the pair-blocked result layout (common.h)
+    int64_t ldc;         // row stride of C (elements), row-major C only
+    int64_t sc;          // channel stride of C (elements), row-major C only
     const void* z;       // [rows][cols][c_z] pair tensor (same tile as C)
     const uint8_t* mask; // token mask over global indices, or null
     int64_t row0, col0;  // global token index of tile row 0 / column 0
@@ -50,9 +51,10 @@ struct EpilogueArgs {
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
                           int64_t N, int incoming, void* A, void* B, hipStream_t s);
 
-// K2: C[b] (+)= A[b] * diag(kmask) * B[b]^T for b < batch, C [b][M][ldc] row-major.
+// K2: C[b] (+)= A[b] * diag(kmask) * B[b]^T for b < batch.
 // blocked != 0: A, B in the blocked panel layout of M (N) rows and K columns
-// (lda, ldb, sA, sB unused); blocked == 0: A [b][M][lda], B [b][N][ldb].
+// (lda, ldb, sA, sB unused) and C in the pair-blocked result layout (ldc, sC
+// unused); blocked == 0: A [b][M][lda], B [b][N][ldb], C [b][M][ldc] (stride sC).
 hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B, float* C, int64_t M,
                            int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int64_t sA,
                            int64_t sB, int64_t sC, int batch, int accumulate, const uint8_t* kmask, int cus,

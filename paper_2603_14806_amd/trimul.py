@@ -217,12 +217,14 @@ class TriMul:
         return A, B
 
     def contract(self, A, B, N, stream=None):
-        """A, B in the panel layout (project / dense_to_panel)."""
-        C = torch.empty((128, N, N), dtype=torch.float32, device=self.device)
+        """A, B in the panel layout (project / dense_to_panel); returns C in
+        the result layout (flat; see result_to_dense)."""
+        C = torch.empty(N * (-(-N // 32) * 32) * 128, dtype=torch.float32, device=self.device)
         tri_mul_contract(self.h, A, B, N, C, stream)
         return C
 
     def epilogue(self, C, z, mask=None, out=None, stream=None):
+        """C in the result layout (contract / dense_to_result)."""
         N = z.shape[0]
         out = self._out(N, out)
         tri_mul_epilogue(self.h, C, z, mask, N, out, stream)
@@ -253,3 +255,18 @@ def dense_to_panel(X):
     Y = torch.zeros((c, T * 256, S * 32), dtype=X.dtype, device=X.device)
     Y[:, :N, :N] = X
     return Y.reshape(c, T, 256, S, 32).permute(0, 1, 3, 2, 4).contiguous().reshape(-1)
+
+
+def result_to_dense(Cr, N, c=128):
+    """Result-layout C (flat) -> dense [c][N][N]."""
+    J = -(-N // 32)
+    return Cr.reshape(N, J, c, 32).permute(2, 0, 1, 3).reshape(c, N, J * 32)[:, :, :N]
+
+
+def dense_to_result(C):
+    """Dense [c][N][N] -> flat result-layout C (zero padding)."""
+    c, N = C.shape[0], C.shape[1]
+    J = -(-N // 32)
+    Y = torch.zeros((c, N, J * 32), dtype=C.dtype, device=C.device)
+    Y[:, :, :N] = C
+    return Y.reshape(c, N, J, 32).permute(1, 2, 0, 3).contiguous().reshape(-1)

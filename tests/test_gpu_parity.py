@@ -30,7 +30,7 @@ def test_contract_exact_on_integers(dtype, N):
     C = layer.contract(T.dense_to_panel(A).cuda(), T.dense_to_panel(B).cuda(), N)
     torch.cuda.synchronize()
     ref = oracle.block_contract([host(A)], [host(B)], [np.ones(N)])    # [i][j][c]
-    np.testing.assert_array_equal(host(C).transpose(1, 2, 0), ref)
+    np.testing.assert_array_equal(host(T.result_to_dense(C, N)).transpose(1, 2, 0), ref)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -103,7 +103,7 @@ def test_epilogue_matches_oracle(dtype, out_dtype, N):
     mask = synth.random_mask(N, 0.85, sub=3)
     # contraction-like input: sums of ~N unit products have scale sqrt(N)
     C = (torch.randn((128, N, N), generator=torch.Generator().manual_seed(5)) * np.sqrt(N)).float()
-    out = layer.epilogue(C.cuda(), z.cuda(), mask.cuda())
+    out = layer.epilogue(T.dense_to_result(C).cuda(), z.cuda(), mask.cuda())
     torch.cuda.synchronize()
     m = oracle.pair_mask(mask)
     _, _, gate = oracle.project(z, m, W)

@@ -19,3 +19,17 @@ def test_panel_index_formula(N):
                 idx = ((c * Tn + i // 256) * S + k // 32) * 8192 + (i % 256) * 32 + k % 32
                 assert P[idx] == X[c, i, k]
     assert torch.equal(T.panel_to_dense(P, N, 3), X)
+
+
+@pytest.mark.parametrize("N", [1, 31, 33, 100])
+def test_result_index_formula(N):
+    c = 5
+    X = torch.arange(c * N * N, dtype=torch.float64).reshape(c, N, N)
+    R = T.dense_to_result(X)
+    J = -(-N // 32)
+    assert R.numel() == N * J * 32 * c
+    for ch in range(c):
+        for i in {0, N // 2, N - 1}:
+            for j in {0, N // 3, N - 1}:
+                assert R[((i * J + j // 32) * c + ch) * 32 + j % 32] == X[ch, i, j]
+    assert torch.equal(T.result_to_dense(R, N, c), X)
