@@ -170,8 +170,8 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v,
  * (c, i, k) is at index
  *     ((c * T + i / 256) * S + k / 32) * 8192 + (i % 256) * 32 + k % 32
  * with T = ceil(N / 256) and S = ceil(N / 32), so one operand takes
- * c * T * 256 * S * 32 elements.  Padding elements (i >= N or k >= N) are
- * never written and never contribute.
+ * c * T * 256 * S * 32 elements.  Padding elements (i >= N or k >= N) hold
+ * unspecified values and never contribute.
  *
  * tri_mul_panel_size: bytes of one operand for N tokens (*bytes is HOST). */
 int tri_mul_panel_size(tri_mul_handle_t h, int64_t N, size_t* bytes);

@@ -66,7 +66,10 @@ __host__ __device__ __forceinline__ int64_t result_off(int64_t jblocks, int nch,
     return ((i * jblocks + j / kResJ) * nch + c) * kResJ + j % kResJ;
 }
 
-__device__ __forceinline__ float sigmoidf_(float t) { return 1.0f / (1.0f + __expf(-t)); }
+// Logistic function with the hardware exponential and reciprocal (v_exp_f32,
+// v_rcp_f32, ~1 ulp each) instead of an IEEE division; exp overflow gives
+// rcp(inf) = 0 as the limit requires.
+__device__ __forceinline__ float sigmoidf_(float t) { return __builtin_amdgcn_rcpf(1.0f + __expf(-t)); }
 
 // Raw buffer resource over `bytes` bytes starting at p: loads at offsets
 // >= bytes return zero (the hardware range check of untyped buffer access).
@@ -76,6 +79,63 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
 
 __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// ---------------------------------------------------------------- direct-to-LDS
+
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor (gfx9): base, stride 0, num_records = bytes, 32-bit
+// untyped access.  Loads at byte offsets >= bytes return zero.  The
+// arguments must be wave-uniform; the words are moved to scalar registers
+// explicitly because the inline-assembly loads take the descriptor there.
+__device__ __forceinline__ v4i_t buffer_desc(const void* p, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    v4i_t r;
+    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+    r.w = 0x00020000;
+    return r;
+}
+
+// Direct-to-LDS load: lane i writes `size` bytes at LDS address lds + size * i.
+// Issued as inline assembly so that the compiler does not serialise every
+// later LDS read behind it; the kernel waits on vmcnt itself.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_load16(v4i_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    lds = __builtin_amdgcn_readfirstlane(lds);
+    soff = __builtin_amdgcn_readfirstlane(soff);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+__device__ __forceinline__ void lds_load4(v4i_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    lds = __builtin_amdgcn_readfirstlane(lds);
+    soff = __builtin_amdgcn_readfirstlane(soff);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(p));
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// The same wait as inline assembly with a memory clobber: the compiler moves
+// no load or store across it, so the number of vector-memory instructions
+// issued between a load and its wait is the one the source shows.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_pinned() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
 }  // namespace trimul

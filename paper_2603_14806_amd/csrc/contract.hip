@@ -48,50 +48,6 @@ template <int BM> struct Geo {
     static constexpr int STAGES = (160 * 1024) / ST_BYTES >= 4 ? 4 : 3;
 };
 
-typedef int v4i_t __attribute__((ext_vector_type(4)));
-
-// Raw buffer descriptor (gfx9): base, stride 0, num_records = bytes, 32-bit
-// untyped access.  Loads at byte offsets >= bytes return zero.
-__device__ __forceinline__ v4i_t buffer_desc(const void* p, uint32_t bytes) {
-    const uint64_t a = reinterpret_cast<uint64_t>(p);
-    v4i_t r;
-    r.x = (int)(uint32_t)a;
-    r.y = (int)(uint32_t)(a >> 32);
-    r.z = (int)bytes;
-    r.w = 0x00020000;
-    return r;
-}
-
-// Direct-to-LDS load: lane i writes `size` bytes at LDS address lds + size * i.
-// Issued as inline assembly so that the compiler does not serialise every
-// later LDS read behind it; the kernel waits on vmcnt itself.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_load16(v4i_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
-    lds = __builtin_amdgcn_readfirstlane(lds);
-    soff = __builtin_amdgcn_readfirstlane(soff);
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
-}
-__device__ __forceinline__ void lds_load4(v4i_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
-    lds = __builtin_amdgcn_readfirstlane(lds);
-    soff = __builtin_amdgcn_readfirstlane(soff);
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
-                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(p));
-}
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
 template <int BM, bool KMASK, bool BLOCKED>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C,
@@ -370,7 +326,7 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
 
 __global__ void k_stage_kmask(const uint8_t* __restrict__ mask, int klen, int padded, uint8_t* __restrict__ dst) {
     const int k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k < padded) dst[k] = (k < klen && mask[k] != 0) ? 1 : 0;
+    if (k < padded) dst[k] = (k < klen && (!mask || mask[k] != 0)) ? 1 : 0;
 }
 
 }  // namespace

@@ -146,7 +146,8 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
         for (int s2 = 0; s2 < 4; ++s2) cv[s2] = make_float4(0.f, 0.f, 0.f, 0.f);
         z0 = z1 = make_uint4(0, 0, 0, 0);
         if (u >= nunits) return;
-        const int64_t i = u / nchunk, j0 = (u - i * nchunk) * kP3;
+        const uint32_t uq = (uint32_t)u / (uint32_t)nchunk;   // units < 2^31
+        const int64_t i = uq, j0 = (int64_t)((uint32_t)u - uq * (uint32_t)nchunk) * kP3;
         const int np = (int)min<int64_t>(kP3, a.cols - j0);
         if (CBLK) {   // the unit's 128 channels x 32 pairs are one contiguous block
             const float4* blk = reinterpret_cast<const float4*>(a.C + result_off(nchunk, kCh, 0, i, j0));
@@ -275,14 +276,15 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
             const bf16x8_t yl = *reinterpret_cast<const bf16x8_t*>(ys[1] + o);
             const bf16x8_t xh = *reinterpret_cast<const bf16x8_t*>(ys[2] + o);
             ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yh, wo[ks], ay, 0, 0, 0);
-            ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yl, wo[ks], ay, 0, 0, 0);
             ag = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, wg[ks], ag, 0, 0, 0);
+            ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yl, wo[ks], ay, 0, 0, 0);
         }
 
         // Lane holds output channel 32 w + (lane & 31); register r holds pair
         // 8 (r / 4) + 4 (lane / 32) + r % 4.  Stage the unit's outputs in LDS,
         // then write its contiguous [32 pairs][128] block with 16-byte stores.
-        const int64_t i = u / nchunk, j0 = (u - i * nchunk) * kP3;
+        const uint32_t uq = (uint32_t)u / (uint32_t)nchunk;   // units < 2^31
+        const int64_t i = uq, j0 = (int64_t)((uint32_t)u - uq * (uint32_t)nchunk) * kP3;
         const int np = (int)min<int64_t>(kP3, a.cols - j0);
         const bool mi = a.mask ? a.mask[a.row0 + i] != 0 : true;
         const int d = w * 32 + (lane & 31);
@@ -294,11 +296,12 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
         }
         __syncthreads();
         TO* ob = out + ((i * a.cols) + j0) * kCz;
+        const bool full = np == kP3;   // uniform: no per-lane predicates on full units
         if (sizeof(TO) == 4) {
 #pragma unroll
             for (int s2 = 0; s2 < 4; ++s2) {
                 const int q = t + 256 * s2, p = q >> 5, d4 = (q & 31) * 4;
-                if (p < np)
+                if (full || p < np)
                     *reinterpret_cast<float4*>(reinterpret_cast<float*>(ob) + p * kCz + d4) =
                         *reinterpret_cast<const float4*>(&os[p * kOsRow + d4]);
             }
@@ -306,7 +309,7 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
                 const int q = t + 256 * s2, p = q >> 4, d8 = (q & 15) * 8;
-                if (p < np) {
+                if (full || p < np) {
                     const float4 f0 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8]);
                     const float4 f1 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8 + 4]);
                     uint4 pk;

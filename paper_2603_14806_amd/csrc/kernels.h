@@ -24,12 +24,12 @@ struct DeviceWeights {
     uint16_t* epi_bf = nullptr;   // [2*c_z][128]: W_o rows then W_g rows
     float eps = 1e-5f;
     int cus = 256;                // compute units of the device (persistent grids)
-    uint8_t* kmask_pad = nullptr; // staging of a k-panel token mask, kMaxKPanel + 64 bytes
+    uint8_t* kmask_pad = nullptr; // 0/1 staging of a token mask (k-panel or whole sequence), kMaxKPanel + 64 bytes
 };
 
 constexpr int64_t kMaxKPanel = 65536;   // longest k-panel of one block call
 
-// Copies mask[0, klen) into dst as 0/1 bytes and zero-fills dst up to the next
+// Copies mask[0, klen) into dst as 0/1 bytes (mask NULL: all ones) and zero-fills dst up to the next
 // multiple of 32 (so the contraction can read whole 4-byte words of it).
 hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s);
 

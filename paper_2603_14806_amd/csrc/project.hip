@@ -95,28 +95,73 @@ __global__ __launch_bounds__(256) void k1_project_valu(
 // operand, so the 4 x 32 outputs of a channel land in the same lane and
 // register and the gating is element-wise in registers.
 //
+// z and the token mask reach LDS through a 3-stage ring filled by
+// direct-to-LDS buffer loads two lines ahead of the line being computed, so
+// the HBM latency of z hides behind two lines of work.  Every wave issues
+// the same number of vector-memory instructions per line (3 loads, 8 stores,
+// tails included), which makes the vmcnt waits exact constants.
+//
 // Precision: the LayerNormed input x (fp32) is split into x_hi = bf16(x) and
 // x_lo = bf16(x - x_hi); with exact bf16 weights W x_hi + W x_lo carries ~16
 // mantissa bits, so a and b see one bf16 rounding only (their store).
-constexpr int kP1 = 32;             // pairs per line
-constexpr int kXRow = kCz * 2;      // bytes of one bf16 x row (256)
+constexpr int kP1 = 32;                 // pairs per line
+constexpr int kXRow = kCz * 2;          // bytes of one bf16 row of 128 channels (256)
+constexpr int kZSt = kP1 * kXRow;       // z bytes of one line (8 KB)
+constexpr int kMSt = 4 * 256;           // per-wave token-mask bytes of one line
+constexpr int kSt = kZSt + kMSt;        // one ring stage
+constexpr int kRing = 3;
 
 // x rows [p][128] bf16: 16-byte chunk q of row p lives at slot q ^ (p & 15).
 __device__ __forceinline__ uint32_t xoff(int p, int chunk) {
     return (uint32_t)(p * kXRow + ((chunk ^ (p & 15)) << 4));
 }
 
+// tmask: the token mask as 0/1 bytes, zero from N up to mpad = ceil(N/32)*32.
 template <bool INCOMING>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
-void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ mask, int N,
-                     int nchunk, int64_t nlines, const bf16_t* __restrict__ wproj,
-                     const float* __restrict__ lnw, const float* __restrict__ lnb, float eps,
-                     bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
+void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ tmask, int N, int nchunk,
+                     int nlines, const bf16_t* __restrict__ wproj, const float* __restrict__ lnw,
+                     const float* __restrict__ lnb, float eps, bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
+    __shared__ __attribute__((aligned(16))) char ring[kRing * kSt];     // z rows [p][256 B], mask
     __shared__ __attribute__((aligned(16))) char xs[2][kP1 * kXRow];   // x_hi, x_lo
     __shared__ __attribute__((aligned(16))) float os[2][kCh][kP1];      // a, b as [c][p]
     __shared__ __attribute__((aligned(16))) float gb[2][kCz];           // LayerNorm gain, bias
-    const int t = threadIdx.x, lane = t & 63, g = t >> 6;
+    const int t = threadIdx.x, lane = t & 63;
+    const int g = __builtin_amdgcn_readfirstlane(t >> 6);
     const int lp = t >> 3, lq = t & 7;     // LayerNorm: pair lp, channels 16 lq .. 16 lq + 15
+    const int G = gridDim.x;
+
+    // Ring fill.  Stage row p holds pair k0 + p of the line; its 16-byte
+    // chunk q sits at slot q ^ (p & 1), so that the LayerNorm reads of two
+    // neighbouring rows hit disjoint banks.  Wave g loads rows 8 g .. 8 g + 7
+    // (two 1 KB loads: lane i -> row 8 g + 4 h + i / 16, slot i % 16) and its
+    // own copy of the line's mask bytes: m[k0 .. k0 + 31] at 0, the dword of
+    // m[r] at 32.  Lines past the end load nothing (zero-size descriptor).
+    const uint32_t zstep = INCOMING ? (uint32_t)N * kXRow : (uint32_t)kXRow;   // bytes between pairs
+    const uint32_t ring_base = lds_addr(ring);
+    const int drow = g * 8 + (lane >> 4);
+    const uint32_t dchunk = (uint32_t)(((lane & 15) ^ (drow & 1)) << 4);
+    const uint32_t dv0 = (uint32_t)drow * zstep + dchunk, dv1 = (uint32_t)(drow + 4) * zstep + dchunk;
+    const uint32_t mpad = (uint32_t)((N + 31) / 32 * 32);
+    auto issue = [&](int line, int stage) {
+        const bool valid = line < nlines;
+        int r = 0, k0 = 0;
+        if (valid) {
+            r = line / nchunk;
+            k0 = (line - r * nchunk) * kP1;
+        }
+        const int np = valid ? min(kP1, N - k0) : 0;
+        const int64_t pair0 = INCOMING ? (int64_t)k0 * N + r : (int64_t)r * N + k0;
+        const v4i_t rz = buffer_desc(z + pair0 * kCz, np > 0 ? (uint32_t)(np - 1) * zstep + kXRow : 0u);
+        const uint32_t st = ring_base + (uint32_t)(stage * kSt);
+        lds_load16(rz, dv0, 0, st + g * 2048);
+        lds_load16(rz, dv1, 0, st + g * 2048 + 1024);
+        const v4i_t rm = buffer_desc(tmask, valid ? mpad : 0u);
+        const uint32_t mo = lane < 8 ? (uint32_t)(k0 + 4 * lane) : lane == 8 ? (uint32_t)(r & ~3) : 0xfffffff0u;
+        lds_load4(rm, mo, 0, st + kZSt + g * 256);
+    };
+    issue(blockIdx.x, 0);
+    issue(blockIdx.x + G, 1);
 
     bf16x8_t w[4][8];
 #pragma unroll
@@ -129,36 +174,27 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ m
         gb[0][t] = lnw[t];
         gb[1][t] = lnb[t];
     }
-    __syncthreads();
+    const PanelGeom pg = panel_geom(N, N);
 
-    auto pair_of = [&](int64_t line, int p, int64_t& r, int64_t& k0) -> int64_t {
-        r = line / nchunk;
-        k0 = (line - r * nchunk) * kP1;
-        return INCOMING ? (k0 + p) * N + r : r * N + k0 + p;
-    };
-    auto load_z = [&](int64_t line, uint4& z0, uint4& z1) {
-        z0 = z1 = make_uint4(0, 0, 0, 0);
-        if (line < nlines) {
-            int64_t r, k0;
-            const int64_t pr = pair_of(line, lp, r, k0);
-            if (k0 + lp < N) {
-                const uint4* src = reinterpret_cast<const uint4*>(z + pr * kCz + 16 * lq);
-                z0 = src[0];
-                z1 = src[1];
-            }
-        }
-    };
-
-    uint4 zc0, zc1;
-    load_z(blockIdx.x, zc0, zc1);
-    for (int64_t line = blockIdx.x; line < nlines; line += gridDim.x) {
-        uint4 zn0, zn1;
-        load_z(line + gridDim.x, zn0, zn1);      // prefetch the next line
+    int stage = 0;
+    for (int it = 0, line = blockIdx.x; line < nlines; ++it, line += G) {
+        // Vector-memory instructions issued after this line's loads: the
+        // next line's loads (3) and, from the second line on, the 8 stores
+        // of every line in between.
+        if (it == 0) wait_vmcnt_pinned<3>();
+        else if (it == 1) wait_vmcnt_pinned<3 + 8>();
+        else wait_vmcnt_pinned<3 + 8 + 8>();
+        __syncthreads();
+        issue(line + 2 * G, stage == 0 ? 2 : stage - 1);   // into the stage read one line ago
+        const char* zs = ring + stage * kSt;
+        stage = stage == 2 ? 0 : stage + 1;
 
         // LayerNorm of pair lp over 128 channels (8 lanes x 16 channels).
         float v[16];
         {
-            const uint32_t u[8] = {zc0.x, zc0.y, zc0.z, zc0.w, zc1.x, zc1.y, zc1.z, zc1.w};
+            const uint4 z0 = *reinterpret_cast<const uint4*>(zs + lp * kXRow + (((2 * lq) ^ (lp & 1)) << 4));
+            const uint4 z1 = *reinterpret_cast<const uint4*>(zs + lp * kXRow + (((2 * lq + 1) ^ (lp & 1)) << 4));
+            const uint32_t u[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 v[2 * i] = __uint_as_float(u[i] << 16);
@@ -224,42 +260,35 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ m
         }
 
         // Gate, mask, stage as [c][p] fp32.  Lane holds pair (lane & 31); in
-        // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.
-        int64_t r0, k0;
-        (void)pair_of(line, 0, r0, k0);
-        const int np = (int)min<int64_t>(kP1, N - k0);
-        const bool mrow = mask ? mask[r0] != 0 : true;
-        const bool mp = bp < np && mrow && (mask ? mask[k0 + bp] != 0 : true);
+        // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.  The
+        // staged mask is zero past N, which also zeroes a ragged line's tail.
+        const int r0 = line / nchunk, k0 = (line - r0 * nchunk) * kP1;
+        const uint8_t* ms = reinterpret_cast<const uint8_t*>(zs + kZSt + g * 256);
+        const uint32_t keep = (ms[bp] & ms[32 + (r0 & 3)]) ? 0xffffffffu : 0u;   // branch-free select
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int c = g * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            os[0][c][bp] = mp ? sigmoidf_(acc[1][r]) * acc[0][r] : 0.f;
-            os[1][c][bp] = mp ? sigmoidf_(acc[3][r]) * acc[2][r] : 0.f;
+            os[0][c][bp] = __uint_as_float(__float_as_uint(sigmoidf_(acc[1][r]) * acc[0][r]) & keep);
+            os[1][c][bp] = __uint_as_float(__float_as_uint(sigmoidf_(acc[3][r]) * acc[2][r]) & keep);
         }
         __syncthreads();
 
         // Channel-major stores: 8 lanes write the 32 pairs (64 bytes) of one
-        // panel row; the 32 pairs are one k-step of the blocked layout.
+        // panel row, one k-step of the blocked layout.  A ragged line's tail
+        // writes zeros into the k padding of its step, so every wave issues
+        // exactly 8 stores per line.
         const int j = t & 7;
-        const PanelGeom pg = panel_geom(N, N);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int R = (t >> 3) + 32 * i, ab = R >> 7, c = R & 127;
             const float4 f = *reinterpret_cast<const float4*>(&os[ab][c][4 * j]);
             bf16_t* dst = (ab ? B : A) + panel_off(pg, c, r0, k0 + 4 * j);
-            if (4 * j + 4 <= np) {
-                const uint32_t lo2 = (uint32_t)f2bf(f.x) | ((uint32_t)f2bf(f.y) << 16);
-                const uint32_t hi2 = (uint32_t)f2bf(f.z) | ((uint32_t)f2bf(f.w) << 16);
-                *reinterpret_cast<uint2*>(dst) = make_uint2(lo2, hi2);
-            } else {
-                const float e[4] = {f.x, f.y, f.z, f.w};
-                for (int u = 0; u < 4; ++u)
-                    if (4 * j + u < np) dst[u] = f2bf(e[u]);
-            }
+            const uint32_t lo2 = (uint32_t)f2bf(f.x) | ((uint32_t)f2bf(f.y) << 16);
+            const uint32_t hi2 = (uint32_t)f2bf(f.z) | ((uint32_t)f2bf(f.w) << 16);
+            *reinterpret_cast<uint2*>(dst) = make_uint2(lo2, hi2);
         }
-        zc0 = zn0;
-        zc1 = zn1;
     }
+    wait_vmcnt_pinned<0>();   // the ring loads past the last line land before the work-group ends
 }
 
 }  // namespace
@@ -278,14 +307,16 @@ hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, cons
                                nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
     } else {
         const int nch = (int)((N + kP1 - 1) / kP1);
-        const int64_t nlines = N * nch;
-        const unsigned g = (unsigned)(nlines < 2 * (int64_t)w.cus ? nlines : 2 * (int64_t)w.cus);
+        const int nlines = (int)(N * nch);
+        const unsigned g = (unsigned)(nlines < 2 * w.cus ? nlines : 2 * w.cus);
+        hipError_t e = launch_stage_kmask(mask, N, w.kmask_pad, s);
+        if (e != hipSuccess) return e;
         if (incoming)
-            hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N,
-                               nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
+            hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, w.kmask_pad,
+                               (int)N, nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
         else
-            hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, mask, (int)N,
-                               nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
+            hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, w.kmask_pad,
+                               (int)N, nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
     }
     return hipGetLastError();
 }
