@@ -23,6 +23,36 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
     return __builtin_bit_cast(bf16_t, b);
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats to two round-to-nearest-even bf16 in one dword (lo in bits 0-15);
+// one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+// Sum over each aligned group of 8 lanes, returned to all 8 lanes, with DPP
+// moves instead of LDS permutes: pairs (xor 1), quads (xor 2), then the two
+// quads of the group (lane i meets lane 7 - i).  Every lane of a group adds
+// the same operands, so all 8 results are bitwise equal.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float sum_lanes8(float v) {
+    v += dpp_mov<0xb1>(v);    // quad_perm [1, 0, 3, 2]
+    v += dpp_mov<0x4e>(v);    // quad_perm [2, 3, 0, 1]
+    v += dpp_mov<0x141>(v);   // row_half_mirror
+    return v;
+}
+__device__ __forceinline__ float sum_lanes4(float v) {
+    v += dpp_mov<0xb1>(v);
+    v += dpp_mov<0x4e>(v);
+    return v;
+}
+
 template <typename T> struct Store;
 template <> struct Store<float> {
     static __device__ __forceinline__ float ld(const float* p) { return *p; }

@@ -44,10 +44,8 @@ __global__ __launch_bounds__(256) void k3_epilogue_valu(
             s1 += cs[p][d];
             s2 += xs[p][d];
         }
-        s1 += __shfl_xor(s1, 1);
-        s1 += __shfl_xor(s1, 2);
-        s2 += __shfl_xor(s2, 1);
-        s2 += __shfl_xor(s2, 2);
+        s1 = sum_lanes4(s1);
+        s2 = sum_lanes4(s2);
         const float mu1 = s1 * (1.0f / kCh), mu2 = s2 * (1.0f / kCz);
         float v1 = 0.f, v2 = 0.f;
         for (int d = q * 32; d < q * 32 + 32; ++d) {
@@ -55,10 +53,8 @@ __global__ __launch_bounds__(256) void k3_epilogue_valu(
             v1 += e1 * e1;
             v2 += e2 * e2;
         }
-        v1 += __shfl_xor(v1, 1);
-        v1 += __shfl_xor(v1, 2);
-        v2 += __shfl_xor(v2, 1);
-        v2 += __shfl_xor(v2, 2);
+        v1 = sum_lanes4(v1);
+        v2 = sum_lanes4(v2);
         const float r1 = rsqrtf(v1 * (1.0f / kCh) + eps), r2 = rsqrtf(v2 * (1.0f / kCz) + eps);
         for (int d = q * 32; d < q * 32 + 32; ++d) {
             cs[p][d] = (cs[p][d] - mu1) * r1 * lnout_w[d] + lnout_b[d];
@@ -203,9 +199,7 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
                 v[i] = cs[(lq + 8 * i) * kCsRow + lp];
                 s1 += v[i];
             }
-            s1 += __shfl_xor(s1, 1);
-            s1 += __shfl_xor(s1, 2);
-            s1 += __shfl_xor(s1, 4);
+            s1 = sum_lanes8(s1);
             const float mu = s1 * (1.0f / kCh);
             float q2 = 0.f;
 #pragma unroll
@@ -213,9 +207,7 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
                 v[i] -= mu;
                 q2 += v[i] * v[i];
             }
-            q2 += __shfl_xor(q2, 1);
-            q2 += __shfl_xor(q2, 2);
-            q2 += __shfl_xor(q2, 4);
+            q2 = sum_lanes8(q2);
             const float rs = rsqrtf(q2 * (1.0f / kCh) + eps);
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -238,9 +230,7 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
             float s1 = 0.f;
 #pragma unroll
             for (int i = 0; i < 16; ++i) s1 += v[i];
-            s1 += __shfl_xor(s1, 1);
-            s1 += __shfl_xor(s1, 2);
-            s1 += __shfl_xor(s1, 4);
+            s1 = sum_lanes8(s1);
             const float mu = s1 * (1.0f / kCz);
             float q2 = 0.f;
 #pragma unroll
@@ -248,9 +238,7 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
                 v[i] -= mu;
                 q2 += v[i] * v[i];
             }
-            q2 += __shfl_xor(q2, 1);
-            q2 += __shfl_xor(q2, 2);
-            q2 += __shfl_xor(q2, 4);
+            q2 = sum_lanes8(q2);
             const float rs = rsqrtf(q2 * (1.0f / kCz) + eps);
             uint32_t hx[8];
 #pragma unroll

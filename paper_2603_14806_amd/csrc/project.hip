@@ -175,6 +175,10 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         gb[1][t] = lnb[t];
     }
     const PanelGeom pg = panel_geom(N, N);
+    // Store mapping: thread t writes pairs 4 (t & 7) .. 4 (t & 7) + 3 of
+    // channel (t >> 3) + 32 (i & 3) of A (i < 4) or B (i >= 4).
+    const int64_t ch_stride = panel_elems(pg);
+    const int64_t st_lane = (t >> 3) * ch_stride + 4 * (t & 7);
 
     int stage = 0;
     for (int it = 0, line = blockIdx.x; line < nlines; ++it, line += G) {
@@ -204,9 +208,7 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         float s = 0.f;
 #pragma unroll
         for (int i = 0; i < 16; ++i) s += v[i];
-        s += __shfl_xor(s, 1);
-        s += __shfl_xor(s, 2);
-        s += __shfl_xor(s, 4);
+        s = sum_lanes8(s);
         const float mu = s * (1.0f / kCz);
         float q2 = 0.f;
 #pragma unroll
@@ -214,9 +216,7 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
             v[i] -= mu;
             q2 += v[i] * v[i];
         }
-        q2 += __shfl_xor(q2, 1);
-        q2 += __shfl_xor(q2, 2);
-        q2 += __shfl_xor(q2, 4);
+        q2 = sum_lanes8(q2);
         const float rs = rsqrtf(q2 * (1.0f / kCz) + eps);
         float gam[16], bet[16];
 #pragma unroll
@@ -231,9 +231,8 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         for (int i = 0; i < 8; ++i) {
             const float x0 = v[2 * i] * rs * gam[2 * i] + bet[2 * i];
             const float x1 = v[2 * i + 1] * rs * gam[2 * i + 1] + bet[2 * i + 1];
-            const bf16_t h0 = f2bf(x0), h1 = f2bf(x1);
-            hi[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            lo[i] = (uint32_t)f2bf(x0 - bf2f(h0)) | ((uint32_t)f2bf(x1 - bf2f(h1)) << 16);
+            hi[i] = pack_bf16x2(x0, x1);
+            lo[i] = pack_bf16x2(x0 - __uint_as_float(hi[i] << 16), x1 - __uint_as_float(hi[i] & 0xffff0000u));
         }
         *reinterpret_cast<uint4*>(xs[0] + xoff(lp, 2 * lq)) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
         *reinterpret_cast<uint4*>(xs[0] + xoff(lp, 2 * lq + 1)) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
@@ -277,15 +276,13 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         // panel row, one k-step of the blocked layout.  A ragged line's tail
         // writes zeros into the k padding of its step, so every wave issues
         // exactly 8 stores per line.
-        const int j = t & 7;
+        const int64_t line_off = panel_off(pg, 0, r0, k0);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const int R = (t >> 3) + 32 * i, ab = R >> 7, c = R & 127;
-            const float4 f = *reinterpret_cast<const float4*>(&os[ab][c][4 * j]);
-            bf16_t* dst = (ab ? B : A) + panel_off(pg, c, r0, k0 + 4 * j);
-            const uint32_t lo2 = (uint32_t)f2bf(f.x) | ((uint32_t)f2bf(f.y) << 16);
-            const uint32_t hi2 = (uint32_t)f2bf(f.z) | ((uint32_t)f2bf(f.w) << 16);
-            *reinterpret_cast<uint2*>(dst) = make_uint2(lo2, hi2);
+            const int ab = i >> 2, c = (t >> 3) + 32 * (i & 3);
+            const float4 f = *reinterpret_cast<const float4*>(&os[ab][c][4 * (t & 7)]);
+            bf16_t* dst = (ab ? B : A) + (line_off + st_lane + 32 * (i & 3) * ch_stride);
+            *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(f.x, f.y), pack_bf16x2(f.z, f.w));
         }
     }
     wait_vmcnt_pinned<0>();   // the ring loads past the last line land before the work-group ends
