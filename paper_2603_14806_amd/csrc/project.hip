@@ -129,7 +129,12 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
     const int t = threadIdx.x, lane = t & 63;
     const int g = __builtin_amdgcn_readfirstlane(t >> 6);
     const int lp = t >> 3, lq = t & 7;     // LayerNorm: pair lp, channels 16 lq .. 16 lq + 15
+    // Line order: rows fastest (line = kc * N + r covers pairs k0 = 32 kc ..
+    // k0 + 31 of row r), and the work-groups of one XCD take consecutive
+    // lines; the grid's lines of one round then fill whole 256-row blocks of
+    // the operands and read long runs of z in either direction.
     const int G = gridDim.x;
+    const int first = (G & 7) == 0 ? (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3) : blockIdx.x;
 
     // Ring fill.  Stage row p holds pair k0 + p of the line; its 16-byte
     // chunk q sits at slot q ^ (p & 1), so that the LayerNorm reads of two
@@ -147,8 +152,9 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         const bool valid = line < nlines;
         int r = 0, k0 = 0;
         if (valid) {
-            r = line / nchunk;
-            k0 = (line - r * nchunk) * kP1;
+            const int kc = line / N;
+            r = line - kc * N;
+            k0 = kc * kP1;
         }
         const int np = valid ? min(kP1, N - k0) : 0;
         const int64_t pair0 = INCOMING ? (int64_t)k0 * N + r : (int64_t)r * N + k0;
@@ -160,8 +166,8 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         const uint32_t mo = lane < 8 ? (uint32_t)(k0 + 4 * lane) : lane == 8 ? (uint32_t)(r & ~3) : 0xfffffff0u;
         lds_load4(rm, mo, 0, st + kZSt + g * 256);
     };
-    issue(blockIdx.x, 0);
-    issue(blockIdx.x + G, 1);
+    issue(first, 0);
+    issue(first + G, 1);
 
     bf16x8_t w[4][8];
 #pragma unroll
@@ -181,7 +187,7 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
     const int64_t st_lane = (t >> 3) * ch_stride + 4 * (t & 7);
 
     int stage = 0;
-    for (int it = 0, line = blockIdx.x; line < nlines; ++it, line += G) {
+    for (int it = 0, line = first; line < nlines; ++it, line += G) {
         // Vector-memory instructions issued after this line's loads: the
         // next line's loads (3) and, from the second line on, the 8 stores
         // of every line in between.
@@ -261,7 +267,7 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         // Gate, mask, stage as [c][p] fp32.  Lane holds pair (lane & 31); in
         // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.  The
         // staged mask is zero past N, which also zeroes a ragged line's tail.
-        const int r0 = line / nchunk, k0 = (line - r0 * nchunk) * kP1;
+        const int kc = line / N, r0 = line - kc * N, k0 = kc * kP1;
         const uint8_t* ms = reinterpret_cast<const uint8_t*>(zs + kZSt + g * 256);
         const uint32_t keep = (ms[bp] & ms[32 + (r0 & 3)]) ? 0xffffffffu : 0u;   // branch-free select
 #pragma unroll
