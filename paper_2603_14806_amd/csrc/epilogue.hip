@@ -316,6 +316,226 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
     }
 }
 
+// ---------------------------------------------------------------- ring variant
+//
+// The full update's epilogue (C in the pair-blocked layout, z [N][N][c_z]).
+// Same work split and arithmetic as k3_epilogue_mfma, but C, z and the mask
+// bytes of the next unit arrive by direct-to-LDS loads into a 2-stage ring
+// while the current unit is computed, and the bf16 activations are written
+// back into the stage they were read from.  Every wave issues 7 loads and a
+// fixed number of range-checked buffer stores per unit (tail pairs are
+// dropped by the range check), so the vmcnt waits are constants.
+//
+// Stage layout (bytes):
+//   [0, 16384)      C of the unit, [128 channels][32 pairs] fp32: chunk q
+//                   (pairs 4q .. 4q + 3) of channel row c at slot q ^ (c & 7);
+//                   afterwards y_hi [0, 8192) and y_lo [8192, 16384)
+//   [16384, 24576)  z of the unit, [32 pairs][128] bf16: chunk q of pair row p
+//                   at slot q ^ (p & 1); afterwards x_hi
+//   [24576, 25600)  per-wave mask bytes: m[j0 .. j0 + 31] at 0, the dword of
+//                   m[i] at 32 (0/1 bytes, zero past N)
+constexpr int kRC = 16384, kRZ = 8192, kRM = 1024;
+constexpr int kRSt = kRC + kRZ + kRM;
+
+template <typename TO>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
+void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z, const uint8_t* __restrict__ tmask,
+                      int N, int nunits, TO* __restrict__ out, const bf16_t* __restrict__ wepi,
+                      const float* __restrict__ lnin_w, const float* __restrict__ lnin_b,
+                      const float* __restrict__ lnout_w, const float* __restrict__ lnout_b, float eps) {
+    __shared__ __attribute__((aligned(16))) char ring[2 * kRSt];
+    __shared__ __attribute__((aligned(16))) float prm[4][128];               // LN gains and biases
+    __shared__ __attribute__((aligned(16))) float os[kP3 * kOsRow];          // outputs as [p][d]
+    const int t = threadIdx.x, lane = t & 63;
+    const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int lp = t >> 3, lq = t & 7;     // LayerNorms: pair lp, 8 lanes per pair
+    const int G = gridDim.x;
+    const int first = (G & 7) == 0 ? (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+    const int nchunk = (N + kP3 - 1) / kP3;
+    constexpr int kStores = (int)(kP3 * kCz * sizeof(TO)) / (4 * 1024);   // 16-byte stores per lane per unit
+
+    // Ring fill.  C: load k of wave w covers channel rows 8 (4 w + k) .. + 7,
+    // lane -> row + lane / 8, slot lane % 8.  z and mask as in the projection.
+    const uint32_t ring_base = lds_addr(ring);
+    const uint32_t cvo = (uint32_t)((lane >> 3) * 128 + (((lane & 7) ^ (lane >> 3)) << 4)) + (uint32_t)w * 4096;
+    const int drow = w * 8 + (lane >> 4);
+    const uint32_t dchunk = (uint32_t)(((lane & 15) ^ (drow & 1)) << 4);
+    const uint32_t dv0 = (uint32_t)drow * kYRow + dchunk, dv1 = (uint32_t)(drow + 4) * kYRow + dchunk;
+    const uint32_t mpad = (uint32_t)((N + 31) / 32 * 32);
+    auto decode = [&](int u, int& i, int& j0) {
+        i = u / nchunk;
+        j0 = (u - i * nchunk) * kP3;
+    };
+    auto issue = [&](int u, int stage) {
+        const bool valid = u < nunits;
+        int i = 0, j0 = 0;
+        if (valid) decode(u, i, j0);
+        const int np = valid ? min(kP3, N - j0) : 0;
+        const uint32_t st = ring_base + (uint32_t)(stage * kRSt);
+        const v4i_t rc = buffer_desc(C + result_off(nchunk, kCh, 0, i, j0), valid ? (uint32_t)kRC : 0u);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) lds_load16(rc, cvo + k * 1024, 0, st + w * 4096 + k * 1024);
+        const v4i_t rz = buffer_desc(z + ((int64_t)i * N + j0) * kCz, (uint32_t)np * kYRow);
+        lds_load16(rz, dv0, 0, st + kRC + w * 2048);
+        lds_load16(rz, dv1, 0, st + kRC + w * 2048 + 1024);
+        const v4i_t rm = buffer_desc(tmask, valid ? mpad : 0u);
+        const uint32_t mo = lane < 8 ? (uint32_t)(j0 + 4 * lane) : lane == 8 ? (uint32_t)(i & ~3) : 0xfffffff0u;
+        lds_load4(rm, mo, 0, st + kRC + kRZ + w * 256);
+    };
+    issue(first, 0);
+
+    bf16x8_t wo[8], wg[8];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+        const size_t col = (size_t)ks * 16 + 8 * (lane >> 5);
+        wo[ks] = *reinterpret_cast<const bf16x8_t*>(wepi + (size_t)(w * 32 + (lane & 31)) * 128 + col);
+        wg[ks] = *reinterpret_cast<const bf16x8_t*>(wepi + (size_t)(128 + w * 32 + (lane & 31)) * 128 + col);
+    }
+    if (t < 128) {
+        prm[0][t] = lnout_w[t];
+        prm[1][t] = lnout_b[t];
+        prm[2][t] = lnin_w[t];
+        prm[3][t] = lnin_b[t];
+    }
+
+    for (int it = 0, u = first; u < nunits; ++it, u += G) {
+        // Wait for this unit's loads: issued after them are only the stores
+        // of the previous unit.
+        if (it == 0) wait_vmcnt_pinned<0>();
+        else wait_vmcnt_pinned<kStores>();
+        __syncthreads();
+        issue(u + G, (it + 1) & 1);   // into the stage of the previous unit
+        char* st = ring + (it & 1) * kRSt;
+
+        // LN_out over the 128 hidden channels of pair lp (lane lq holds
+        // c = lq + 8 k) and LN_in over the 128 pair channels (lane lq holds
+        // 16 lq .. 16 lq + 15), both from the stage.
+        float v[16];
+        {
+            const char* crow = st + (((lp >> 2) ^ lq) << 4) + (lp & 3) * 4;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) v[k] = *reinterpret_cast<const float*>(crow + (lq + 8 * k) * 128);
+        }
+        float zv[16];
+        {
+            const char* zr = st + kRC + lp * kYRow;
+            const uint4 z0 = *reinterpret_cast<const uint4*>(zr + (((2 * lq) ^ (lp & 1)) << 4));
+            const uint4 z1 = *reinterpret_cast<const uint4*>(zr + (((2 * lq + 1) ^ (lp & 1)) << 4));
+            const uint32_t uu[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                zv[2 * k] = __uint_as_float(uu[k] << 16);
+                zv[2 * k + 1] = __uint_as_float(uu[k] & 0xffff0000u);
+            }
+        }
+        const uint8_t* ms = reinterpret_cast<const uint8_t*>(st + kRC + kRZ + w * 256);
+        int ui, uj0;
+        decode(u, ui, uj0);
+        const uint32_t mrow = ms[32 + (ui & 3)];
+        __syncthreads();   // every thread has read its C and z; the stage becomes y_hi, y_lo, x_hi
+
+        {
+            float s1 = 0.f;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) s1 += v[k];
+            s1 = sum_lanes8(s1);
+            const float mu = s1 * (1.0f / kCh);
+            float q2 = 0.f;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                v[k] -= mu;
+                q2 += v[k] * v[k];
+            }
+            q2 = sum_lanes8(q2);
+            const float rs = rsqrtf(q2 * (1.0f / kCh) + eps);
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                const int c = lq + 8 * k;
+                const float y = v[k] * rs * prm[0][c] + prm[1][c];
+                const bf16_t h = f2bf(y);
+                const uint32_t o = yoff(lp, c >> 3) + 2 * (c & 7);
+                *reinterpret_cast<bf16_t*>(st + o) = h;
+                *reinterpret_cast<bf16_t*>(st + 8192 + o) = f2bf(y - bf2f(h));
+            }
+        }
+        {
+            float s1 = 0.f;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) s1 += zv[k];
+            s1 = sum_lanes8(s1);
+            const float mu = s1 * (1.0f / kCz);
+            float q2 = 0.f;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                zv[k] -= mu;
+                q2 += zv[k] * zv[k];
+            }
+            q2 = sum_lanes8(q2);
+            const float rs = rsqrtf(q2 * (1.0f / kCz) + eps);
+            uint32_t hx[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int c = 16 * lq + 2 * k;
+                hx[k] = pack_bf16x2(zv[2 * k] * rs * prm[2][c] + prm[3][c], zv[2 * k + 1] * rs * prm[2][c + 1] + prm[3][c + 1]);
+            }
+            *reinterpret_cast<uint4*>(st + kRC + yoff(lp, 2 * lq)) = make_uint4(hx[0], hx[1], hx[2], hx[3]);
+            *reinterpret_cast<uint4*>(st + kRC + yoff(lp, 2 * lq + 1)) = make_uint4(hx[4], hx[5], hx[6], hx[7]);
+        }
+        __syncthreads();
+
+        f32x16_t ay, ag;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ay[r] = ag[r] = 0.f;
+        const int ap = lane & 31;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            const uint32_t o = yoff(ap, 2 * ks + (lane >> 5));
+            const bf16x8_t yh = *reinterpret_cast<const bf16x8_t*>(st + o);
+            const bf16x8_t yl = *reinterpret_cast<const bf16x8_t*>(st + 8192 + o);
+            const bf16x8_t xh = *reinterpret_cast<const bf16x8_t*>(st + kRC + o);
+            ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yh, wo[ks], ay, 0, 0, 0);
+            ag = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, wg[ks], ag, 0, 0, 0);
+            ay = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yl, wo[ks], ay, 0, 0, 0);
+        }
+
+        // Lane holds output channel 32 w + (lane & 31); register r holds pair
+        // 8 (r / 4) + 4 (lane / 32) + r % 4.  The staged mask is zero past N,
+        // so tail pairs come out as zeros (and are not stored).
+        const int d = w * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int p = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            const uint32_t keep = (ms[p] & mrow) ? 0xffffffffu : 0u;
+            os[p * kOsRow + d] = __uint_as_float(__float_as_uint(sigmoidf_(ag[r]) * ay[r]) & keep);
+        }
+        __syncthreads();
+
+        // The unit's [32 pairs][128] block is contiguous in out: store k of
+        // the work-group covers its bytes [4096 k, 4096 k + 4096), 16 per
+        // thread; bytes past the row's last pair fall outside the descriptor.
+        const int np = min(kP3, N - uj0);
+        const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * N + uj0) * kCz,
+                                                    (uint32_t)(np * kCz * (int)sizeof(TO)));
+#pragma unroll
+        for (int k = 0; k < kStores; ++k) {
+            const uint32_t off = (uint32_t)(k * 4096 + t * 16);
+            uint4 pk;
+            if (sizeof(TO) == 4) {
+                const int p = off / 512, d4 = (off % 512) / 4;
+                pk = __builtin_bit_cast(uint4, *reinterpret_cast<const float4*>(&os[p * kOsRow + d4]));
+            } else {
+                const int p = off / 256, d8 = (off % 256) / 2;
+                const float4 f0 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8]);
+                const float4 f1 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8 + 4]);
+                pk = make_uint4(pack_bf16x2(f0.x, f0.y), pack_bf16x2(f0.z, f0.w), pack_bf16x2(f1.x, f1.y),
+                                pack_bf16x2(f1.z, f1.w));
+            }
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i_t, pk), ro, off, 0, 0);
+        }
+    }
+    wait_vmcnt_pinned<0>();   // the ring load past the last unit lands before the work-group ends
+}
+
 template <typename T, typename TO>
 hipError_t launch_valu(const DeviceWeights& w, const EpilogueArgs& a, hipStream_t s) {
     const int64_t nchunk = (a.cols + kPairs - 1) / kPairs;
@@ -331,10 +551,13 @@ hipError_t launch_mfma(const DeviceWeights& w, const EpilogueArgs& a, hipStream_
     const int64_t cap = 2 * (int64_t)w.cus;
     const unsigned g = (unsigned)(nunits < cap ? nunits : cap);
     const bool vec = (a.ldc % 4) == 0 && (a.sc % 4) == 0 && (reinterpret_cast<uintptr_t>(a.C) & 15u) == 0;
-    if (a.cblocked)
-        hipLaunchKernelGGL((k3_epilogue_mfma<TO, true, true>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
-                           w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
-    else if (vec)
+    if (a.cblocked) {   // the full update: rows = cols = N, row0 = col0 = 0
+        hipError_t e = launch_stage_kmask(a.mask, a.cols, w.kmask_pad, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k3_epilogue_ring<TO>), dim3(g), dim3(256), 0, s, a.C, (const bf16_t*)a.z, w.kmask_pad,
+                           (int)a.cols, (int)nunits, (TO*)a.out, w.epi_bf, w.ln_in_w, w.ln_in_b, w.ln_out_w,
+                           w.ln_out_b, w.eps);
+    } else if (vec)
         hipLaunchKernelGGL((k3_epilogue_mfma<TO, true, false>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
                            w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);
     else

@@ -46,8 +46,8 @@ struct EpilogueArgs {
 };
 
 // K1: LN_in + gated projections + pair mask -> channel-major operands A, B in
-// the blocked panel layout (common.h) of N rows and K = N.  Elements of the
-// padding (rows or k >= N) are left untouched.
+// the blocked panel layout (common.h) of N rows and K = N.  Padding rows are
+// left untouched; the k padding of a row's last k-step is written with zeros.
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
                           int64_t N, int incoming, void* A, void* B, hipStream_t s);
 
