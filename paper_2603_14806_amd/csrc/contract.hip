@@ -36,16 +36,17 @@ constexpr int BN = 256, BK = 32;
 constexpr int ROWB = BK * 2;                    // 64 bytes per row per stage
 constexpr int B_ST = BN * ROWB;                 // 16 KB
 constexpr int MASK_ST = 4 * 256;                // per-wave k-mask bytes (KMASK only)
+constexpr int kLdsBytes = 160 * 1024;           // gfx950 LDS per work-group
 
 // Tile geometry for BM output rows per work-group (256 or 384): each wave owns
 // BM/2 x 128 outputs = MI x 4 MFMA blocks, and loads LA blocks of 16 A rows
 // and 4 blocks of 16 B rows per k-step.
-template <int BM> struct Geo {
+template <int BM, bool KMASK> struct Geo {
     static constexpr int MI = BM / 64;
     static constexpr int LA = BM / 64;
     static constexpr int A_ST = BM * ROWB;
-    static constexpr int ST_BYTES = A_ST + B_ST + MASK_ST;
-    static constexpr int STAGES = (160 * 1024) / ST_BYTES >= 4 ? 4 : 3;
+    static constexpr int ST_BYTES = A_ST + B_ST + (KMASK ? MASK_ST : 0);
+    static constexpr int STAGES = kLdsBytes / ST_BYTES >= 5 ? 5 : kLdsBytes / ST_BYTES >= 4 ? 4 : 3;
 };
 
 template <int BM, bool KMASK, bool BLOCKED>
@@ -54,7 +55,7 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
                       int M, int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB,
                       int64_t sC, int tiles_m, int tiles_n, int total, int accumulate,
                       const uint8_t* __restrict__ kmask) {
-    using GG = Geo<BM>;
+    using GG = Geo<BM, KMASK>;
     constexpr int MI = GG::MI, LA = GG::LA, A_ST = GG::A_ST, ST_BYTES = GG::ST_BYTES, STAGES = GG::STAGES;
     constexpr int NPART = LA + 4;                // buffer loads of A and B per wave per step
     __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
@@ -166,7 +167,8 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
         for (int kt = 0; kt < nk; ++kt) {
             const int s = it * nk + kt;
             const int ahead = min(STAGES - 2, steps - 1 - s);   // later steps already in flight
-            if (ahead >= 2) wait_vmcnt<2 * LOADS>();
+            if (ahead >= 3) wait_vmcnt<3 * LOADS>();
+            else if (ahead == 2) wait_vmcnt<2 * LOADS>();
             else if (ahead == 1) wait_vmcnt<LOADS>();
             else wait_vmcnt<0>();
             __syncthreads();
