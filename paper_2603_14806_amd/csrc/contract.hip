@@ -18,10 +18,11 @@ namespace {
 //
 // Persistent kernel: one work-group (4 waves) per CU, each looping over
 // 256 x 256 output tiles; a wave owns a 128 x 128 sub-tile = 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16.  The k loop runs in steps of 32 through a
-// 4-stage LDS ring (32 KB per stage) filled by direct-to-LDS buffer loads
-// (no VGPR staging), three steps ahead of the step being multiplied.  The
-// ring flows straight from one output tile into the next.
+// v_mfma_f32_32x32x16_bf16.  The k loop runs in steps of 32 through an LDS
+// ring of 32 KB stages (5 stages without a k-mask, 4 with one) filled by
+// direct-to-LDS buffer loads (no VGPR staging), STAGES - 1 steps ahead of
+// the step being multiplied.  The ring flows straight from one output tile
+// into the next.
 //
 // Tile order: in round r the work-groups on XCD x take 32 consecutive
 // logical tiles, i.e. a 4 x 8 block of one channel, so the A row panels and B
@@ -120,13 +121,18 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
     };
     // Part j of the next step's fetch: j < LA are A row blocks, then 4 B row
     // blocks (16 rows each per wave); part NPART is the k-mask.
-    auto issue_part = [&](int j) {
+    // With live == false the part is still issued, through a zero-size
+    // descriptor: it reads nothing, and keeps the k loop free of branches.
+    // (Past the last step the cursor no longer advances, so such loads go to
+    // the stage after the last fetched step, which no later step uses.)
+    const v4i_t rnone = buffer_desc(A, 0u);
+    auto issue_part = [&](int j, bool live) {
         const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
-        if (j < LA) lds_load16(ra, va, j * a_j + l_kt * a_k, st + (wave * (BM / 4) + 16 * j) * ROWB);
+        if (j < LA) lds_load16(live ? ra : rnone, va, j * a_j + l_kt * a_k, st + (wave * (BM / 4) + 16 * j) * ROWB);
         else if (j < NPART)
-            lds_load16(rb, vb, (j - LA) * b_j + l_kt * b_k, st + A_ST + (wave * 64 + 16 * (j - LA)) * ROWB);
+            lds_load16(live ? rb : rnone, vb, (j - LA) * b_j + l_kt * b_k, st + A_ST + (wave * 64 + 16 * (j - LA)) * ROWB);
         else if (KMASK)   // bytes [kt*32, kt*32 + 256) of the staged k-mask; past its end reads as 0
-            lds_load4(rmask, (uint32_t)lane * 4, (uint32_t)l_kt * BK, st + A_ST + B_ST + wave * 256);
+            lds_load4(live ? rmask : rnone, (uint32_t)lane * 4, (uint32_t)l_kt * BK, st + A_ST + B_ST + wave * 256);
     };
     auto advance = [&]() {
         l_stage = l_stage == STAGES - 1 ? 0 : l_stage + 1;
@@ -137,7 +143,7 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
     };
     auto issue_next = [&]() {
 #pragma unroll
-        for (int j = 0; j <= NPART; ++j) issue_part(j);
+        for (int j = 0; j <= NPART; ++j) issue_part(j, true);
         advance();
     };
 
@@ -224,17 +230,13 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
                 if (x & 1) {
                     const int y = x >> 1;   // 0 .. 2 MI - 1 >= NPART - 1
-                    __builtin_amdgcn_sched_barrier(0);
-                    if (fetch && y < NPART) issue_part(y);
+                    if (y < NPART) issue_part(y, fetch);
                     if (y < 4) b1[y] = *reinterpret_cast<const bf16x8_t*>(st + rdB[1] + y * 32 * ROWB);
                     else if (y < 4 + MI) a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
-                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
-            if (fetch) {
-                if (KMASK) issue_part(NPART);
-                advance();
-            }
+            if (KMASK) issue_part(NPART, fetch);
+            if (fetch) advance();
             if (KMASK || tail) mask_frags(1, a1, b1);
 #pragma unroll
             for (int x = 0; x < 4 * MI; ++x) {
@@ -270,6 +272,7 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
                     }
                 }
     }
+    wait_vmcnt<0>();   // the zero-size loads of the last steps land before the work-group ends
 }
 
 // ---------------------------------------------------------------- fp32 VALU
