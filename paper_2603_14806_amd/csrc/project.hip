@@ -98,7 +98,7 @@ __global__ __launch_bounds__(256) void k1_project_valu(
 // z and the token mask reach LDS through a 3-stage ring filled by
 // direct-to-LDS buffer loads two lines ahead of the line being computed, so
 // the HBM latency of z hides behind two lines of work.  Every wave issues
-// the same number of vector-memory instructions per line (3 loads, 8 stores,
+// the same number of vector-memory instructions per line (3 loads, 4 stores,
 // tails included), which makes the vmcnt waits exact constants.
 //
 // Precision: the LayerNormed input x (fp32) is split into x_hi = bf16(x) and
@@ -181,19 +181,19 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         gb[1][t] = lnb[t];
     }
     const PanelGeom pg = panel_geom(N, N);
-    // Store mapping: thread t writes pairs 4 (t & 7) .. 4 (t & 7) + 3 of
-    // channel (t >> 3) + 32 (i & 3) of A (i < 4) or B (i >= 4).
+    // Store mapping: thread t writes pairs 8 (t & 3) .. 8 (t & 3) + 7 of
+    // channel (t >> 2) + 64 (i & 1) of A (i < 2) or B (i >= 2).
     const int64_t ch_stride = panel_elems(pg);
-    const int64_t st_lane = (t >> 3) * ch_stride + 4 * (t & 7);
+    const int64_t st_lane = (t >> 2) * ch_stride + 8 * (t & 3);
 
     int stage = 0;
     for (int it = 0, line = first; line < nlines; ++it, line += G) {
         // Vector-memory instructions issued after this line's loads: the
-        // next line's loads (3) and, from the second line on, the 8 stores
+        // next line's loads (3) and, from the second line on, the 4 stores
         // of every line in between.
         if (it == 0) wait_vmcnt_pinned<3>();
-        else if (it == 1) wait_vmcnt_pinned<3 + 8>();
-        else wait_vmcnt_pinned<3 + 8 + 8>();
+        else if (it == 1) wait_vmcnt_pinned<3 + 4>();
+        else wait_vmcnt_pinned<3 + 4 + 4>();
         __syncthreads();
         issue(line + 2 * G, stage == 0 ? 2 : stage - 1);   // into the stage read one line ago
         const char* zs = ring + stage * kSt;
@@ -278,17 +278,19 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         }
         __syncthreads();
 
-        // Channel-major stores: 8 lanes write the 32 pairs (64 bytes) of one
+        // Channel-major stores: 4 lanes write the 32 pairs (64 bytes) of one
         // panel row, one k-step of the blocked layout.  A ragged line's tail
         // writes zeros into the k padding of its step, so every wave issues
-        // exactly 8 stores per line.
+        // exactly 4 stores per line.
         const int64_t line_off = panel_off(pg, 0, r0, k0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int ab = i >> 2, c = (t >> 3) + 32 * (i & 3);
-            const float4 f = *reinterpret_cast<const float4*>(&os[ab][c][4 * (t & 7)]);
-            bf16_t* dst = (ab ? B : A) + (line_off + st_lane + 32 * (i & 3) * ch_stride);
-            *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(f.x, f.y), pack_bf16x2(f.z, f.w));
+        for (int i = 0; i < 4; ++i) {
+            const int ab = i >> 1, c = (t >> 2) + 64 * (i & 1);
+            const float4 f0 = *reinterpret_cast<const float4*>(&os[ab][c][8 * (t & 3)]);
+            const float4 f1 = *reinterpret_cast<const float4*>(&os[ab][c][8 * (t & 3) + 4]);
+            bf16_t* dst = (ab ? B : A) + (line_off + st_lane + 64 * (i & 1) * ch_stride);
+            *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(f0.x, f0.y), pack_bf16x2(f0.z, f0.w),
+                                                        pack_bf16x2(f1.x, f1.y), pack_bf16x2(f1.z, f1.w));
         }
     }
     wait_vmcnt_pinned<0>();   // the ring loads past the last line land before the work-group ends
