@@ -206,3 +206,89 @@ def block_epilogue(C_tile, z_tile, row_mask, col_mask, W, eps=EPS):
     m = pair_mask(row_mask, col_mask)
     _, _, g = project(z_tile, m, W, eps)
     return epilogue(C_tile, g, m, W, eps)
+
+
+# ---------------------------------------------------------------- backward
+#
+# Gradients of the update for training.  The paper gives every distributed
+# module an explicit backward pass that runs the same ring schedule as its
+# forward (Section 3.1); for this layer the backward of the contraction is two
+# more per-channel products of the same size.  Chain rule of the forward
+# above, written out step by step.
+
+
+def layer_norm_backward(dy, v, gamma, eps=EPS):
+    """For y = (v - mu) / sqrt(var + eps) * gamma + beta over the last axis,
+    given dL/dy return (dL/dv, dL/dgamma, dL/dbeta), the parameter gradients
+    summed over all leading axes."""
+    v = f64(v)
+    dy = f64(dy)
+    mu = v.mean(axis=-1, keepdims=True)
+    d = v - mu
+    rs = 1.0 / np.sqrt((d * d).mean(axis=-1, keepdims=True) + eps)
+    xh = d * rs                                   # the normalised vector
+    dxh = dy * f64(gamma)
+    dv = rs * (dxh - dxh.mean(axis=-1, keepdims=True) - xh * (dxh * xh).mean(axis=-1, keepdims=True))
+    lead = tuple(range(dy.ndim - 1))
+    return dv, (dy * xh).sum(axis=lead), dy.sum(axis=lead)
+
+
+def contract_backward(A, B, dC):
+    """Backward of the per-channel contraction C[c] = A[c] @ B[c]^T (the form
+    both directions take on the channel-major operands): given dL/dC return
+        dA[c] = dC[c] @ B[c],   dB[c] = dC[c]^T @ A[c].
+    A: [c][n][K], B: [c][m][K], dC: [c][n][m]."""
+    A, B, dC = f64(A), f64(B), f64(dC)
+    return dC @ B, dC.transpose(0, 2, 1) @ A
+
+
+def tri_mul_backward(z, mask, W, direction, dout, eps=EPS):
+    """Gradients of sum(out * dout) for the whole update (all pairs).
+
+    Returns a dict: "dz" [N][N][c_z] and one entry per weight name of
+    WEIGHT_NAMES (same shapes as the weights; gradients summed over pairs)."""
+    z = f64(z)
+    dout = f64(dout)
+    m = pair_mask(mask)[..., None]
+    x = layer_norm(z, W["ln_in_w"], W["ln_in_b"], eps)
+    pa, ga = linear(x, W["w_a"]), linear(x, W["w_ga"])
+    pb, gb = linear(x, W["w_b"]), linear(x, W["w_gb"])
+    sa, sb = sigmoid(ga), sigmoid(gb)
+    a, b = m * sa * pa, m * sb * pb
+    sg = sigmoid(linear(x, W["w_g"]))
+    if direction == "outgoing":
+        C = contract_outgoing(a, b)
+    elif direction == "incoming":
+        C = contract_incoming(a, b)
+    else:
+        raise ValueError(direction)
+    y = layer_norm(C, W["ln_out_w"], W["ln_out_b"], eps)
+    u = linear(y, W["w_o"])
+
+    cz, c = u.shape[-1], y.shape[-1]
+    g = {}
+    du = dout * m * sg                            # out = m * sg * u
+    dgg = dout * m * u * sg * (1.0 - sg)          # d/d(W_g x) through the logistic
+    g["w_o"] = du.reshape(-1, cz).T @ y.reshape(-1, c)
+    dy = du @ f64(W["w_o"])
+    dC, g["ln_out_w"], g["ln_out_b"] = layer_norm_backward(dy, C, W["ln_out_w"], eps)
+
+    # contraction: outgoing C = A B^T with A[c][i][k] = a[i][k][c]; incoming
+    # with A[c][i][k] = a[k][i][c] -- the same channel-major form.
+    dCc = dC.transpose(2, 0, 1)
+    if direction == "outgoing":
+        dA, dB = contract_backward(a.transpose(2, 0, 1), b.transpose(2, 0, 1), dCc)
+        da, db = dA.transpose(1, 2, 0), dB.transpose(1, 2, 0)
+    else:
+        dA, dB = contract_backward(a.transpose(2, 1, 0), b.transpose(2, 1, 0), dCc)
+        da, db = dA.transpose(2, 1, 0), dB.transpose(2, 1, 0)
+
+    dpa, dga = da * m * sa, da * m * pa * sa * (1.0 - sa)
+    dpb, dgb = db * m * sb, db * m * pb * sb * (1.0 - sb)
+    xf = x.reshape(-1, x.shape[-1])
+    for name, d in (("w_a", dpa), ("w_ga", dga), ("w_b", dpb), ("w_gb", dgb), ("w_g", dgg)):
+        g[name] = d.reshape(-1, d.shape[-1]).T @ xf
+    dx = (dpa @ f64(W["w_a"]) + dga @ f64(W["w_ga"]) + dpb @ f64(W["w_b"]) + dgb @ f64(W["w_gb"])
+          + dgg @ f64(W["w_g"]))
+    g["dz"], g["ln_in_w"], g["ln_in_b"] = layer_norm_backward(dx, z, W["ln_in_w"], eps)
+    return g
