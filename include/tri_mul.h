@@ -197,6 +197,37 @@ int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_pan
 int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z,
                      const uint8_t* mask, int64_t N, void* out, void* stream);
 
+/* ---------------------------------------------------------------- backward
+ *
+ * Backward of the contraction, for training (Section 3.1: every distributed
+ * module has an explicit backward running the same schedule as its forward).
+ * With the operands of tri_mul_contract, C_c = A_c * B_c^T for every channel
+ * c, and L a loss with gradient dC = dL/dC:
+ *
+ *     dA_c = dC_c * B_c          dB_c = dC_c^T * A_c
+ *
+ * The operands are direction-agnostic: for the incoming update, A and B are
+ * the incoming panels (tri_mul_project with TRI_MUL_INCOMING), and the
+ * caller maps dA back to a by the same transposition.
+ *
+ * tri_mul_contract_backward_workspace_size: bytes of device workspace for N
+ * tokens (four operands in the panel layout, 256-byte aligned each).
+ * *bytes is a HOST pointer. */
+int tri_mul_contract_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
+
+/* tri_mul_contract_backward:
+ *   dC        float32, result layout of tri_mul_contract (N x J x 32 x c floats)
+ *   a_panels, b_panels   dtype, panel layout (as written by tri_mul_project)
+ *   dA        float32, result layout over (i, k): element (ch, i, k) at
+ *             ((i * J + k / 32) * c + ch) * 32 + k % 32; overwritten
+ *   dB        float32, result layout over (j, k); overwritten
+ *   ws        workspace of >= tri_mul_contract_backward_workspace_size bytes,
+ *             256-byte aligned; must not alias any other argument
+ * In the bf16 path dC is rounded to bf16 for the products (fp32
+ * accumulation).  Returns TRI_MUL_ENOMEM if ws_bytes is too small. */
+int tri_mul_contract_backward(tri_mul_handle_t h, const float* dC, const void* a_panels, const void* b_panels,
+                              int64_t N, float* dA, float* dB, void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

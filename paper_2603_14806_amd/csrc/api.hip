@@ -328,6 +328,46 @@ int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z, const
     return ok();
 }
 
+int tri_mul_contract_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    *bytes = 4 * round256(panel_bytes(N, h->c, h->dtype));
+    return ok();
+}
+
+int tri_mul_contract_backward(tri_mul_handle_t h, const float* dC, const void* a_panels, const void* b_panels,
+                              int64_t N, float* dA, float* dB, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!dC || !a_panels || !b_panels || !dA || !dB || !ws) return fail(TRI_MUL_EINVAL, "null pointer argument");
+    if (!aligned16(dC) || !aligned16(a_panels) || !aligned16(b_panels) || !aligned16(dA) || !aligned16(dB))
+        return fail(TRI_MUL_EINVAL, "tensors must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
+    size_t need = 0;
+    if (int rc = tri_mul_contract_backward_workspace_size(h, N, &need)) return rc;
+    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed for N = %lld", ws_bytes, need, (long long)N);
+    const size_t panel = round256(panel_bytes(N, h->c, h->dtype));
+    char* base = static_cast<char*>(ws);
+    void* dCp = base;               // dC as operand rows i, k = j
+    void* dCt = base + panel;       // dC^T: rows j, k = i
+    void* At = base + 2 * panel;    // A^T
+    void* Bt = base + 3 * panel;    // B^T
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int cus = h->w.cus;
+    hipError_t e = trimul::launch_result_to_panel(h->dtype, dC, dCp, N, cus, s);
+    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, dCp, dCt, N, cus, s);
+    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, a_panels, At, N, cus, s);
+    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, b_panels, Bt, N, cus, s);
+    if (e != hipSuccess) return hip_fail(e, "backward layout kernel launch");
+    // dA[i][k] = sum_j dC[i][j] B^T[k][j];  dB[j][k] = sum_i dC^T[j][i] A^T[k][i]
+    e = trimul::launch_contract(h->dtype, 1, dCp, Bt, dA, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    if (e == hipSuccess)
+        e = trimul::launch_contract(h->dtype, 1, dCt, At, dB, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    if (e != hipSuccess) return hip_fail(e, "backward contraction kernel launch");
+    return ok();
+}
+
 int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
                              const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
                              void* out_tile, void* stream) {

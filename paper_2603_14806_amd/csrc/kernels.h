@@ -64,4 +64,9 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
 hipError_t launch_epilogue(int dtype, int out_dtype, const DeviceWeights& w, const EpilogueArgs& a,
                            hipStream_t s);
 
+// Backward of the contraction: the fp32 result layout -> a panel (dtype
+// elements), and the per-channel panel transpose X_c[i][k] -> X_c[k][i].
+hipError_t launch_result_to_panel(int dtype, const float* R, void* P, int64_t N, int cus, hipStream_t s);
+hipError_t launch_panel_transpose(int dtype, const void* X, void* Y, int64_t N, int cus, hipStream_t s);
+
 }  // namespace trimul

@@ -47,6 +47,8 @@ SIGNATURES = {
     "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
+    "tri_mul_contract_backward_workspace_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_contract_backward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
 }
 
 _lib = None
@@ -151,6 +153,17 @@ def tri_mul_epilogue(h, c_in, z, mask, N, out, stream=None):
     _check(lib().tri_mul_epilogue(h, _ptr(c_in), _ptr(z), _ptr(mask), N, _ptr(out), _stream(stream)))
 
 
+def tri_mul_contract_backward_workspace_size(h, N):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_contract_backward_workspace_size(h, N, ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_contract_backward(h, dC, a_panels, b_panels, N, dA, dB, ws, ws_bytes, stream=None):
+    _check(lib().tri_mul_contract_backward(h, _ptr(dC), _ptr(a_panels), _ptr(b_panels), N, _ptr(dA), _ptr(dB),
+                                           _ptr(ws), ws_bytes, _stream(stream)))
+
+
 # ---------------------------------------------------------------- wrapper
 
 class TriMul:
@@ -229,6 +242,17 @@ class TriMul:
         out = self._out(N, out)
         tri_mul_epilogue(self.h, C, z, mask, N, out, stream)
         return out
+
+    def contract_backward(self, dC, A, B, N, stream=None):
+        """Gradients of the contraction: dC in the result layout, A, B in the
+        panel layout; returns (dA, dB), both in the result layout (flat)."""
+        n = N * (-(-N // 32) * 32) * 128
+        dA = torch.empty(n, dtype=torch.float32, device=self.device)
+        dB = torch.empty(n, dtype=torch.float32, device=self.device)
+        wsb = tri_mul_contract_backward_workspace_size(self.h, N)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
+        tri_mul_contract_backward(self.h, dC, A, B, N, dA, dB, ws, wsb, stream)
+        return dA, dB
 
     def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None):
         tri_mul_block_accumulate(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream)
