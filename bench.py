@@ -180,6 +180,22 @@ def main():
     torch.cuda.synchronize()
     full_ms = f0.elapsed_time(f1) / 2
 
+    # the contraction backward (training), outside the timed region: both
+    # gradients of one direction, with C standing in for dC
+    dA, dB = torch.empty_like(C), torch.empty_like(C)
+    bws_n = T.tri_mul_contract_backward_workspace_size(h, N)
+    bws = torch.empty(bws_n, dtype=torch.uint8, device=dev)
+    T.tri_mul_contract_backward(h, C, A, B, N, dA, dB, bws, bws_n, stream)
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record(stream)
+    for _ in range(3):
+        T.tri_mul_contract_backward(h, C, A, B, N, dA, dB, bws, bws_n, stream)
+    b1.record(stream)
+    torch.cuda.synchronize()
+    bwd_ms = b0.elapsed_time(b1) / 3
+    del dA, dB, bws
+    print(f"[bench] contraction backward {bwd_ms:.3f} ms", file=sys.stderr, flush=True)
+
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
     layer_flops = 2 * fl["total"]
@@ -206,9 +222,13 @@ def main():
             "epilogue": {"ms": round(k_ms["epilogue"], 4),
                          "GB_per_s": round(by["epilogue"] / (k_ms["epilogue"] * 1e-3) / 1e9, 1)},
         },
+        "backward_contract": {"ms": round(bwd_ms, 4),
+                              "TFLOP_per_s": round(2 * fl["contract"] / (bwd_ms * 1e-3) / 1e12, 2),
+                              "what": "dA = dC B and dB = dC^T A for all 128 channels (one direction), "
+                                      "including the layout kernels; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(), "kernel": "k2_contract_mfma",
+                     "traffic": measured_traffic(), "kernel": "k2_contract_w8",
                      "per_launch": f"2*N^3*c = {fl['contract']:.4e} flop (128 channels of one {N}^3 product)"},
         "cpu_baseline": None,
     }
