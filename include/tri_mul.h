@@ -228,6 +228,38 @@ int tri_mul_contract_backward_workspace_size(tri_mul_handle_t h, int64_t N, size
 int tri_mul_contract_backward(tri_mul_handle_t h, const float* dC, const void* a_panels, const void* b_panels,
                               int64_t N, float* dA, float* dB, void* ws, size_t ws_bytes, void* stream);
 
+/* Gradients of the whole update (bf16 storage path), for training.  Given
+ * dout = dL/dout (same layout and dtype as the forward's out), the call
+ * recomputes the forward from z and returns dz = dL/dz and the gradients of
+ * all ten weight tensors:
+ *   grads   HOST struct of DEVICE pointers, float32, shapes as in
+ *           tri_mul_params_t ([out][in] for the linear maps); overwritten
+ *           (sums over all pairs)
+ *   dz      [N][N][c_z] dtype; overwritten
+ *   ws      workspace of >= tri_mul_backward_workspace_size bytes, 256-byte
+ *           aligned; must not alias any other argument
+ * Pairs with m_ij = 0 receive dz = 0 and contribute nothing.  Returns
+ * TRI_MUL_EUNSUPPORTED for the float32 storage path, TRI_MUL_ENOMEM if
+ * ws_bytes is too small. */
+typedef struct {
+    float* ln_in_w;
+    float* ln_in_b;
+    float* w_a;
+    float* w_ga;
+    float* w_b;
+    float* w_gb;
+    float* w_g;
+    float* ln_out_w;
+    float* ln_out_b;
+    float* w_o;
+} tri_mul_grads_t;
+
+int tri_mul_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
+int tri_mul_outgoing_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
+                              void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream);
+int tri_mul_incoming_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
+                              void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

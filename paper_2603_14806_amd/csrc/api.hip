@@ -135,6 +135,83 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
     return ok();
 }
 
+// Workspace of the layer backward (bf16 path), in this order: A, B and the
+// four operands of the contraction backward (panels), C, dA, dB (result
+// layout), dx_g [N*N][c_z] fp32, nine unit-block tensors, and the partial
+// sums of the weight-gradient reductions.
+struct BwdLayout {
+    size_t panel, result, dxg, block, part_eb, part_pb, part_w, total;
+    int grid;
+};
+BwdLayout bwd_layout(tri_mul_handle_t h, int64_t N) {
+    BwdLayout L;
+    const int64_t units = N * ((N + 31) / 32);
+    L.grid = trimul::backward_grid(units, h->w.cus);
+    L.panel = round256(panel_bytes(N, h->c, h->dtype));
+    L.result = round256(result_bytes(N, h->c));
+    L.dxg = round256((size_t)N * (size_t)N * (size_t)h->c_z * 4);
+    L.block = round256((size_t)units * 128 * 32 * 2);
+    L.part_eb = round256((size_t)L.grid * 4 * 128 * 4);
+    L.part_pb = round256((size_t)L.grid * 2 * 128 * 4);
+    L.part_w = round256((size_t)L.grid * 128 * 128 * 4);
+    L.total = 6 * L.panel + 3 * L.result + L.dxg + 9 * L.block + L.part_eb + L.part_pb + L.part_w;
+    return L;
+}
+
+int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout, void* dz,
+                 const tri_mul_grads_t* g, void* ws, size_t ws_bytes, void* stream, int incoming) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "the layer backward supports the bf16 storage path only");
+    if (!z || !dout || !dz || !g || !ws) return fail(TRI_MUL_EINVAL, "null pointer argument");
+    const float* gp[] = {g->ln_in_w, g->ln_in_b, g->w_a, g->w_ga, g->w_b, g->w_gb, g->w_g, g->ln_out_w, g->ln_out_b, g->w_o};
+    for (const float* q : gp)
+        if (!q) return fail(TRI_MUL_EINVAL, "null gradient pointer");
+    if (!aligned16(z) || !aligned16(dout) || !aligned16(dz)) return fail(TRI_MUL_EINVAL, "z, dout and dz must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
+    const BwdLayout L = bwd_layout(h, N);
+    if (ws_bytes < L.total) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed for N = %lld", ws_bytes, L.total, (long long)N);
+    char* p = static_cast<char*>(ws);
+    auto take = [&](size_t n) { char* q = p; p += n; return q; };
+    void *A = take(L.panel), *B = take(L.panel), *dCp = take(L.panel), *dCt = take(L.panel), *At = take(L.panel), *Bt = take(L.panel);
+    float* C = reinterpret_cast<float*>(take(L.result));
+    float* dA = reinterpret_cast<float*>(take(L.result));
+    float* dB = reinterpret_cast<float*>(take(L.result));
+    float* dxg = reinterpret_cast<float*>(take(L.dxg));
+    trimul::BackwardBlocks bb;
+    using trimul::bf16_t;
+    bf16_t** blk[] = {&bb.du, &bb.y, &bb.dgg, &bb.xe, &bb.dpa, &bb.dga, &bb.dpb, &bb.dgb, &bb.xp};
+    for (bf16_t** q : blk) *q = reinterpret_cast<bf16_t*>(take(L.block));
+    float* peb = reinterpret_cast<float*>(take(L.part_eb));
+    float* ppb = reinterpret_cast<float*>(take(L.part_pb));
+    float* pw = reinterpret_cast<float*>(take(L.part_w));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int cus = h->w.cus, G = L.grid;
+
+    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, A, B, s);
+    if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    if (e == hipSuccess) e = trimul::launch_epilogue_backward(h->out_dtype, h->w, C, z, mask, dout, N, dCp, dxg, bb, peb, G, s);
+    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, dCp, dCt, N, cus, s);
+    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, A, At, N, cus, s);
+    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, B, Bt, N, cus, s);
+    if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, dCp, Bt, dA, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, dCt, At, dB, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    if (e == hipSuccess) e = trimul::launch_projection_backward(h->w, z, mask, N, incoming, dA, dB, dxg, dz, bb, ppb, G, s);
+    const struct { const bf16_t* u; const bf16_t* v; float* out; } wg[] = {
+        {bb.du, bb.y, g->w_o}, {bb.dgg, bb.xe, g->w_g}, {bb.dpa, bb.xp, g->w_a},
+        {bb.dga, bb.xp, g->w_ga}, {bb.dpb, bb.xp, g->w_b}, {bb.dgb, bb.xp, g->w_gb}};
+    for (const auto& q : wg) {
+        if (e == hipSuccess) e = trimul::launch_wgrad(q.u, q.v, N, pw, G, s);
+        if (e == hipSuccess) e = trimul::launch_sum_parts(pw, G, 128 * 128, 128 * 128, q.out, s);
+    }
+    if (e == hipSuccess) e = trimul::launch_sum_parts(peb, 2 * G, 256, 128, g->ln_out_w, s);
+    if (e == hipSuccess) e = trimul::launch_sum_parts(peb + 128, 2 * G, 256, 128, g->ln_out_b, s);
+    if (e == hipSuccess) e = trimul::launch_sum_parts(ppb, G, 256, 128, g->ln_in_w, s);
+    if (e == hipSuccess) e = trimul::launch_sum_parts(ppb + 128, G, 256, 128, g->ln_in_b, s);
+    if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -220,6 +297,20 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
     if (!rc) rc = upload(h, &h->w.proj4, proj4, s);
     if (!rc) rc = upload(h, &h->w.wo_t, wo_t, s);
     if (!rc) rc = upload(h, &h->w.wg_t, wg_t, s);
+    {   // untransposed copies for the backward (gradients flow through W^T)
+        std::vector<float> f_wo(wo.begin(), wo.end()), f_wg(wg.begin(), wg.end()), projb((size_t)c * cz * 4);
+        for (int ch = 0; ch < c; ++ch)
+            for (int d = 0; d < cz; ++d) {
+                float* q = &projb[((size_t)ch * cz + d) * 4];
+                q[0] = (float)wa[(size_t)ch * cz + d];
+                q[1] = (float)wga[(size_t)ch * cz + d];
+                q[2] = (float)wb[(size_t)ch * cz + d];
+                q[3] = (float)wgb[(size_t)ch * cz + d];
+            }
+        if (!rc) rc = upload(h, &h->w.wo, f_wo, s);
+        if (!rc) rc = upload(h, &h->w.wg, f_wg, s);
+        if (!rc) rc = upload(h, &h->w.projb, projb, s);
+    }
 
     if (!rc) {
         std::vector<uint8_t> zeros((size_t)trimul::kMaxKPanel + 64, 0);
@@ -407,6 +498,25 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
         if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
     }
     return ok();
+}
+
+
+int tri_mul_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    *bytes = bwd_layout(h, N).total;
+    return ok();
+}
+
+int tri_mul_outgoing_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
+                              void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream) {
+    return run_backward(h, z, mask, N, dout, dz, grads, ws, ws_bytes, stream, 0);
+}
+
+int tri_mul_incoming_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
+                              void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream) {
+    return run_backward(h, z, mask, N, dout, dz, grads, ws, ws_bytes, stream, 1);
 }
 
 }  // extern "C"

@@ -18,6 +18,9 @@ struct DeviceWeights {
     float* proj4 = nullptr;     // [c_z][c][4]: (W_a, W_ga, W_b, W_gb)[c][d] at [d][c][*]
     float* wo_t = nullptr;      // [c][c_z]:   W_o[d][c] at [c][d]
     float* wg_t = nullptr;      // [c_z][c_z]: W_g[d][e] at [e][d]
+    float* wo = nullptr;        // [c_z][c]:   W_o as given (backward)
+    float* wg = nullptr;        // [c_z][c_z]: W_g as given (backward)
+    float* projb = nullptr;     // [c][c_z][4]: (W_a, W_ga, W_b, W_gb)[c][d] at [c][d][*] (backward)
     // bf16 copies used by the MFMA kernels (bf16 storage only)
     uint16_t* proj_bf = nullptr;  // [4*c][c_z]: rows ordered per 32-channel group g:
                                   // W_a[g], W_ga[g], W_b[g], W_gb[g] (32 rows each)
@@ -68,5 +71,21 @@ hipError_t launch_epilogue(int dtype, int out_dtype, const DeviceWeights& w, con
 // elements), and the per-channel panel transpose X_c[i][k] -> X_c[k][i].
 hipError_t launch_result_to_panel(int dtype, const float* R, void* P, int64_t N, int cus, hipStream_t s);
 hipError_t launch_panel_transpose(int dtype, const void* X, void* Y, int64_t N, int cus, hipStream_t s);
+
+// Layer backward (bf16 storage).  Unit blocks: per unit of 32 pairs a bf16
+// [128][32] block of one per-pair quantity (see backward.hip).
+struct BackwardBlocks {
+    bf16_t *du, *y, *dgg, *xe;         // from the epilogue backward
+    bf16_t *dpa, *dga, *dpb, *dgb, *xp; // from the projection backward
+};
+int backward_grid(int64_t units, int cus);
+hipError_t launch_epilogue_backward(int out_dtype, const DeviceWeights& w, const float* C, const void* z,
+                                    const uint8_t* mask, const void* dout, int64_t N, void* dCp, float* dxg,
+                                    const BackwardBlocks& bb, float* partial, int grid, hipStream_t s);
+hipError_t launch_projection_backward(const DeviceWeights& w, const void* z, const uint8_t* mask, int64_t N,
+                                      int incoming, const float* dA, const float* dB, const float* dxg, void* dz,
+                                      const BackwardBlocks& bb, float* partial, int grid, hipStream_t s);
+hipError_t launch_wgrad(const bf16_t* U, const bf16_t* V, int64_t N, float* partial, int grid, hipStream_t s);
+hipError_t launch_sum_parts(const float* in, int parts, int64_t stride, int n, float* out, hipStream_t s);
 
 }  // namespace trimul

@@ -34,6 +34,11 @@ class BlockView(ctypes.Structure):
                 ("k_index", _i32), ("k_count", _i32)]
 
 
+class Grads(ctypes.Structure):
+    """tri_mul_grads_t: device pointers of the float32 weight gradients."""
+    _fields_ = [(name, _vp) for name in WEIGHT_FIELDS]
+
+
 # name -> (restype, argtypes); the same order and meaning as include/tri_mul.h
 SIGNATURES = {
     "tri_mul_init": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.POINTER(Params), _vp]),
@@ -49,6 +54,11 @@ SIGNATURES = {
     "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_contract_backward_workspace_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
     "tri_mul_contract_backward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_backward_workspace_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_outgoing_backward": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.POINTER(Grads), _vp,
+                                                 ctypes.c_size_t, _vp]),
+    "tri_mul_incoming_backward": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.POINTER(Grads), _vp,
+                                                 ctypes.c_size_t, _vp]),
 }
 
 _lib = None
@@ -164,6 +174,19 @@ def tri_mul_contract_backward(h, dC, a_panels, b_panels, N, dA, dB, ws, ws_bytes
                                            _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def tri_mul_backward_workspace_size(h, N):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_backward_workspace_size(h, N, ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_layer_backward(h, direction, z, mask, N, dout, dz, grads, ws, ws_bytes, stream=None):
+    """grads: dict WEIGHT_FIELDS -> float32 device tensors (overwritten)."""
+    g = Grads(*[_ptr(grads[n]) for n in WEIGHT_FIELDS])
+    f = lib().tri_mul_incoming_backward if direction in (TRI_MUL_INCOMING, "incoming") else lib().tri_mul_outgoing_backward
+    _check(f(h, _ptr(z), _ptr(mask), N, _ptr(dout), _ptr(dz), ctypes.byref(g), _ptr(ws), ws_bytes, _stream(stream)))
+
+
 # ---------------------------------------------------------------- wrapper
 
 class TriMul:
@@ -253,6 +276,26 @@ class TriMul:
         ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
         tri_mul_contract_backward(self.h, dC, A, B, N, dA, dB, ws, wsb, stream)
         return dA, dB
+
+    def backward(self, z, dout, mask=None, direction="outgoing", stream=None):
+        """Gradients of sum(out * dout) for the update of z: returns (dz,
+        grads) with grads a dict of float32 tensors shaped like the weights."""
+        N = z.shape[0]
+        c, cz = 128, 128
+        if tuple(z.shape) != (N, N, cz) or tuple(dout.shape) != (N, N, cz):
+            raise ValueError(f"z and dout must be [N, N, {cz}], got {tuple(z.shape)} and {tuple(dout.shape)}")
+        if dout.dtype != TORCH_DTYPE[DTYPE_CODE[self.out_dtype]] or z.dtype != TORCH_DTYPE[DTYPE_CODE[self.dtype]]:
+            raise ValueError("z must have the storage dtype and dout the output dtype of the layer")
+        if not (z.is_contiguous() and dout.is_contiguous()):
+            raise ValueError("z and dout must be contiguous")
+        shapes = {"ln_in_w": (cz,), "ln_in_b": (cz,), "w_a": (c, cz), "w_ga": (c, cz), "w_b": (c, cz),
+                  "w_gb": (c, cz), "w_g": (cz, cz), "ln_out_w": (c,), "ln_out_b": (c,), "w_o": (cz, c)}
+        grads = {k: torch.empty(v, dtype=torch.float32, device=self.device) for k, v in shapes.items()}
+        dz = torch.empty_like(z)
+        wsb = tri_mul_backward_workspace_size(self.h, N)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
+        tri_mul_layer_backward(self.h, direction, z, mask, N, dout, dz, grads, ws, wsb, stream)
+        return dz, grads
 
     def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None):
         tri_mul_block_accumulate(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream)
