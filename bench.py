@@ -196,6 +196,24 @@ def main():
     del dA, dB, bws
     print(f"[bench] contraction backward {bwd_ms:.3f} ms", file=sys.stderr, flush=True)
 
+    # the whole layer backward (outgoing), outside the timed region: dz and
+    # all weight gradients for an upstream gradient dout ~ N(0,1)
+    dout = synth.pair_tensor(N, dtype="f32", device=dev, name="dout")
+    dz = torch.empty_like(z)
+    grads = {k: torch.empty(v, dtype=torch.float32, device=dev) for k, v in T.WEIGHT_SHAPES.items()}
+    lws_n = T.tri_mul_backward_workspace_size(h, N)
+    lws = torch.empty(lws_n, dtype=torch.uint8, device=dev)
+    T.tri_mul_layer_backward(h, "outgoing", z, mask, N, dout, dz, grads, lws, lws_n, stream)
+    l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    l0.record(stream)
+    for _ in range(2):
+        T.tri_mul_layer_backward(h, "outgoing", z, mask, N, dout, dz, grads, lws, lws_n, stream)
+    l1.record(stream)
+    torch.cuda.synchronize()
+    lbwd_ms = l0.elapsed_time(l1) / 2
+    del dout, dz, grads, lws
+    print(f"[bench] layer backward {lbwd_ms:.3f} ms", file=sys.stderr, flush=True)
+
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
     layer_flops = 2 * fl["total"]
@@ -226,6 +244,9 @@ def main():
                               "TFLOP_per_s": round(2 * fl["contract"] / (bwd_ms * 1e-3) / 1e12, 2),
                               "what": "dA = dC B and dB = dC^T A for all 128 channels (one direction), "
                                       "including the layout kernels; not part of ms_per_step"},
+        "backward_layer": {"ms": round(lbwd_ms, 4),
+                           "what": "tri_mul_outgoing_backward: recompute of the forward projections and "
+                                   "contraction, dz and all ten weight gradients; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(), "kernel": "k2_contract_w8",

@@ -141,19 +141,21 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
 // sums of the weight-gradient reductions.
 struct BwdLayout {
     size_t panel, result, dxg, block, part_eb, part_pb, part_w, total;
-    int grid;
+    int grid_pair;   // per-pair stages: one 512-thread work-group per compute unit
+    int grid_w;      // weight-gradient sums: two 256-thread work-groups per compute unit
 };
 BwdLayout bwd_layout(tri_mul_handle_t h, int64_t N) {
     BwdLayout L;
     const int64_t units = N * ((N + 31) / 32);
-    L.grid = trimul::backward_grid(units, h->w.cus);
+    L.grid_pair = trimul::backward_grid(units, h->w.cus, 1);
+    L.grid_w = trimul::backward_grid(units, h->w.cus, 2);
     L.panel = round256(panel_bytes(N, h->c, h->dtype));
     L.result = round256(result_bytes(N, h->c));
     L.dxg = round256((size_t)N * (size_t)N * (size_t)h->c_z * 4);
     L.block = round256((size_t)units * 128 * 32 * 2);
-    L.part_eb = round256((size_t)L.grid * 4 * 128 * 4);
-    L.part_pb = round256((size_t)L.grid * 2 * 128 * 4);
-    L.part_w = round256((size_t)L.grid * 128 * 128 * 4);
+    L.part_eb = round256((size_t)L.grid_pair * 2 * 128 * 4);
+    L.part_pb = round256((size_t)L.grid_pair * 2 * 128 * 4);
+    L.part_w = round256((size_t)L.grid_w * 128 * 128 * 4);
     L.total = 6 * L.panel + 3 * L.result + L.dxg + 9 * L.block + L.part_eb + L.part_pb + L.part_w;
     return L;
 }
@@ -186,7 +188,7 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     float* ppb = reinterpret_cast<float*>(take(L.part_pb));
     float* pw = reinterpret_cast<float*>(take(L.part_w));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int cus = h->w.cus, G = L.grid;
+    const int cus = h->w.cus, G = L.grid_pair, GW = L.grid_w;
 
     hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, A, B, s);
     if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
@@ -201,11 +203,11 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
         {bb.du, bb.y, g->w_o}, {bb.dgg, bb.xe, g->w_g}, {bb.dpa, bb.xp, g->w_a},
         {bb.dga, bb.xp, g->w_ga}, {bb.dpb, bb.xp, g->w_b}, {bb.dgb, bb.xp, g->w_gb}};
     for (const auto& q : wg) {
-        if (e == hipSuccess) e = trimul::launch_wgrad(q.u, q.v, N, pw, G, s);
-        if (e == hipSuccess) e = trimul::launch_sum_parts(pw, G, 128 * 128, 128 * 128, q.out, s);
+        if (e == hipSuccess) e = trimul::launch_wgrad(q.u, q.v, N, pw, GW, s);
+        if (e == hipSuccess) e = trimul::launch_sum_parts(pw, GW, 128 * 128, 128 * 128, q.out, s);
     }
-    if (e == hipSuccess) e = trimul::launch_sum_parts(peb, 2 * G, 256, 128, g->ln_out_w, s);
-    if (e == hipSuccess) e = trimul::launch_sum_parts(peb + 128, 2 * G, 256, 128, g->ln_out_b, s);
+    if (e == hipSuccess) e = trimul::launch_sum_parts(peb, G, 256, 128, g->ln_out_w, s);
+    if (e == hipSuccess) e = trimul::launch_sum_parts(peb + 128, G, 256, 128, g->ln_out_b, s);
     if (e == hipSuccess) e = trimul::launch_sum_parts(ppb, G, 256, 128, g->ln_in_w, s);
     if (e == hipSuccess) e = trimul::launch_sum_parts(ppb + 128, G, 256, 128, g->ln_in_b, s);
     if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
@@ -297,21 +299,6 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
     if (!rc) rc = upload(h, &h->w.proj4, proj4, s);
     if (!rc) rc = upload(h, &h->w.wo_t, wo_t, s);
     if (!rc) rc = upload(h, &h->w.wg_t, wg_t, s);
-    {   // untransposed copies for the backward (gradients flow through W^T)
-        std::vector<float> f_wo(wo.begin(), wo.end()), f_wg(wg.begin(), wg.end()), projb((size_t)c * cz * 4);
-        for (int ch = 0; ch < c; ++ch)
-            for (int d = 0; d < cz; ++d) {
-                float* q = &projb[((size_t)ch * cz + d) * 4];
-                q[0] = (float)wa[(size_t)ch * cz + d];
-                q[1] = (float)wga[(size_t)ch * cz + d];
-                q[2] = (float)wb[(size_t)ch * cz + d];
-                q[3] = (float)wgb[(size_t)ch * cz + d];
-            }
-        if (!rc) rc = upload(h, &h->w.wo, f_wo, s);
-        if (!rc) rc = upload(h, &h->w.wg, f_wg, s);
-        if (!rc) rc = upload(h, &h->w.projb, projb, s);
-    }
-
     if (!rc) {
         std::vector<uint8_t> zeros((size_t)trimul::kMaxKPanel + 64, 0);
         rc = upload(h, &h->w.kmask_pad, zeros, s);
@@ -332,8 +319,22 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
                 eb[(size_t)d * 128 + k] = to_bf16_exact(wo[(size_t)d * c + k]);
                 eb[(size_t)(cz + d) * 128 + k] = to_bf16_exact(wg[(size_t)d * cz + k]);
             }
+        // backward: W_o^T and W_g^T rows; row d of [W_a^T | W_ga^T | W_b^T | W_gb^T]
+        std::vector<uint16_t> ebt((size_t)256 * cz), pbt((size_t)cz * 4 * c);
+        for (int k = 0; k < 128; ++k)
+            for (int d = 0; d < cz; ++d) {
+                ebt[(size_t)k * cz + d] = to_bf16_exact(wo[(size_t)d * c + k]);
+                ebt[(size_t)(128 + k) * cz + d] = to_bf16_exact(wg[(size_t)d * cz + k]);
+            }
+        for (int d = 0; d < cz; ++d)
+            for (int m = 0; m < 4; ++m) {
+                const std::vector<double>& src = m == 0 ? wa : m == 1 ? wga : m == 2 ? wb : wgb;
+                for (int ch = 0; ch < c; ++ch) pbt[((size_t)d * 4 + m) * c + ch] = to_bf16_exact(src[(size_t)ch * cz + d]);
+            }
         if (!rc) rc = upload(h, &h->w.proj_bf, pb, s);
         if (!rc) rc = upload(h, &h->w.epi_bf, eb, s);
+        if (!rc) rc = upload(h, &h->w.epit_bf, ebt, s);
+        if (!rc) rc = upload(h, &h->w.projt_bf, pbt, s);
     }
     if (!rc) {
         e = hipStreamSynchronize(s);

@@ -119,424 +119,637 @@ __global__ __launch_bounds__(256) void k_panel_transpose(const T* __restrict__ X
 // Work unit = 32 pairs (one row r, columns k = 32 kb .. 32 kb + 31), the
 // unit of the result layout.  Per-pair intermediates that feed the weight
 // gradients are written as "unit blocks": for unit u = r * J + kb, a bf16
-// block [128 channels][32 slots] at u * 4096 elements; slots of pairs past N
-// hold zeros.  Each weight gradient is then a sum over units of
-// U_block * V_block^T (k_wgrad).  The per-pair stages here are fp32 VALU
-// kernels (4 x 4 register tiles per thread over an LDS copy of the unit).
-constexpr int kQ = 32;              // pairs per unit
-constexpr int kRow = 129;           // LDS row stride (floats) of [pair][channel] tiles
-constexpr int kCol = 33;            // LDS row stride (floats) of [channel][pair] tiles
-constexpr int kCol4 = 36;           // the same, 16-byte aligned rows (read as float4)
+// block [128 channels][32 slots] at u * 4096 elements.  Each weight gradient
+// is then a sum over units of U_block * V_block^T (k_wgrad); slots of pairs
+// past N or masked out carry a zero in at least one of the two blocks.
+//
+// The per-pair stages are 128-wide products per unit, run on matrix cores
+// (v_mfma_f32_16x16x32_bf16): 8 waves, wave w owns the 16 output columns
+// 16 w .. 16 w + 15 of every product and keeps its slice of the weights in
+// VGPRs as the B operand.  Activations are the A operand, split into
+// bf16 hi + lo (two products), so the products carry about 16 mantissa bits
+// of the fp32 activations; the weights are bf16 already.  Operand layout of
+// the 16 x 16 x 32 product: lane l supplies row (or column) l % 16 and the
+// eight k values 8 (l / 16) .. + 7; the result gives lane l column l % 16 and
+// rows 4 (l / 16) + 0 .. 3.
+constexpr int kQ = 32;        // pairs per unit
+constexpr int kBT = 512;      // threads of the per-pair backward kernels
+constexpr int kCs = 36;       // row stride (floats) of [channel][pair] tiles
+constexpr int kPq = 132;      // row stride (floats) of [pair][channel] tiles
+constexpr int kArow = 256;    // bytes of one bf16 activation row [128]
+constexpr int kDrow = 1024;   // bytes of one bf16 row [4][128] (projection-backward A operand)
 
-__device__ __forceinline__ float bfr(float v) { return bf2f(f2bf(v)); }
+// Byte offset of 16-byte chunk ch of row p in bf16 row tiles; chunks are
+// XOR-swizzled over 16 rows so that the A-operand reads (16 rows, one chunk
+// each) hit distinct banks.
+__device__ __forceinline__ uint32_t arow(int p, int ch) { return (uint32_t)(p * kArow + ((ch ^ (p & 15)) << 4)); }
+__device__ __forceinline__ uint32_t drow(int p, int ch) { return (uint32_t)(p * kDrow + ((ch ^ (p & 15)) << 4)); }
 
-// 16 consecutive floats -> 16 bf16 (32 bytes) at dst.
-__device__ __forceinline__ void st16bf(bf16_t* dst, const float (&v)[16]) {
-    uint4 o0 = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
-    uint4 o1 = make_uint4(pack_bf16x2(v[8], v[9]), pack_bf16x2(v[10], v[11]), pack_bf16x2(v[12], v[13]),
-                          pack_bf16x2(v[14], v[15]));
-    reinterpret_cast<uint4*>(dst)[0] = o0;
-    reinterpret_cast<uint4*>(dst)[1] = o1;
+// The value itself, hidden from the optimiser: lane indices passed through
+// this inside a loop make the LDS addresses derived from them loop-variant,
+// so they are recomputed where used instead of being hoisted out of the loop
+// and held in (or spilled from) registers for the whole kernel.
+__device__ __forceinline__ int opaque(int v) {
+    asm volatile("" : "+v"(v));
+    return v;
 }
 
-template <typename T> __device__ __forceinline__ float ldv(const T* p);
-template <> __device__ __forceinline__ float ldv<float>(const float* p) { return *p; }
-template <> __device__ __forceinline__ float ldv<bf16_t>(const bf16_t* p) { return bf2f(*p); }
+__device__ __forceinline__ float sum_lanes16(float v) {
+    v = sum_lanes8(v);
+    v += dpp_mov<0x140>(v);   // row_mirror: lane i meets lane 15 - i (the other group of 8)
+    return v;
+}
+
+__device__ __forceinline__ void st_hilo(char* hi, char* lo, uint32_t off, float v) {
+    const bf16_t h = f2bf(v);
+    *reinterpret_cast<bf16_t*>(hi + off) = h;
+    *reinterpret_cast<bf16_t*>(lo + off) = f2bf(v - bf2f(h));
+}
+
+__device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8_t ld_frag(const char* base, uint32_t off) {
+    return *reinterpret_cast<const bf16x8_t*>(base + off);
+}
+
+// 8 bf16 of column `col` of a swizzled row tile, rows q0 .. q0 + 7, packed.
+__device__ __forceinline__ uint4 gather_col8(const char* tile, int q0, int col) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = q0 + 2 * i;
+        const uint32_t a = *reinterpret_cast<const bf16_t*>(tile + arow(q, col >> 3) + 2 * (col & 7));
+        const uint32_t b = *reinterpret_cast<const bf16_t*>(tile + arow(q + 1, col >> 3) + 2 * (col & 7));
+        w[i] = a | (b << 16);
+    }
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Four bf16 (rows 4 kq .. + 3 of one 16 x 16 result tile) as one 8-byte word.
+__device__ __forceinline__ uint2 pack4(float a, float b, float c, float d) {
+    return make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));
+}
+
+template <typename TO> struct DoutRegs;
+template <> struct DoutRegs<float> { float4 a, b; };
+template <> struct DoutRegs<bf16_t> { uint4 a; };
 
 // Epilogue backward.  For the unit's pairs (r, k): recompute x = LN_in(z),
 // y = LN_out(C), u = W_o y, g = sigmoid(W_g x); then
 //   du = dout m g,  dgg = dout m u g (1 - g),  dy = du W_o,  dx_g = dgg W_g,
 //   dC = LN_out backward of dy.
-// Writes dC into the panel (rows r, k), dx_g [pair][c_z] fp32, unit blocks
-// du, y, dgg, x, and per-work-group partial sums of dgamma_out, dbeta_out.
-template <typename T, typename TO>
-__global__ __launch_bounds__(256) void k_epilogue_backward(
-    const float* __restrict__ C, const T* __restrict__ z, const uint8_t* __restrict__ mask, const TO* __restrict__ dout,
-    int N, int64_t units, const float* __restrict__ wo_t, const float* __restrict__ wg_t, const float* __restrict__ wo,
-    const float* __restrict__ wg, const float* __restrict__ lniw, const float* __restrict__ lnib,
-    const float* __restrict__ lnow, const float* __restrict__ lnob, float eps, T* __restrict__ dCp,
+// Writes dC into the panel (row r, columns k), dx_g [pair][c_z] fp32, unit
+// blocks du, y, dgg, x, and per-work-group sums of dgamma_out, dbeta_out at
+// partial[(2 wg + {0, 1}) * 128 + c].
+template <typename TO>
+__global__ __launch_bounds__(kBT) void k_epilogue_backward(
+    const float* __restrict__ C, const bf16_t* __restrict__ z, const uint8_t* __restrict__ mask,
+    const TO* __restrict__ dout, int N, int64_t units, const bf16_t* __restrict__ wfwd,
+    const bf16_t* __restrict__ wbwd, const float* __restrict__ lniw, const float* __restrict__ lnib,
+    const float* __restrict__ lnow, const float* __restrict__ lnob, float eps, bf16_t* __restrict__ dCp,
     float* __restrict__ dxg, bf16_t* __restrict__ b_du, bf16_t* __restrict__ b_y, bf16_t* __restrict__ b_dgg,
     bf16_t* __restrict__ b_x, float* __restrict__ partial) {
-    __shared__ float cs[kCh * kCol];      // C [c][q]
-    __shared__ float xs[kQ * kRow];       // z, then x [q][d]
-    __shared__ float ds[kQ * kRow];       // dout [q][d], then dy [q][c]
-    __shared__ float ys[kQ * kRow];       // y [q][c]
-    __shared__ float yh[kQ * kRow];       // normalised C [q][c]
-    __shared__ float us[kQ * kRow];       // du [q][d]
-    __shared__ float gs[kQ * kRow];       // dgg [q][d]
-    __shared__ float st[3][kQ];           // rstd, mean(dyhat), mean(dyhat * yhat)
-    __shared__ float mq[kQ];              // pair mask
-    const int t = threadIdx.x;
+    __shared__ __align__(16) float cs[kCh * kCs];        // C [c][q]
+    __shared__ __align__(16) float dq[kQ * kPq];         // dout [q][d], then dy [q][c]
+    __shared__ __align__(16) float dct[kCh * kCs];       // dC [c][q]
+    __shared__ __align__(16) char act[4][kQ * kArow];    // y hi, y lo, x hi, x lo  [q][128]
+    __shared__ __align__(16) char act2[4][kQ * kArow];   // du hi, du lo, dgg hi, dgg lo  [q][128]
+    __shared__ float prm[4][128];                        // gamma_out, beta_out, gamma_in, beta_in
+    __shared__ float mq[kQ];                             // pair mask of the unit
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int lp = t >> 4, lq = t & 15;                  // LayerNorms: pair lp, 16 lanes per pair
+    const int col = lane & 15, kq = lane >> 4;           // MFMA operand / result lanes
+    const int sc = t >> 2, sq = t & 3;                   // channel-major stores: channel sc, pairs 8 sq .. + 7
     const int J = (N + kQ - 1) / kQ;
     const PanelGeom pg = panel_geom(N, N);
-    const int lp = t >> 3, lq = t & 7;                 // LayerNorms: pair lp, 8 lanes per pair
-    const int tg = t & 31, tq = t >> 5;                // matvecs: outputs 4 tg .. + 3, pairs 4 tq .. + 3
-    const int pc = t >> 1, ph = t & 1;                 // channel-major passes: channel pc, pairs 16 ph .. + 15
-    float acc_g = 0.f, acc_b = 0.f;                    // dgamma_out, dbeta_out of channel pc, pairs of half ph
+
+    bf16x8_t wo[4], wg[4], wot[4], wgt[4];               // B operands: W_o, W_g rows n; W_o^T, W_g^T rows n
+    {
+        const int n = 16 * w + col;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int k = 32 * ks + 8 * kq;
+            wo[ks] = *reinterpret_cast<const bf16x8_t*>(wfwd + n * 128 + k);
+            wg[ks] = *reinterpret_cast<const bf16x8_t*>(wfwd + (128 + n) * 128 + k);
+            wot[ks] = *reinterpret_cast<const bf16x8_t*>(wbwd + n * 128 + k);
+            wgt[ks] = *reinterpret_cast<const bf16x8_t*>(wbwd + (128 + n) * 128 + k);
+        }
+    }
+    if (t < 128) {
+        prm[0][t] = lnow[t];
+        prm[1][t] = lnob[t];
+        prm[2][t] = lniw[t];
+        prm[3][t] = lnib[t];
+    }
+
+    // Global loads of one unit, issued one unit ahead; nothing here reads the
+    // loaded registers, so the loads stay in flight until the unit starts.
+    struct Pre {
+        float4 c0, c1;        // C block floats 4 t .. and 2048 + 4 t ..
+        uint4 zv;             // z of pair lp, channels 8 lq .. + 7
+        DoutRegs<TO> o;       // dout of pair lp, channels 8 lq .. + 7
+        uint32_t mr, mk;      // mask bytes of row r and of column k0 + t (t < 32)
+    };
+    auto load = [&](int64_t u, Pre& p) {
+        p.c0 = p.c1 = make_float4(0.f, 0.f, 0.f, 0.f);
+        p.zv = make_uint4(0, 0, 0, 0);
+        if constexpr (sizeof(TO) == 4) p.o.a = p.o.b = make_float4(0.f, 0.f, 0.f, 0.f);
+        else p.o.a = make_uint4(0, 0, 0, 0);
+        p.mr = p.mk = 1;
+        if (u >= units) return;
+        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
+        const float4* cb = reinterpret_cast<const float4*>(C + u * (kCh * kQ));
+        p.c0 = cb[t];
+        p.c1 = cb[t + kBT];
+        if (k0 + lp < N) {
+            const int64_t pr = (int64_t)r * N + k0 + lp;
+            p.zv = *reinterpret_cast<const uint4*>(z + pr * kCz + 8 * lq);
+            if constexpr (sizeof(TO) == 4) {
+                p.o.a = *reinterpret_cast<const float4*>(dout + pr * kCz + 8 * lq);
+                p.o.b = *reinterpret_cast<const float4*>(dout + pr * kCz + 8 * lq + 4);
+            } else {
+                p.o.a = *reinterpret_cast<const uint4*>(dout + pr * kCz + 8 * lq);
+            }
+        }
+        if (mask && t < kQ) {
+            p.mr = mask[r];
+            if (k0 + t < N) p.mk = mask[k0 + t];
+        }
+    };
+
+    float accg[8], accb[8];                              // dgamma_out, dbeta_out of c = lq + 16 i
+#pragma unroll
+    for (int i = 0; i < 8; ++i) accg[i] = accb[i] = 0.f;
+    Pre cur, nxt;
+    load(blockIdx.x, cur);
 
     for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
-        const int r = (int)(u / J), kb = (int)(u - (int64_t)r * J);
-        const int k0 = kb * kQ;
-        // (1) loads
-        {
-            // C's columns past N hold unspecified values: read them as zero
-            const float4* cb = reinterpret_cast<const float4*>(C + u * (kCh * kQ));
-            const int nq = N - k0;
-#pragma unroll
-            for (int s2 = 0; s2 < 4; ++s2) {
-                const int e = 4 * (t + 256 * s2), ch = e >> 5, q = e & 31;
-                const float4 v = cb[t + 256 * s2];
-                cs[ch * kCol + q] = q < nq ? v.x : 0.f;
-                cs[ch * kCol + q + 1] = q + 1 < nq ? v.y : 0.f;
-                cs[ch * kCol + q + 2] = q + 2 < nq ? v.z : 0.f;
-                cs[ch * kCol + q + 3] = q + 3 < nq ? v.w : 0.f;
+        load(u + gridDim.x, nxt);
+        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
+        const int np = min(kQ, N - k0);
+        {   // stage C (columns past N read as zero) and the pair mask
+            const int c = t >> 3, q = 4 * (t & 7);
+            float4 a = cur.c0, b = cur.c1;
+            if (q + 4 > np) {
+                if (q + 0 >= np) a.x = b.x = 0.f;
+                if (q + 1 >= np) a.y = b.y = 0.f;
+                if (q + 2 >= np) a.z = b.z = 0.f;
+                if (q + 3 >= np) a.w = b.w = 0.f;
             }
-            const bool valid = k0 + lp < N;
-            const int64_t pr = (int64_t)r * N + k0 + lp;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int d = 16 * lq + i;
-                xs[lp * kRow + d] = valid ? ldv<T>(z + pr * kCz + d) : 0.f;
-                ds[lp * kRow + d] = valid ? ldv<TO>(dout + pr * kCz + d) : 0.f;
-            }
-            if (t < kQ) {
-                const int k = k0 + t;
-                mq[t] = (k < N && (!mask || (mask[r] != 0 && mask[k] != 0))) ? 1.f : 0.f;
-            }
+            *reinterpret_cast<float4*>(&cs[c * kCs + q]) = a;
+            *reinterpret_cast<float4*>(&cs[(c + 64) * kCs + q]) = b;
+            if (t < kQ) mq[t] = (t < np && cur.mr != 0 && cur.mk != 0) ? 1.f : 0.f;
         }
         __syncthreads();
-        // (2) LN_out over c for pair lp (lane lq: c = lq + 8 i), LN_in over d (16 lq + i)
-        {
-            float v[16], s1 = 0.f;
+        float yh[8], rs;                                 // LN_out(C) normalised, c = lq + 16 i; 1 / std
+        {   // LN_out of pair lp over c = lq + 16 i -> y hi / lo rows
+            float s1 = 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { v[i] = cs[(lq + 8 * i) * kCol + lp]; s1 += v[i]; }
-            s1 = sum_lanes8(s1);
-            const float mu = s1 * (1.f / kCh);
+            for (int i = 0; i < 8; ++i) { yh[i] = cs[(lq + 16 * i) * kCs + lp]; s1 += yh[i]; }
+            const float mu = sum_lanes16(s1) * (1.f / kCh);
             float q2 = 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { v[i] -= mu; q2 += v[i] * v[i]; }
-            q2 = sum_lanes8(q2);
-            const float rs = rsqrtf(q2 * (1.f / kCh) + eps);
+            for (int i = 0; i < 8; ++i) { yh[i] -= mu; q2 += yh[i] * yh[i]; }
+            rs = rsqrtf(sum_lanes16(q2) * (1.f / kCh) + eps);
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int c = lq + 8 * i;
-                yh[lp * kRow + c] = v[i] * rs;
-                ys[lp * kRow + c] = v[i] * rs * lnow[c] + lnob[c];
-            }
-            if (lq == 0) st[0][lp] = rs;
-            float w[16];
-            s1 = 0.f;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) { w[i] = xs[lp * kRow + 16 * lq + i]; s1 += w[i]; }
-            s1 = sum_lanes8(s1);
-            const float mz = s1 * (1.f / kCz);
-            q2 = 0.f;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) { w[i] -= mz; q2 += w[i] * w[i]; }
-            q2 = sum_lanes8(q2);
-            const float rz = rsqrtf(q2 * (1.f / kCz) + eps);
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int d = 16 * lq + i;
-                xs[lp * kRow + d] = w[i] * rz * lniw[d] + lnib[d];
+            for (int i = 0; i < 8; ++i) {
+                const int c = lq + 16 * i;
+                yh[i] *= rs;
+                st_hilo(act[0], act[1], arow(lp, c >> 3) + 2 * (c & 7), yh[i] * prm[0][c] + prm[1][c]);
             }
         }
-        __syncthreads();
-        // (3) u = W_o y, gg = W_g x; du, dgg
-        {
-            float au[4][4] = {}, ag[4][4] = {};
-            for (int c = 0; c < kCh; ++c) {
-                const float4 wu = *reinterpret_cast<const float4*>(wo_t + c * kCz + 4 * tg);
-                const float4 wv = *reinterpret_cast<const float4*>(wg_t + c * kCz + 4 * tg);
+        {   // LN_in of pair lp over d = 8 lq + i -> x hi / lo rows; dout -> dq
+            const uint32_t zw[4] = {cur.zv.x, cur.zv.y, cur.zv.z, cur.zv.w};
+            float x[8], s1 = 0.f;
 #pragma unroll
-                for (int a = 0; a < 4; ++a) {
-                    const float yv = ys[(4 * tq + a) * kRow + c], xv = xs[(4 * tq + a) * kRow + c];
-                    au[a][0] += yv * wu.x; au[a][1] += yv * wu.y; au[a][2] += yv * wu.z; au[a][3] += yv * wu.w;
-                    ag[a][0] += xv * wv.x; ag[a][1] += xv * wv.y; ag[a][2] += xv * wv.z; ag[a][3] += xv * wv.w;
-                }
+            for (int i = 0; i < 4; ++i) {
+                x[2 * i] = __uint_as_float(zw[i] << 16);
+                x[2 * i + 1] = __uint_as_float(zw[i] & 0xffff0000u);
             }
 #pragma unroll
-            for (int a = 0; a < 4; ++a) {
-                const int q = 4 * tq + a;
-                const float m = mq[q];
+            for (int i = 0; i < 8; ++i) s1 += x[i];
+            const float mz = sum_lanes16(s1) * (1.f / kCz);
+            float q2 = 0.f;
 #pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    const int d = 4 * tg + b;
-                    const float g = 1.f / (1.f + __expf(-ag[a][b]));
-                    const float o = ds[q * kRow + d] * m;
-                    us[q * kRow + d] = o * g;
-                    gs[q * kRow + d] = o * au[a][b] * g * (1.f - g);
-                }
+            for (int i = 0; i < 8; ++i) { x[i] -= mz; q2 += x[i] * x[i]; }
+            const float rz = rsqrtf(sum_lanes16(q2) * (1.f / kCz) + eps);
+            uint32_t hw[4], lw[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int d = 8 * lq + 2 * i;
+                const float x0 = x[2 * i] * rz * prm[2][d] + prm[3][d];
+                const float x1 = x[2 * i + 1] * rz * prm[2][d + 1] + prm[3][d + 1];
+                hw[i] = pack_bf16x2(x0, x1);
+                lw[i] = pack_bf16x2(x0 - __uint_as_float(hw[i] << 16), x1 - __uint_as_float(hw[i] & 0xffff0000u));
             }
-        }
-        __syncthreads();
-        // (4) dy = du W_o (into ds), dx_g = dgg W_g (to HBM)
-        {
-            float ay[4][4] = {}, ax[4][4] = {};
-            for (int d = 0; d < kCz; ++d) {
-                const float4 wu = *reinterpret_cast<const float4*>(wo + d * kCh + 4 * tg);
-                const float4 wv = *reinterpret_cast<const float4*>(wg + d * kCz + 4 * tg);
-#pragma unroll
-                for (int a = 0; a < 4; ++a) {
-                    const float uv = us[(4 * tq + a) * kRow + d], gv = gs[(4 * tq + a) * kRow + d];
-                    ay[a][0] += uv * wu.x; ay[a][1] += uv * wu.y; ay[a][2] += uv * wu.z; ay[a][3] += uv * wu.w;
-                    ax[a][0] += gv * wv.x; ax[a][1] += gv * wv.y; ax[a][2] += gv * wv.z; ax[a][3] += gv * wv.w;
-                }
-            }
-#pragma unroll
-            for (int a = 0; a < 4; ++a) {
-                const int q = 4 * tq + a;
-#pragma unroll
-                for (int b = 0; b < 4; ++b) ds[q * kRow + 4 * tg + b] = ay[a][b];
-                if (k0 + q < N)
-                    *reinterpret_cast<float4*>(dxg + ((int64_t)r * N + k0 + q) * kCz + 4 * tg) =
-                        make_float4(ax[a][0], ax[a][1], ax[a][2], ax[a][3]);
-            }
-        }
-        __syncthreads();
-        // (5) LN_out backward statistics of pair lp
-        {
-            float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int c = lq + 8 * i;
-                const float dh = ds[lp * kRow + c] * lnow[c];
-                s1 += dh;
-                s2 += dh * yh[lp * kRow + c];
-            }
-            s1 = sum_lanes8(s1);
-            s2 = sum_lanes8(s2);
-            if (lq == 0) { st[1][lp] = s1 * (1.f / kCh); st[2][lp] = s2 * (1.f / kCh); }
-        }
-        __syncthreads();
-        // (6) channel-major outputs: dC into the panel, unit blocks, dgamma / dbeta
-        {
-            float dc[16], v0[16], v1[16], v2[16], v3[16];
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int q = 16 * ph + i;
-                const bool ok = k0 + q < N;
-                const float dy = ds[q * kRow + pc], yv = yh[q * kRow + pc];
-                dc[i] = st[0][q] * (dy * lnow[pc] - st[1][q] - yv * st[2][q]);
-                acc_g += dy * yv;
-                acc_b += dy;
-                v0[i] = us[q * kRow + pc];
-                v1[i] = ok ? ys[q * kRow + pc] : 0.f;
-                v2[i] = gs[q * kRow + pc];
-                v3[i] = ok ? xs[q * kRow + pc] : 0.f;
-            }
-            T* dst = dCp + panel_off(pg, pc, r, k0 + 16 * ph);
-            if constexpr (sizeof(T) == 2) {
-                st16bf(dst, dc);
+            *reinterpret_cast<uint4*>(act[2] + arow(lp, lq)) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            *reinterpret_cast<uint4*>(act[3] + arow(lp, lq)) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+            float4 o0, o1;
+            if constexpr (sizeof(TO) == 4) {
+                o0 = cur.o.a;
+                o1 = cur.o.b;
             } else {
-#pragma unroll
-                for (int i = 0; i < 16; ++i) dst[i] = dc[i];
+                const uint4 v = cur.o.a;
+                o0 = make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                                 __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+                o1 = make_float4(__uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
+                                 __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u));
             }
-            const int64_t bo = u * (kCh * kQ) + pc * kQ + 16 * ph;
-            st16bf(b_du + bo, v0);
-            st16bf(b_y + bo, v1);
-            st16bf(b_dgg + bo, v2);
-            st16bf(b_x + bo, v3);
+            *reinterpret_cast<float4*>(&dq[lp * kPq + 8 * lq]) = o0;
+            *reinterpret_cast<float4*>(&dq[lp * kPq + 8 * lq + 4]) = o1;
         }
         __syncthreads();
+        {   // u = y W_o^T, gg = x W_g^T (columns d = 16 w + col); du, dgg
+            f32x4_t au[2], ag[2];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) au[mb] = ag[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb) {
+                    const uint32_t o = arow(16 * mb + col, 4 * ks + kq);
+                    au[mb] = mfma16(ld_frag(act[0], o), wo[ks], au[mb]);
+                    ag[mb] = mfma16(ld_frag(act[2], o), wg[ks], ag[mb]);
+                    au[mb] = mfma16(ld_frag(act[1], o), wo[ks], au[mb]);
+                    ag[mb] = mfma16(ld_frag(act[3], o), wg[ks], ag[mb]);
+                }
+            // unit blocks of y and x (bf16 = the hi rows), channel-major
+            *reinterpret_cast<uint4*>(b_y + u * (kCh * kQ) + sc * kQ + 8 * sq) = gather_col8(act[0], 8 * sq, sc);
+            *reinterpret_cast<uint4*>(b_x + u * (kCh * kQ) + sc * kQ + 8 * sq) = gather_col8(act[2], 8 * sq, sc);
+            const int d = 16 * w + col;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                float vu[4], vg[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int q = 16 * mb + 4 * kq + i;
+                    const float o = dq[q * kPq + d] * mq[q];
+                    const float g = sigmoidf_(ag[mb][i]);
+                    vu[i] = o * g;
+                    vg[i] = o * au[mb][i] * g * (1.f - g);
+                    const uint32_t off = arow(q, d >> 3) + 2 * (d & 7);
+                    st_hilo(act2[0], act2[1], off, vu[i]);
+                    st_hilo(act2[2], act2[3], off, vg[i]);
+                }
+                const int64_t bo = u * (kCh * kQ) + d * kQ + 16 * mb + 4 * kq;
+                *reinterpret_cast<uint2*>(b_du + bo) = pack4(vu[0], vu[1], vu[2], vu[3]);
+                *reinterpret_cast<uint2*>(b_dgg + bo) = pack4(vg[0], vg[1], vg[2], vg[3]);
+            }
+        }
+        __syncthreads();
+        {   // dy = du W_o -> dq; dx_g = dgg W_g -> HBM (columns n = 16 w + col)
+            f32x4_t ay[2], ax[2];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) ay[mb] = ax[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb) {
+                    const uint32_t o = arow(16 * mb + col, 4 * ks + kq);
+                    ay[mb] = mfma16(ld_frag(act2[0], o), wot[ks], ay[mb]);
+                    ax[mb] = mfma16(ld_frag(act2[2], o), wgt[ks], ax[mb]);
+                    ay[mb] = mfma16(ld_frag(act2[1], o), wot[ks], ay[mb]);
+                    ax[mb] = mfma16(ld_frag(act2[3], o), wgt[ks], ax[mb]);
+                }
+            const int n = 16 * w + col;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int q = 16 * mb + 4 * kq + i;
+                    dq[q * kPq + n] = ay[mb][i];
+                    if (q < np) dxg[((int64_t)r * N + k0 + q) * kCz + n] = ax[mb][i];
+                }
+        }
+        __syncthreads();
+        {   // LN_out backward of pair lp: dC = rs (dy gamma - mean(dy gamma) - yh mean(dy gamma yh))
+            float dy[8], s1 = 0.f, s2 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = lq + 16 * i;
+                dy[i] = dq[lp * kPq + c];
+                const float dh = dy[i] * prm[0][c];
+                s1 += dh;
+                s2 += dh * yh[i];
+            }
+            s1 = sum_lanes16(s1) * (1.f / kCh);
+            s2 = sum_lanes16(s2) * (1.f / kCh);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = lq + 16 * i;
+                dct[c * kCs + lp] = rs * (dy[i] * prm[0][c] - s1 - yh[i] * s2);
+                accg[i] += dy[i] * yh[i];
+                accb[i] += dy[i];
+            }
+        }
+        __syncthreads();
+        {   // dC row r, columns k0 + 8 sq .. + 7 of channel sc into the panel
+            const float4 a = *reinterpret_cast<const float4*>(&dct[sc * kCs + 8 * sq]);
+            const float4 b = *reinterpret_cast<const float4*>(&dct[sc * kCs + 8 * sq + 4]);
+            *reinterpret_cast<uint4*>(dCp + panel_off(pg, sc, r, k0 + 8 * sq)) =
+                make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
+        }
+        cur = nxt;
     }
-    partial[((int64_t)blockIdx.x * 4 + 2 * ph + 0) * kCh + pc] = acc_g;
-    partial[((int64_t)blockIdx.x * 4 + 2 * ph + 1) * kCh + pc] = acc_b;
+    // per-work-group sums over the pairs lanes (lp) through LDS
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        cs[lp * kCh + lq + 16 * i] = accg[i];
+        dct[lp * kCh + lq + 16 * i] = accb[i];
+    }
+    __syncthreads();
+    if (t < 2 * kCh) {
+        const float* src = t < kCh ? cs : dct;
+        const int c = t & (kCh - 1);
+        float s = 0.f;
+        for (int q = 0; q < kQ; ++q) s += src[q * kCh + c];
+        partial[((int64_t)blockIdx.x * 2 + (t >> 7)) * kCh + c] = s;
+    }
 }
 
 // Projection backward.  Unit (r, kb) of dA / dB; its pairs are P(q) = (r, k)
 // (outgoing) or (k, r) (incoming).  Recompute x = LN_in(z) and the four
-// projections; then dpa = da m s_a, dga = da m p_a s_a (1 - s_a) (same for b),
-// dx = dx_g + W_a^T dpa + W_ga^T dga + W_b^T dpb + W_gb^T dgb, and
-// dz = LN_in backward of dx.  Writes dz, unit blocks dpa, dga, dpb, dgb, x,
-// and per-work-group partial sums of dgamma_in, dbeta_in.
-template <typename T, bool INCOMING>
-__global__ __launch_bounds__(256) void k_projection_backward(
-    const T* __restrict__ z, const uint8_t* __restrict__ mask, int N, int64_t units, const float* __restrict__ dA,
-    const float* __restrict__ dB, const float* __restrict__ dxg, const float4* __restrict__ proj4,
-    const float4* __restrict__ projb, const float* __restrict__ lniw, const float* __restrict__ lnib, float eps,
-    T* __restrict__ dz, bf16_t* __restrict__ b_dpa, bf16_t* __restrict__ b_dga, bf16_t* __restrict__ b_dpb,
+// projections p_a, g_a, p_b, g_b (pre-sigmoid gates); then
+//   dpa = da m s_a,  dga = da m p_a s_a (1 - s_a)  (the same for b),
+//   dx = dx_g + [dpa dga dpb dgb] [W_a; W_ga; W_b; W_gb],  dz = LN_in backward of dx.
+// Writes dz, unit blocks dpa, dga, dpb, dgb, x, and per-work-group sums of
+// dgamma_in, dbeta_in at partial[(2 wg + {0, 1}) * 128 + d].
+//
+// Wave w owns 32 output columns of both products and keeps both weight
+// slices in registers: rows 32 w + col of W_a, W_ga, W_b, W_gb for the
+// projections and row d = 32 w + col of [W_a^T | W_ga^T | W_b^T | W_gb^T]
+// (512 long) for dx, 256 registers; so the kernel runs 4 waves, one per
+// SIMD, each with the whole register file.  Products on
+// v_mfma_f32_32x32x16_bf16: lane l supplies row (column) l % 32 and k values
+// 8 (l / 32) .. + 7; the result gives lane l column l % 32 and rows
+// 8 (i / 4) + 4 (l / 32) + i % 4, i = 0 .. 15.
+constexpr int kPT = 256;      // threads of the projection backward
+constexpr int kPq4 = 136;     // [pair][channel] row stride: rows 4 apart land 32 banks apart
+
+template <bool INCOMING>
+__global__ __attribute__((amdgpu_flat_work_group_size(kPT, kPT), amdgpu_waves_per_eu(1, 1)))
+void k_projection_backward(
+    const bf16_t* __restrict__ z, const uint8_t* __restrict__ mask, int N, int64_t units, const float* __restrict__ dA,
+    const float* __restrict__ dB, const float* __restrict__ dxg, const bf16_t* __restrict__ wproj,
+    const bf16_t* __restrict__ wprojt, const float* __restrict__ lniw, const float* __restrict__ lnib, float eps,
+    bf16_t* __restrict__ dz, bf16_t* __restrict__ b_dpa, bf16_t* __restrict__ b_dga, bf16_t* __restrict__ b_dpb,
     bf16_t* __restrict__ b_dgb, bf16_t* __restrict__ b_x, float* __restrict__ partial) {
-    __shared__ float zs[kQ * kRow];       // z [q][d]
-    __shared__ float xs[kQ * kRow];       // x [q][d]
-    __shared__ float gx[kQ * kRow];       // dx_g, then dx [q][d]
-    __shared__ float das[kCh * kCol];     // da [c][q]
-    __shared__ float dbs[kCh * kCol];     // db [c][q]
-    __shared__ __align__(16) float d4[4][kCh * kCol4];  // dpa, dga, dpb, dgb [c][q]
-    __shared__ float st[4][kQ];           // mean, rstd, mean(dxhat), mean(dxhat * xhat)
+    __shared__ __align__(16) float das[kCh * kCs];       // da [c][q]
+    __shared__ __align__(16) float dbs[kCh * kCs];       // db [c][q]
+    __shared__ __align__(16) char xa[2][kQ * kArow];     // x hi, x lo  [q][128]
+    __shared__ __align__(16) char d4[2][kQ * kDrow];     // hi, lo  [q][dpa | dga | dpb | dgb]
+    __shared__ __align__(16) float dxs[kQ * kPq4];       // dx from the projections [q][d]
+    __shared__ __align__(16) float xhs[kQ * kPq4];       // LN_in(z) normalised [q][d]
+    __shared__ float rzs[kQ];                            // 1 / std of LN_in per pair
+    __shared__ float prm[2][128];                        // gamma_in, beta_in
     __shared__ float mq[kQ];
-    const int t = threadIdx.x;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int lp = t >> 3, lq = t & 7;                   // LayerNorm: pair lp, d = 16 lq .. + 15
     const int J = (N + kQ - 1) / kQ;
-    const int lp = t >> 3, lq = t & 7;
-    const int tg = t & 31, tq = t >> 5;
-    const int pc = t & 127, ph = t >> 7;               // projections: channel pc, pairs 16 ph .. + 15
-    const int bc = t >> 1, bh = t & 1;                 // x block: channel bc, pairs 16 bh .. + 15
-    float acc_g[16], acc_b[16];                        // dgamma_in, dbeta_in for d = 16 lq + i
-#pragma unroll
-    for (int i = 0; i < 16; ++i) acc_g[i] = acc_b[i] = 0.f;
     auto pair_of = [&](int r, int k) -> int64_t { return INCOMING ? (int64_t)k * N + r : (int64_t)r * N + k; };
 
-    for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
-        const int r = (int)(u / J), kb = (int)(u - (int64_t)r * J);
-        const int k0 = kb * kQ;
-        {
-            const float4* ab = reinterpret_cast<const float4*>(dA + u * (kCh * kQ));
-            const float4* bb = reinterpret_cast<const float4*>(dB + u * (kCh * kQ));
+    bf16x8_t wp[32], wt[32];   // wp[8 m + ks]: map m, k = 16 ks + 8 hi;  wt[ks]: k = 16 ks + 8 hi
+    {
+        const int col = lane & 31, hi = lane >> 5;
 #pragma unroll
-            for (int s2 = 0; s2 < 4; ++s2) {
-                const int e = 4 * (t + 256 * s2), ch = e >> 5, q = e & 31;
-                const float4 a = ab[t + 256 * s2], b = bb[t + 256 * s2];
-                das[ch * kCol + q] = a.x; das[ch * kCol + q + 1] = a.y; das[ch * kCol + q + 2] = a.z; das[ch * kCol + q + 3] = a.w;
-                dbs[ch * kCol + q] = b.x; dbs[ch * kCol + q + 1] = b.y; dbs[ch * kCol + q + 2] = b.z; dbs[ch * kCol + q + 3] = b.w;
-            }
-            const bool valid = k0 + lp < N;
-            const int64_t pr = valid ? pair_of(r, k0 + lp) : 0;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int d = 16 * lq + i;
-                zs[lp * kRow + d] = valid ? ldv<T>(z + pr * kCz + d) : 0.f;
-                gx[lp * kRow + d] = valid ? dxg[pr * kCz + d] : 0.f;
-            }
-            if (t < kQ) {
-                const int k = k0 + t;
-                mq[t] = (k < N && (!mask || (mask[r] != 0 && mask[k] != 0))) ? 1.f : 0.f;
-            }
+        for (int j = 0; j < 32; ++j) {
+            wp[j] = *reinterpret_cast<const bf16x8_t*>(
+                wproj + ((int64_t)w * 128 + (j >> 3) * 32 + col) * 128 + 16 * (j & 7) + 8 * hi);
+            wt[j] = *reinterpret_cast<const bf16x8_t*>(wprojt + (int64_t)(32 * w + col) * 512 + 16 * j + 8 * hi);
         }
-        __syncthreads();
-        {   // LN_in of pair lp
-            float w[16], s1 = 0.f;
+    }
+    if (t < 128) {
+        prm[0][t] = lniw[t];
+        prm[1][t] = lnib[t];
+    }
+    __syncthreads();   // the first unit's LN_in reads prm before the loop's first barrier
+
+    // One unit's loads, issued one unit ahead; dx_g is fetched separately
+    // (it is used last).  Nothing here reads the loaded registers.
+    struct Pre {
+        float4 a[4], b[4];       // dA, dB block floats 4 (t + 256 s) ..
+        uint4 z0, z1;            // z of pair lp, channels 16 lq .. + 15
+        uint32_t mr, mk;
+    };
+    auto load = [&](int64_t u, Pre& p) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { w[i] = zs[lp * kRow + 16 * lq + i]; s1 += w[i]; }
-            s1 = sum_lanes8(s1);
-            const float mz = s1 * (1.f / kCz);
+        for (int s = 0; s < 4; ++s) p.a[s] = p.b[s] = make_float4(0.f, 0.f, 0.f, 0.f);
+        p.z0 = p.z1 = make_uint4(0, 0, 0, 0);
+        p.mr = p.mk = 1;
+        if (u >= units) return;
+        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
+        const float4* ab = reinterpret_cast<const float4*>(dA + u * (kCh * kQ));
+        const float4* bb = reinterpret_cast<const float4*>(dB + u * (kCh * kQ));
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            p.a[s] = ab[t + kPT * s];
+            p.b[s] = bb[t + kPT * s];
+        }
+        if (k0 + lp < N) {
+            const uint4* zs = reinterpret_cast<const uint4*>(z + pair_of(r, k0 + lp) * kCz + 16 * lq);
+            p.z0 = zs[0];
+            p.z1 = zs[1];
+        }
+        if (mask && t < kQ) {
+            p.mr = mask[r];
+            if (k0 + t < N) p.mk = mask[k0 + t];
+        }
+    };
+    auto load_dxg = [&](int64_t u, float4 (&g)[4]) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) g[s] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (u >= units) return;
+        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
+        if (k0 + lp < N) {
+            const float4* src = reinterpret_cast<const float4*>(dxg + pair_of(r, k0 + lp) * kCz + 16 * lq);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) g[s] = src[s];
+        }
+    };
+
+    float accg[16], accb[16];                            // dgamma_in, dbeta_in of d = 16 lq + i
+#pragma unroll
+    for (int i = 0; i < 16; ++i) accg[i] = accb[i] = 0.f;
+    Pre cur;
+    float4 xg[4];
+    load(blockIdx.x, cur);
+    load_dxg(blockIdx.x, xg);
+
+    for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
+        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
+        const int np = min(kQ, N - k0);
+        float xh[16], rz;   // LN_in(z) normalised, d = 16 lq + i, and 1 / std: to LDS after the barrier
+        {   // stage da, db and the mask; LN_in of pair lp -> x hi / lo rows
+            const int t = opaque(threadIdx.x), lp = t >> 3, lq = t & 7;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int c = (t >> 3) + 32 * s, q = 4 * (t & 7);
+                *reinterpret_cast<float4*>(&das[c * kCs + q]) = cur.a[s];
+                *reinterpret_cast<float4*>(&dbs[c * kCs + q]) = cur.b[s];
+            }
+            if (t < kQ) mq[t] = (t < np && cur.mr != 0 && cur.mk != 0) ? 1.f : 0.f;
+            const uint32_t zw[8] = {cur.z0.x, cur.z0.y, cur.z0.z, cur.z0.w, cur.z1.x, cur.z1.y, cur.z1.z, cur.z1.w};
+            float s1 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                xh[2 * i] = __uint_as_float(zw[i] << 16);
+                xh[2 * i + 1] = __uint_as_float(zw[i] & 0xffff0000u);
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s1 += xh[i];
+            const float mz = sum_lanes8(s1) * (1.f / kCz);
             float q2 = 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { w[i] -= mz; q2 += w[i] * w[i]; }
-            q2 = sum_lanes8(q2);
-            const float rz = rsqrtf(q2 * (1.f / kCz) + eps);
+            for (int i = 0; i < 16; ++i) { xh[i] -= mz; q2 += xh[i] * xh[i]; }
+            rz = rsqrtf(sum_lanes8(q2) * (1.f / kCz) + eps);
+            uint32_t hw[8], lw[8];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int d = 16 * lq + i;
-                xs[lp * kRow + d] = w[i] * rz * lniw[d] + lnib[d];
+            for (int i = 0; i < 8; ++i) {
+                const int d = 16 * lq + 2 * i;
+                xh[2 * i] *= rz;
+                xh[2 * i + 1] *= rz;
+                const float x0 = xh[2 * i] * prm[0][d] + prm[1][d];
+                const float x1 = xh[2 * i + 1] * prm[0][d + 1] + prm[1][d + 1];
+                hw[i] = pack_bf16x2(x0, x1);
+                lw[i] = pack_bf16x2(x0 - __uint_as_float(hw[i] << 16), x1 - __uint_as_float(hw[i] & 0xffff0000u));
             }
-            if (lq == 0) { st[0][lp] = mz; st[1][lp] = rz; }
+            *reinterpret_cast<uint4*>(xa[0] + arow(lp, 2 * lq)) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            *reinterpret_cast<uint4*>(xa[0] + arow(lp, 2 * lq + 1)) = make_uint4(hw[4], hw[5], hw[6], hw[7]);
+            *reinterpret_cast<uint4*>(xa[1] + arow(lp, 2 * lq)) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+            *reinterpret_cast<uint4*>(xa[1] + arow(lp, 2 * lq + 1)) = make_uint4(lw[4], lw[5], lw[6], lw[7]);
         }
+        load(u + gridDim.x, cur);                        // next unit's dA, dB, z, mask
         __syncthreads();
-        {   // projections of channel pc for 16 pairs, then the four gradients
-            float acc[16][4];
+        {   // xhs and rzs are read by the previous unit's last phase: written only past the barrier
+            const int t = opaque(threadIdx.x), lp = t >> 3, lq = t & 7;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) acc[i][0] = acc[i][1] = acc[i][2] = acc[i][3] = 0.f;
-            for (int d = 0; d < kCz; ++d) {
-                const float4 w = proj4[d * kCh + pc];
+            for (int s = 0; s < 4; ++s)
+                *reinterpret_cast<float4*>(&xhs[lp * kPq4 + 16 * lq + 4 * s]) =
+                    make_float4(xh[4 * s], xh[4 * s + 1], xh[4 * s + 2], xh[4 * s + 3]);
+            if (lq == 0) rzs[lp] = rz;
+        }
+        {   // projections of channels c = 32 w + col; the four gradients
+            const int lo = opaque(lane), col = lo & 31, hi = lo >> 5;
+            const int c = 32 * w + col;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float xv = xs[(16 * ph + i) * kRow + d];
-                    acc[i][0] += w.x * xv; acc[i][1] += w.y * xv; acc[i][2] += w.z * xv; acc[i][3] += w.w * xv;
+            for (int h = 0; h < 2; ++h) {                // h = 0: (p_a, g_a), h = 1: (p_b, g_b)
+                f32x16_t ap, ag;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) ap[i] = ag[i] = 0.f;
+#pragma unroll
+                for (int ks = 0; ks < 8; ++ks) {
+                    const uint32_t o = arow(col, 2 * ks + hi);
+                    const bf16x8_t xhi = ld_frag(xa[0], o), xlo = ld_frag(xa[1], o);
+                    ap = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xhi, wp[16 * h + ks], ap, 0, 0, 0);
+                    ag = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xhi, wp[16 * h + 8 + ks], ag, 0, 0, 0);
+                    ap = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xlo, wp[16 * h + ks], ap, 0, 0, 0);
+                    ag = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xlo, wp[16 * h + 8 + ks], ag, 0, 0, 0);
+                }
+                const float* dsrc = h ? dbs : das;
+                bf16_t* bp = h ? b_dpb : b_dpa;
+                bf16_t* bg = h ? b_dgb : b_dga;
+                const int kp = 256 * h + c, kg = 256 * h + 128 + c;
+#pragma unroll
+                for (int a = 0; a < 4; ++a) {
+                    const int q0 = 8 * a + 4 * hi;
+                    const float4 dd4 = *reinterpret_cast<const float4*>(&dsrc[c * kCs + q0]);
+                    const float dd[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
+                    float vp[4], vg[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = q0 + i;
+                        const bool m = mq[q] != 0.f;
+                        const float s = sigmoidf_(ag[4 * a + i]);
+                        vp[i] = m ? dd[i] * s : 0.f;
+                        vg[i] = m ? dd[i] * ap[4 * a + i] * s * (1.f - s) : 0.f;
+                        st_hilo(d4[0], d4[1], drow(q, kp >> 3) + 2 * (kp & 7), vp[i]);
+                        st_hilo(d4[0], d4[1], drow(q, kg >> 3) + 2 * (kg & 7), vg[i]);
+                    }
+                    const int64_t bo = u * (kCh * kQ) + c * kQ + q0;
+                    *reinterpret_cast<uint2*>(bp + bo) = pack4(vp[0], vp[1], vp[2], vp[3]);
+                    *reinterpret_cast<uint2*>(bg + bo) = pack4(vg[0], vg[1], vg[2], vg[3]);
                 }
             }
-            float o0[16], o1[16], o2[16], o3[16];
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int q = 16 * ph + i;
-                const bool m = mq[q] != 0.f;
-                const float sa = 1.f / (1.f + __expf(-acc[i][1])), sb = 1.f / (1.f + __expf(-acc[i][3]));
-                const float da = das[pc * kCol + q], db = dbs[pc * kCol + q];
-                o0[i] = m ? da * sa : 0.f;
-                o1[i] = m ? da * acc[i][0] * sa * (1.f - sa) : 0.f;
-                o2[i] = m ? db * sb : 0.f;
-                o3[i] = m ? db * acc[i][2] * sb * (1.f - sb) : 0.f;
-                d4[0][pc * kCol4 + q] = o0[i];
-                d4[1][pc * kCol4 + q] = o1[i];
-                d4[2][pc * kCol4 + q] = o2[i];
-                d4[3][pc * kCol4 + q] = o3[i];
-            }
-            const int64_t bo = u * (kCh * kQ) + pc * kQ + 16 * ph;
-            st16bf(b_dpa + bo, o0);
-            st16bf(b_dga + bo, o1);
-            st16bf(b_dpb + bo, o2);
-            st16bf(b_dgb + bo, o3);
         }
         __syncthreads();
-        {   // dx = dx_g + sum over the four maps of W^T (gradient)
-            float ax[4][4];
+        {   // dx (projection part) of columns d = 32 w + col over K = 512; unit block of x
+            const int lo = opaque(lane), col = lo & 31, hi = lo >> 5;
+            f32x16_t ax;
 #pragma unroll
-            for (int a = 0; a < 4; ++a)
+            for (int i = 0; i < 16; ++i) ax[i] = 0.f;
 #pragma unroll
-                for (int b = 0; b < 4; ++b) ax[a][b] = gx[(4 * tq + a) * kRow + 4 * tg + b];
-            for (int c = 0; c < kCh; ++c) {
-                float4 w[4];
-#pragma unroll
-                for (int b = 0; b < 4; ++b) w[b] = projb[c * kCz + 4 * tg + b];
-                const float4 g0 = *reinterpret_cast<const float4*>(&d4[0][c * kCol4 + 4 * tq]);
-                const float4 g1 = *reinterpret_cast<const float4*>(&d4[1][c * kCol4 + 4 * tq]);
-                const float4 g2 = *reinterpret_cast<const float4*>(&d4[2][c * kCol4 + 4 * tq]);
-                const float4 g3 = *reinterpret_cast<const float4*>(&d4[3][c * kCol4 + 4 * tq]);
-                const float ga[4][4] = {{g0.x, g1.x, g2.x, g3.x}, {g0.y, g1.y, g2.y, g3.y},
-                                        {g0.z, g1.z, g2.z, g3.z}, {g0.w, g1.w, g2.w, g3.w}};
-#pragma unroll
-                for (int a = 0; a < 4; ++a)
-#pragma unroll
-                    for (int b = 0; b < 4; ++b)
-                        ax[a][b] += ga[a][0] * w[b].x + ga[a][1] * w[b].y + ga[a][2] * w[b].z + ga[a][3] * w[b].w;
+            for (int ks = 0; ks < 32; ++ks) {
+                const uint32_t o = drow(col, 2 * ks + hi);
+                ax = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(d4[0], o), wt[ks], ax, 0, 0, 0);
+                ax = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(d4[1], o), wt[ks], ax, 0, 0, 0);
             }
+            const int to = opaque(threadIdx.x), sc = to >> 1, sh = to & 1;
+            bf16_t* xb = b_x + u * (kCh * kQ) + sc * kQ + 16 * sh;
+            reinterpret_cast<uint4*>(xb)[0] = gather_col8(xa[0], 16 * sh, sc);
+            reinterpret_cast<uint4*>(xb)[1] = gather_col8(xa[0], 16 * sh + 8, sc);
+            const int d = 32 * w + col;
 #pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int b = 0; b < 4; ++b) gx[(4 * tq + a) * kRow + 4 * tg + b] = ax[a][b];
+            for (int i = 0; i < 16; ++i) dxs[(8 * (i >> 2) + 4 * hi + (i & 3)) * kPq4 + d] = ax[i];
         }
         __syncthreads();
-        {   // LN_in backward of pair lp, dz, dgamma_in / dbeta_in
-            const float mz = st[0][lp], rz = st[1][lp];
-            float dh[16], xh[16], s1 = 0.f, s2 = 0.f;
+        {   // LN_in backward of pair lp: dz = rz (dx gamma - mean(dx gamma) - xh mean(dx gamma xh))
+            const int t = opaque(threadIdx.x), lp = t >> 3, lq = t & 7;
+            float dx[16], xh[16], s1 = 0.f, s2 = 0.f;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const float4 p = *reinterpret_cast<const float4*>(&dxs[lp * kPq4 + 16 * lq + 4 * s]);
+                const float4 hh = *reinterpret_cast<const float4*>(&xhs[lp * kPq4 + 16 * lq + 4 * s]);
+                dx[4 * s] = p.x + xg[s].x;
+                dx[4 * s + 1] = p.y + xg[s].y;
+                dx[4 * s + 2] = p.z + xg[s].z;
+                dx[4 * s + 3] = p.w + xg[s].w;
+                xh[4 * s] = hh.x;
+                xh[4 * s + 1] = hh.y;
+                xh[4 * s + 2] = hh.z;
+                xh[4 * s + 3] = hh.w;
+            }
+            const float rz = rzs[lp];
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int d = 16 * lq + i;
-                const float dx = gx[lp * kRow + d];
-                xh[i] = (zs[lp * kRow + d] - mz) * rz;
-                dh[i] = dx * lniw[d];
-                s1 += dh[i];
-                s2 += dh[i] * xh[i];
-                acc_g[i] += dx * xh[i];
-                acc_b[i] += dx;
+                const float dh = dx[i] * prm[0][16 * lq + i];
+                s1 += dh;
+                s2 += dh * xh[i];
+                accg[i] += dx[i] * xh[i];
+                accb[i] += dx[i];
             }
             s1 = sum_lanes8(s1) * (1.f / kCz);
             s2 = sum_lanes8(s2) * (1.f / kCz);
-            if (k0 + lp < N) {
-                T* dst = dz + pair_of(r, k0 + lp) * kCz + 16 * lq;
-                float o[16];
+            uint32_t o[8];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) o[i] = rz * (dh[i] - s1 - xh[i] * s2);
-                if constexpr (sizeof(T) == 2) {
-                    st16bf(dst, o);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) dst[i] = o[i];
-                }
+            for (int i = 0; i < 8; ++i) {
+                const int d = 16 * lq + 2 * i;
+                o[i] = pack_bf16x2(rz * (dx[2 * i] * prm[0][d] - s1 - xh[2 * i] * s2),
+                                   rz * (dx[2 * i + 1] * prm[0][d + 1] - s1 - xh[2 * i + 1] * s2));
             }
-            float v[16];
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int q = 16 * bh + i;
-                v[i] = (k0 + q < N) ? xs[q * kRow + bc] : 0.f;
+            if (lp < np) {
+                uint4* dst = reinterpret_cast<uint4*>(dz + pair_of(r, k0 + lp) * kCz + 16 * lq);
+                dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+                dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
             }
-            st16bf(b_x + u * (kCh * kQ) + bc * kQ + 16 * bh, v);
         }
-        __syncthreads();
+        load_dxg(u + gridDim.x, xg);
     }
-    // reduce the per-thread LayerNorm parameter sums over the 32 pairs lanes
-    // (threads with the same lq) through LDS, then one partial per work-group
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-        xs[lp * kRow + 16 * lq + i] = acc_g[i];
-        zs[lp * kRow + 16 * lq + i] = acc_b[i];
+        das[lp * kCz + 16 * lq + i] = accg[i];
+        dbs[lp * kCz + 16 * lq + i] = accb[i];
     }
     __syncthreads();
-    if (t < kCz) {
-        float sg = 0.f, sb = 0.f;
-        for (int q = 0; q < kQ; ++q) { sg += xs[q * kRow + t]; sb += zs[q * kRow + t]; }
-        partial[((int64_t)blockIdx.x * 2 + 0) * kCz + t] = sg;
-        partial[((int64_t)blockIdx.x * 2 + 1) * kCz + t] = sb;
+    {
+        const float* src = t < kCz ? das : dbs;
+        const int d = t & (kCz - 1);
+        float s = 0.f;
+        for (int q = 0; q < kQ; ++q) s += src[q * kCz + d];
+        partial[((int64_t)blockIdx.x * 2 + (t >> 7)) * kCz + d] = s;
     }
 }
 
@@ -615,19 +828,21 @@ hipError_t launch_panel_transpose(int dtype, const void* X, void* Y, int64_t N, 
 
 namespace trimul {
 
-int backward_grid(int64_t units, int cus) { return (int)(units < 2 * (int64_t)cus ? units : 2 * (int64_t)cus); }
+int backward_grid(int64_t units, int cus, int per_cu) {
+    return (int)(units < (int64_t)per_cu * cus ? units : (int64_t)per_cu * cus);
+}
 
 hipError_t launch_epilogue_backward(int out_dtype, const DeviceWeights& w, const float* C, const void* z,
                                     const uint8_t* mask, const void* dout, int64_t N, void* dCp, float* dxg,
                                     const BackwardBlocks& bb, float* partial, int grid, hipStream_t s) {
     const int64_t units = N * ((N + 31) / 32);
     if (out_dtype == 0)
-        hipLaunchKernelGGL((k_epilogue_backward<bf16_t, float>), dim3(grid), dim3(256), 0, s, C, (const bf16_t*)z, mask,
-                           (const float*)dout, (int)N, units, w.wo_t, w.wg_t, w.wo, w.wg, w.ln_in_w, w.ln_in_b,
-                           w.ln_out_w, w.ln_out_b, w.eps, (bf16_t*)dCp, dxg, bb.du, bb.y, bb.dgg, bb.xe, partial);
+        hipLaunchKernelGGL(k_epilogue_backward<float>, dim3(grid), dim3(kBT), 0, s, C, (const bf16_t*)z, mask,
+                           (const float*)dout, (int)N, units, w.epi_bf, w.epit_bf, w.ln_in_w, w.ln_in_b, w.ln_out_w,
+                           w.ln_out_b, w.eps, (bf16_t*)dCp, dxg, bb.du, bb.y, bb.dgg, bb.xe, partial);
     else
-        hipLaunchKernelGGL((k_epilogue_backward<bf16_t, bf16_t>), dim3(grid), dim3(256), 0, s, C, (const bf16_t*)z,
-                           mask, (const bf16_t*)dout, (int)N, units, w.wo_t, w.wg_t, w.wo, w.wg, w.ln_in_w, w.ln_in_b,
+        hipLaunchKernelGGL(k_epilogue_backward<bf16_t>, dim3(grid), dim3(kBT), 0, s, C, (const bf16_t*)z, mask,
+                           (const bf16_t*)dout, (int)N, units, w.epi_bf, w.epit_bf, w.ln_in_w, w.ln_in_b,
                            w.ln_out_w, w.ln_out_b, w.eps, (bf16_t*)dCp, dxg, bb.du, bb.y, bb.dgg, bb.xe, partial);
     return hipGetLastError();
 }
@@ -636,16 +851,14 @@ hipError_t launch_projection_backward(const DeviceWeights& w, const void* z, con
                                       int incoming, const float* dA, const float* dB, const float* dxg, void* dz,
                                       const BackwardBlocks& bb, float* partial, int grid, hipStream_t s) {
     const int64_t units = N * ((N + 31) / 32);
-    const float4* p4 = reinterpret_cast<const float4*>(w.proj4);
-    const float4* pb = reinterpret_cast<const float4*>(w.projb);
     if (incoming)
-        hipLaunchKernelGGL((k_projection_backward<bf16_t, true>), dim3(grid), dim3(256), 0, s, (const bf16_t*)z, mask,
-                           (int)N, units, dA, dB, dxg, p4, pb, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)dz, bb.dpa,
-                           bb.dga, bb.dpb, bb.dgb, bb.xp, partial);
+        hipLaunchKernelGGL(k_projection_backward<true>, dim3(grid), dim3(kPT), 0, s, (const bf16_t*)z, mask, (int)N,
+                           units, dA, dB, dxg, w.proj_bf, w.projt_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)dz,
+                           bb.dpa, bb.dga, bb.dpb, bb.dgb, bb.xp, partial);
     else
-        hipLaunchKernelGGL((k_projection_backward<bf16_t, false>), dim3(grid), dim3(256), 0, s, (const bf16_t*)z, mask,
-                           (int)N, units, dA, dB, dxg, p4, pb, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)dz, bb.dpa,
-                           bb.dga, bb.dpb, bb.dgb, bb.xp, partial);
+        hipLaunchKernelGGL(k_projection_backward<false>, dim3(grid), dim3(kPT), 0, s, (const bf16_t*)z, mask, (int)N,
+                           units, dA, dB, dxg, w.proj_bf, w.projt_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)dz,
+                           bb.dpa, bb.dga, bb.dpb, bb.dgb, bb.xp, partial);
     return hipGetLastError();
 }
 

@@ -18,13 +18,12 @@ struct DeviceWeights {
     float* proj4 = nullptr;     // [c_z][c][4]: (W_a, W_ga, W_b, W_gb)[c][d] at [d][c][*]
     float* wo_t = nullptr;      // [c][c_z]:   W_o[d][c] at [c][d]
     float* wg_t = nullptr;      // [c_z][c_z]: W_g[d][e] at [e][d]
-    float* wo = nullptr;        // [c_z][c]:   W_o as given (backward)
-    float* wg = nullptr;        // [c_z][c_z]: W_g as given (backward)
-    float* projb = nullptr;     // [c][c_z][4]: (W_a, W_ga, W_b, W_gb)[c][d] at [c][d][*] (backward)
     // bf16 copies used by the MFMA kernels (bf16 storage only)
     uint16_t* proj_bf = nullptr;  // [4*c][c_z]: rows ordered per 32-channel group g:
                                   // W_a[g], W_ga[g], W_b[g], W_gb[g] (32 rows each)
     uint16_t* epi_bf = nullptr;   // [2*c_z][128]: W_o rows then W_g rows
+    uint16_t* epit_bf = nullptr;  // [2*128][c_z]: W_o^T rows then W_g^T rows (backward)
+    uint16_t* projt_bf = nullptr; // [c_z][4*c]: row d = W_a[:, d], W_ga[:, d], W_b[:, d], W_gb[:, d] (backward)
     float eps = 1e-5f;
     int cus = 256;                // compute units of the device (persistent grids)
     uint8_t* kmask_pad = nullptr; // 0/1 staging of a token mask (k-panel or whole sequence), kMaxKPanel + 64 bytes
@@ -78,7 +77,8 @@ struct BackwardBlocks {
     bf16_t *du, *y, *dgg, *xe;         // from the epilogue backward
     bf16_t *dpa, *dga, *dpb, *dgb, *xp; // from the projection backward
 };
-int backward_grid(int64_t units, int cus);
+// Persistent grid: min(units, per_cu * compute units).
+int backward_grid(int64_t units, int cus, int per_cu);
 hipError_t launch_epilogue_backward(int out_dtype, const DeviceWeights& w, const float* C, const void* z,
                                     const uint8_t* mask, const void* dout, int64_t N, void* dCp, float* dxg,
                                     const BackwardBlocks& bb, float* partial, int grid, hipStream_t s);

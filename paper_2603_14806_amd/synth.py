@@ -23,7 +23,7 @@ import torch
 SEED = 2603148060
 STREAM = {"z": 1, "w_a": 2, "w_ga": 3, "w_b": 4, "w_gb": 5, "w_g": 6, "w_o": 7,
           "scale": 8, "a_panel": 9, "b_panel": 10, "z_tile": 11,
-          "ln_in_w": 12, "ln_in_b": 13, "ln_out_w": 14, "ln_out_b": 15}
+          "ln_in_w": 12, "ln_in_b": 13, "ln_out_w": 14, "ln_out_b": 15, "dout": 16}
 
 DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
 

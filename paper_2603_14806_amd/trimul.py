@@ -18,6 +18,9 @@ TRI_MUL_OUTGOING, TRI_MUL_INCOMING = 0, 1
 DTYPE_CODE = {"f32": TRI_MUL_F32, "bf16": TRI_MUL_BF16}
 TORCH_DTYPE = {TRI_MUL_F32: torch.float32, TRI_MUL_BF16: torch.bfloat16}
 WEIGHT_FIELDS = ("ln_in_w", "ln_in_b", "w_a", "w_ga", "w_b", "w_gb", "w_g", "ln_out_w", "ln_out_b", "w_o")
+# weight (and weight-gradient) shapes for c_z = c = 128
+WEIGHT_SHAPES = {"ln_in_w": (128,), "ln_in_b": (128,), "w_a": (128, 128), "w_ga": (128, 128), "w_b": (128, 128),
+                 "w_gb": (128, 128), "w_g": (128, 128), "ln_out_w": (128,), "ln_out_b": (128,), "w_o": (128, 128)}
 
 _vp = ctypes.c_void_p
 _i32, _i64 = ctypes.c_int32, ctypes.c_int64
@@ -281,16 +284,14 @@ class TriMul:
         """Gradients of sum(out * dout) for the update of z: returns (dz,
         grads) with grads a dict of float32 tensors shaped like the weights."""
         N = z.shape[0]
-        c, cz = 128, 128
+        cz = 128
         if tuple(z.shape) != (N, N, cz) or tuple(dout.shape) != (N, N, cz):
             raise ValueError(f"z and dout must be [N, N, {cz}], got {tuple(z.shape)} and {tuple(dout.shape)}")
         if dout.dtype != TORCH_DTYPE[DTYPE_CODE[self.out_dtype]] or z.dtype != TORCH_DTYPE[DTYPE_CODE[self.dtype]]:
             raise ValueError("z must have the storage dtype and dout the output dtype of the layer")
         if not (z.is_contiguous() and dout.is_contiguous()):
             raise ValueError("z and dout must be contiguous")
-        shapes = {"ln_in_w": (cz,), "ln_in_b": (cz,), "w_a": (c, cz), "w_ga": (c, cz), "w_b": (c, cz),
-                  "w_gb": (c, cz), "w_g": (cz, cz), "ln_out_w": (c,), "ln_out_b": (c,), "w_o": (cz, c)}
-        grads = {k: torch.empty(v, dtype=torch.float32, device=self.device) for k, v in shapes.items()}
+        grads = {k: torch.empty(v, dtype=torch.float32, device=self.device) for k, v in WEIGHT_SHAPES.items()}
         dz = torch.empty_like(z)
         wsb = tri_mul_backward_workspace_size(self.h, N)
         ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
