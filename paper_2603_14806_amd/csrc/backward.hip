@@ -137,13 +137,11 @@ constexpr int kBT = 512;      // threads of the per-pair backward kernels
 constexpr int kCs = 36;       // row stride (floats) of [channel][pair] tiles
 constexpr int kPq = 132;      // row stride (floats) of [pair][channel] tiles
 constexpr int kArow = 256;    // bytes of one bf16 activation row [128]
-constexpr int kDrow = 1024;   // bytes of one bf16 row [4][128] (projection-backward A operand)
 
-// Byte offset of 16-byte chunk ch of row p in bf16 row tiles; chunks are
-// XOR-swizzled over 16 rows so that the A-operand reads (16 rows, one chunk
-// each) hit distinct banks.
+// Byte offset of 16-byte chunk ch of row p in a bf16 [q][128] tile; chunks
+// are XOR-swizzled over 16 rows so that the A-operand reads (16 rows, one
+// chunk each) hit distinct banks.
 __device__ __forceinline__ uint32_t arow(int p, int ch) { return (uint32_t)(p * kArow + ((ch ^ (p & 15)) << 4)); }
-__device__ __forceinline__ uint32_t drow(int p, int ch) { return (uint32_t)(p * kDrow + ((ch ^ (p & 15)) << 4)); }
 
 // The value itself, hidden from the optimiser: lane indices passed through
 // this inside a loop make the LDS addresses derived from them loop-variant,
@@ -172,6 +170,24 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 
 __device__ __forceinline__ bf16x8_t ld_frag(const char* base, uint32_t off) {
     return *reinterpret_cast<const bf16x8_t*>(base + off);
+}
+
+// Range-checked buffer access (make_rsrc): loads past the resource's size
+// read zero and stores past it are dropped, so tails need no branches and
+// every pass of a unit loop issues the same memory instructions (which keeps
+// the compiler's wait counts exact).
+__device__ __forceinline__ float4 bld_f4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(float4, buf_load16(r, off));
+}
+__device__ __forceinline__ uint32_t bld_u8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bst_f32(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bst_u4(__amdgpu_buffer_rsrc_t r, uint32_t off, uint4 v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)off, 0, 0);
 }
 
 // 8 bf16 of column `col` of a swizzled row tile, rows q0 .. q0 + 7, packed.
@@ -225,6 +241,44 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
     const int J = (N + kQ - 1) / kQ;
     const PanelGeom pg = panel_geom(N, N);
 
+    // Global loads of one unit, issued one unit ahead into the registers the
+    // current unit has just released; nothing here reads the loaded
+    // registers, so the loads stay in flight until the unit starts.
+    struct Pre {
+        float4 c0, c1;        // C block floats 4 t .. and 2048 + 4 t ..
+        uint4 zv;             // z of pair lp, channels 8 lq .. + 7
+        DoutRegs<TO> o;       // dout of pair lp, channels 8 lq .. + 7
+        uint32_t mr, mk;      // mask bytes of row r and of column k0 + t % 32 (zero past N)
+    };
+    auto load = [&](int64_t u, Pre& p) {
+        const bool valid = u < units;                     // past the end: zero-size resources
+        const int64_t uu = valid ? u : 0;
+        const int r = (int)(uu / J), k0 = (int)(uu - (int64_t)r * J) * kQ;
+        const int np = min(kQ, N - k0);
+        const int64_t pr0 = (int64_t)r * N + k0;          // the unit's first pair
+        const auto rc = make_rsrc(C + uu * (kCh * kQ), valid ? kCh * kQ * 4 : 0);
+        p.c0 = bld_f4(rc, 16 * t);
+        p.c1 = bld_f4(rc, 16 * (t + kBT));
+        const auto rzr = make_rsrc(z + pr0 * kCz, valid ? np * kCz * 2 : 0);
+        p.zv = buf_load16(rzr, lp * kCz * 2 + 16 * lq);
+        if constexpr (sizeof(TO) == 4) {
+            const auto ro = make_rsrc(dout + pr0 * kCz, valid ? np * kCz * 4 : 0);
+            p.o.a = bld_f4(ro, lp * kCz * 4 + 32 * lq);
+            p.o.b = bld_f4(ro, lp * kCz * 4 + 32 * lq + 16);
+        } else {
+            const auto ro = make_rsrc(dout + pr0 * kCz, valid ? np * kCz * 2 : 0);
+            p.o.a = buf_load16(ro, lp * kCz * 2 + 16 * lq);
+        }
+        const auto rm = make_rsrc(mask, (valid && mask) ? (uint32_t)N : 0u);
+        p.mr = bld_u8(rm, opaque(r));                    // per lane: a uniform load would be waited for at once
+        p.mk = bld_u8(rm, k0 + (t & (kQ - 1)));
+    };
+
+    float accg[8], accb[8];                              // dgamma_out, dbeta_out of c = lq + 16 i
+#pragma unroll
+    for (int i = 0; i < 8; ++i) accg[i] = accb[i] = 0.f;
+    Pre cur;
+    load(blockIdx.x, cur);
     bf16x8_t wo[4], wg[4], wot[4], wgt[4];               // B operands: W_o, W_g rows n; W_o^T, W_g^T rows n
     {
         const int n = 16 * w + col;
@@ -244,49 +298,12 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
         prm[3][t] = lnib[t];
     }
 
-    // Global loads of one unit, issued one unit ahead; nothing here reads the
-    // loaded registers, so the loads stay in flight until the unit starts.
-    struct Pre {
-        float4 c0, c1;        // C block floats 4 t .. and 2048 + 4 t ..
-        uint4 zv;             // z of pair lp, channels 8 lq .. + 7
-        DoutRegs<TO> o;       // dout of pair lp, channels 8 lq .. + 7
-        uint32_t mr, mk;      // mask bytes of row r and of column k0 + t (t < 32)
-    };
-    auto load = [&](int64_t u, Pre& p) {
-        p.c0 = p.c1 = make_float4(0.f, 0.f, 0.f, 0.f);
-        p.zv = make_uint4(0, 0, 0, 0);
-        if constexpr (sizeof(TO) == 4) p.o.a = p.o.b = make_float4(0.f, 0.f, 0.f, 0.f);
-        else p.o.a = make_uint4(0, 0, 0, 0);
-        p.mr = p.mk = 1;
-        if (u >= units) return;
-        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
-        const float4* cb = reinterpret_cast<const float4*>(C + u * (kCh * kQ));
-        p.c0 = cb[t];
-        p.c1 = cb[t + kBT];
-        if (k0 + lp < N) {
-            const int64_t pr = (int64_t)r * N + k0 + lp;
-            p.zv = *reinterpret_cast<const uint4*>(z + pr * kCz + 8 * lq);
-            if constexpr (sizeof(TO) == 4) {
-                p.o.a = *reinterpret_cast<const float4*>(dout + pr * kCz + 8 * lq);
-                p.o.b = *reinterpret_cast<const float4*>(dout + pr * kCz + 8 * lq + 4);
-            } else {
-                p.o.a = *reinterpret_cast<const uint4*>(dout + pr * kCz + 8 * lq);
-            }
-        }
-        if (mask && t < kQ) {
-            p.mr = mask[r];
-            if (k0 + t < N) p.mk = mask[k0 + t];
-        }
-    };
-
-    float accg[8], accb[8];                              // dgamma_out, dbeta_out of c = lq + 16 i
-#pragma unroll
-    for (int i = 0; i < 8; ++i) accg[i] = accb[i] = 0.f;
-    Pre cur, nxt;
-    load(blockIdx.x, cur);
+    // Everything issued so far completes here, in a wait the compiler sees
+    // (otherwise its waits for the weights land inside the unit loop).
+    wait_vmcnt<0>();
+    __syncthreads();
 
     for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
-        load(u + gridDim.x, nxt);
         const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
         const int np = min(kQ, N - k0);
         {   // stage C (columns past N read as zero) and the pair mask
@@ -300,25 +317,7 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
             }
             *reinterpret_cast<float4*>(&cs[c * kCs + q]) = a;
             *reinterpret_cast<float4*>(&cs[(c + 64) * kCs + q]) = b;
-            if (t < kQ) mq[t] = (t < np && cur.mr != 0 && cur.mk != 0) ? 1.f : 0.f;
-        }
-        __syncthreads();
-        float yh[8], rs;                                 // LN_out(C) normalised, c = lq + 16 i; 1 / std
-        {   // LN_out of pair lp over c = lq + 16 i -> y hi / lo rows
-            float s1 = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) { yh[i] = cs[(lq + 16 * i) * kCs + lp]; s1 += yh[i]; }
-            const float mu = sum_lanes16(s1) * (1.f / kCh);
-            float q2 = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) { yh[i] -= mu; q2 += yh[i] * yh[i]; }
-            rs = rsqrtf(sum_lanes16(q2) * (1.f / kCh) + eps);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int c = lq + 16 * i;
-                yh[i] *= rs;
-                st_hilo(act[0], act[1], arow(lp, c >> 3) + 2 * (c & 7), yh[i] * prm[0][c] + prm[1][c]);
-            }
+            if (t < kQ) mq[t] = (t < np && (!mask || (cur.mr != 0 && cur.mk != 0))) ? 1.f : 0.f;
         }
         {   // LN_in of pair lp over d = 8 lq + i -> x hi / lo rows; dout -> dq
             const uint32_t zw[4] = {cur.zv.x, cur.zv.y, cur.zv.z, cur.zv.w};
@@ -359,6 +358,25 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
             }
             *reinterpret_cast<float4*>(&dq[lp * kPq + 8 * lq]) = o0;
             *reinterpret_cast<float4*>(&dq[lp * kPq + 8 * lq + 4]) = o1;
+        }
+        load(u + gridDim.x, cur);                        // the next unit, into the released registers
+        __syncthreads();
+        float yh[8], rs;                                 // LN_out(C) normalised, c = lq + 16 i; 1 / std
+        {   // LN_out of pair lp over c = lq + 16 i -> y hi / lo rows
+            float s1 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) { yh[i] = cs[(lq + 16 * i) * kCs + lp]; s1 += yh[i]; }
+            const float mu = sum_lanes16(s1) * (1.f / kCh);
+            float q2 = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) { yh[i] -= mu; q2 += yh[i] * yh[i]; }
+            rs = rsqrtf(sum_lanes16(q2) * (1.f / kCh) + eps);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = lq + 16 * i;
+                yh[i] *= rs;
+                st_hilo(act[0], act[1], arow(lp, c >> 3) + 2 * (c & 7), yh[i] * prm[0][c] + prm[1][c]);
+            }
         }
         __syncthreads();
         {   // u = y W_o^T, gg = x W_g^T (columns d = 16 w + col); du, dgg
@@ -414,13 +432,14 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
                     ax[mb] = mfma16(ld_frag(act2[3], o), wgt[ks], ax[mb]);
                 }
             const int n = 16 * w + col;
+            const auto rx = make_rsrc(dxg + ((int64_t)r * N + k0) * kCz, np * kCz * 4);   // pairs past N: dropped
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int q = 16 * mb + 4 * kq + i;
                     dq[q * kPq + n] = ay[mb][i];
-                    if (q < np) dxg[((int64_t)r * N + k0 + q) * kCz + n] = ax[mb][i];
+                    bst_f32(rx, (q * kCz + n) * 4, ax[mb][i]);
                 }
         }
         __syncthreads();
@@ -451,7 +470,6 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
             *reinterpret_cast<uint4*>(dCp + panel_off(pg, sc, r, k0 + 8 * sq)) =
                 make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
         }
-        cur = nxt;
     }
     // per-work-group sums over the pairs lanes (lp) through LDS
     __syncthreads();
@@ -474,7 +492,9 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
 // (outgoing) or (k, r) (incoming).  Recompute x = LN_in(z) and the four
 // projections p_a, g_a, p_b, g_b (pre-sigmoid gates); then
 //   dpa = da m s_a,  dga = da m p_a s_a (1 - s_a)  (the same for b),
-//   dx = dx_g + [dpa dga dpb dgb] [W_a; W_ga; W_b; W_gb],  dz = LN_in backward of dx.
+//   dx = dx_g + [dpa dga dpb dgb] [W_a; W_ga; W_b; W_gb],  dz = LN_in backward of dx
+// (the four gradients enter that product rounded to bf16; x enters the
+// projections as bf16 hi + lo).
 // Writes dz, unit blocks dpa, dga, dpb, dgb, x, and per-work-group sums of
 // dgamma_in, dbeta_in at partial[(2 wg + {0, 1}) * 128 + d].
 //
@@ -488,6 +508,24 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
 // 8 (i / 4) + 4 (l / 32) + i % 4, i = 0 .. 15.
 constexpr int kPT = 256;      // threads of the projection backward
 constexpr int kPq4 = 136;     // [pair][channel] row stride: rows 4 apart land 32 banks apart
+// Padded bf16 row tiles: a row of 128 (x) or 512 (the four gradients)
+// values plus one 16-byte chunk, so the 16 rows an operand read touches
+// start 4 banks apart (conflict-free) and every access is the lane's base
+// address plus an immediate offset.
+constexpr int kXrow = 256 + 16;
+constexpr int kGrow = 1024 + 16;
+
+// 8 bf16 of column `col` of a padded [q][128] bf16 tile, rows q0 .. q0 + 7, packed.
+__device__ __forceinline__ uint4 gather_col8p(const char* tile, int q0, int col) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t a = *reinterpret_cast<const bf16_t*>(tile + (q0 + 2 * i) * kXrow + 2 * col);
+        const uint32_t b = *reinterpret_cast<const bf16_t*>(tile + (q0 + 2 * i + 1) * kXrow + 2 * col);
+        w[i] = a | (b << 16);
+    }
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
 
 template <bool INCOMING>
 __global__ __attribute__((amdgpu_flat_work_group_size(kPT, kPT), amdgpu_waves_per_eu(1, 1)))
@@ -499,8 +537,8 @@ void k_projection_backward(
     bf16_t* __restrict__ b_dgb, bf16_t* __restrict__ b_x, float* __restrict__ partial) {
     __shared__ __align__(16) float das[kCh * kCs];       // da [c][q]
     __shared__ __align__(16) float dbs[kCh * kCs];       // db [c][q]
-    __shared__ __align__(16) char xa[2][kQ * kArow];     // x hi, x lo  [q][128]
-    __shared__ __align__(16) char d4[2][kQ * kDrow];     // hi, lo  [q][dpa | dga | dpb | dgb]
+    __shared__ __align__(16) char xa[2][kQ * kXrow];     // x hi, x lo  [q][128]
+    __shared__ __align__(16) char d4[kQ * kGrow];        // bf16 [q][dpa | dga | dpb | dgb]
     __shared__ __align__(16) float dxs[kQ * kPq4];       // dx from the projections [q][d]
     __shared__ __align__(16) float xhs[kQ * kPq4];       // LN_in(z) normalised [q][d]
     __shared__ float rzs[kQ];                            // 1 / std of LN_in per pair
@@ -511,6 +549,54 @@ void k_projection_backward(
     const int J = (N + kQ - 1) / kQ;
     auto pair_of = [&](int r, int k) -> int64_t { return INCOMING ? (int64_t)k * N + r : (int64_t)r * N + k; };
 
+
+    // One unit's loads, issued one unit ahead; dx_g is fetched separately
+    // (it is used last).  Nothing here reads the loaded registers.
+    struct Pre {
+        float4 a[4], b[4];       // dA, dB block floats 4 (t + 256 s) ..
+        uint4 z0, z1;            // z of pair lp, channels 16 lq .. + 15
+        uint32_t mr, mk;
+    };
+    // Byte distance between consecutive pairs of a unit in [pair][c_z]
+    // tensors: adjacent columns (outgoing) or adjacent rows (incoming).
+    const uint32_t step2 = INCOMING ? (uint32_t)N * kCz * 2 : kCz * 2;   // bf16
+    const uint32_t step4 = 2 * step2;                                    // fp32
+    auto load = [&](int64_t u, Pre& p) {
+        const bool valid = u < units;                     // past the end: zero-size resources
+        const int64_t uu = valid ? u : 0;
+        const int r = (int)(uu / J), k0 = (int)(uu - (int64_t)r * J) * kQ;
+        const int np = min(kQ, N - k0);
+        const auto ra = make_rsrc(dA + uu * (kCh * kQ), valid ? kCh * kQ * 4 : 0);
+        const auto rb = make_rsrc(dB + uu * (kCh * kQ), valid ? kCh * kQ * 4 : 0);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            p.a[s] = bld_f4(ra, 16 * (t + kPT * s));
+            p.b[s] = bld_f4(rb, 16 * (t + kPT * s));
+        }
+        const auto rzr = make_rsrc(z + pair_of(r, k0) * kCz, valid ? (np - 1) * step2 + kCz * 2 : 0);
+        p.z0 = buf_load16(rzr, lp * step2 + 32 * lq);
+        p.z1 = buf_load16(rzr, lp * step2 + 32 * lq + 16);
+        const auto rm = make_rsrc(mask, (valid && mask) ? (uint32_t)N : 0u);
+        p.mr = bld_u8(rm, opaque(r));                    // per lane: a uniform load would be waited for at once
+        p.mk = bld_u8(rm, k0 + (t & (kQ - 1)));
+    };
+    auto load_dxg = [&](int64_t u, float4 (&g)[4]) {
+        const bool valid = u < units;
+        const int64_t uu = valid ? u : 0;
+        const int r = (int)(uu / J), k0 = (int)(uu - (int64_t)r * J) * kQ;
+        const int np = min(kQ, N - k0);
+        const auto rg = make_rsrc(dxg + pair_of(r, k0) * kCz, valid ? (np - 1) * step4 + kCz * 4 : 0);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) g[s] = bld_f4(rg, lp * step4 + 64 * lq + 16 * s);
+    };
+
+    float accg[16], accb[16];                            // dgamma_in, dbeta_in of d = 16 lq + i
+#pragma unroll
+    for (int i = 0; i < 16; ++i) accg[i] = accb[i] = 0.f;
+    Pre cur;
+    float4 xg[4];
+    load(blockIdx.x, cur);
+    load_dxg(blockIdx.x, xg);
     bf16x8_t wp[32], wt[32];   // wp[8 m + ks]: map m, k = 16 ks + 8 hi;  wt[ks]: k = 16 ks + 8 hi
     {
         const int col = lane & 31, hi = lane >> 5;
@@ -525,58 +611,11 @@ void k_projection_backward(
         prm[0][t] = lniw[t];
         prm[1][t] = lnib[t];
     }
+    // Everything issued so far completes here, in a wait the compiler sees:
+    // otherwise it places the waits for the weights inside the unit loop,
+    // where on later passes they stall on the next unit's prefetch.
+    wait_vmcnt<0>();
     __syncthreads();   // the first unit's LN_in reads prm before the loop's first barrier
-
-    // One unit's loads, issued one unit ahead; dx_g is fetched separately
-    // (it is used last).  Nothing here reads the loaded registers.
-    struct Pre {
-        float4 a[4], b[4];       // dA, dB block floats 4 (t + 256 s) ..
-        uint4 z0, z1;            // z of pair lp, channels 16 lq .. + 15
-        uint32_t mr, mk;
-    };
-    auto load = [&](int64_t u, Pre& p) {
-#pragma unroll
-        for (int s = 0; s < 4; ++s) p.a[s] = p.b[s] = make_float4(0.f, 0.f, 0.f, 0.f);
-        p.z0 = p.z1 = make_uint4(0, 0, 0, 0);
-        p.mr = p.mk = 1;
-        if (u >= units) return;
-        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
-        const float4* ab = reinterpret_cast<const float4*>(dA + u * (kCh * kQ));
-        const float4* bb = reinterpret_cast<const float4*>(dB + u * (kCh * kQ));
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            p.a[s] = ab[t + kPT * s];
-            p.b[s] = bb[t + kPT * s];
-        }
-        if (k0 + lp < N) {
-            const uint4* zs = reinterpret_cast<const uint4*>(z + pair_of(r, k0 + lp) * kCz + 16 * lq);
-            p.z0 = zs[0];
-            p.z1 = zs[1];
-        }
-        if (mask && t < kQ) {
-            p.mr = mask[r];
-            if (k0 + t < N) p.mk = mask[k0 + t];
-        }
-    };
-    auto load_dxg = [&](int64_t u, float4 (&g)[4]) {
-#pragma unroll
-        for (int s = 0; s < 4; ++s) g[s] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (u >= units) return;
-        const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
-        if (k0 + lp < N) {
-            const float4* src = reinterpret_cast<const float4*>(dxg + pair_of(r, k0 + lp) * kCz + 16 * lq);
-#pragma unroll
-            for (int s = 0; s < 4; ++s) g[s] = src[s];
-        }
-    };
-
-    float accg[16], accb[16];                            // dgamma_in, dbeta_in of d = 16 lq + i
-#pragma unroll
-    for (int i = 0; i < 16; ++i) accg[i] = accb[i] = 0.f;
-    Pre cur;
-    float4 xg[4];
-    load(blockIdx.x, cur);
-    load_dxg(blockIdx.x, xg);
 
     for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
         const int r = (int)(u / J), k0 = (int)(u - (int64_t)r * J) * kQ;
@@ -590,7 +629,7 @@ void k_projection_backward(
                 *reinterpret_cast<float4*>(&das[c * kCs + q]) = cur.a[s];
                 *reinterpret_cast<float4*>(&dbs[c * kCs + q]) = cur.b[s];
             }
-            if (t < kQ) mq[t] = (t < np && cur.mr != 0 && cur.mk != 0) ? 1.f : 0.f;
+            if (t < kQ) mq[t] = (t < np && (!mask || (cur.mr != 0 && cur.mk != 0))) ? 1.f : 0.f;
             const uint32_t zw[8] = {cur.z0.x, cur.z0.y, cur.z0.z, cur.z0.w, cur.z1.x, cur.z1.y, cur.z1.z, cur.z1.w};
             float s1 = 0.f;
 #pragma unroll
@@ -616,10 +655,10 @@ void k_projection_backward(
                 hw[i] = pack_bf16x2(x0, x1);
                 lw[i] = pack_bf16x2(x0 - __uint_as_float(hw[i] << 16), x1 - __uint_as_float(hw[i] & 0xffff0000u));
             }
-            *reinterpret_cast<uint4*>(xa[0] + arow(lp, 2 * lq)) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-            *reinterpret_cast<uint4*>(xa[0] + arow(lp, 2 * lq + 1)) = make_uint4(hw[4], hw[5], hw[6], hw[7]);
-            *reinterpret_cast<uint4*>(xa[1] + arow(lp, 2 * lq)) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
-            *reinterpret_cast<uint4*>(xa[1] + arow(lp, 2 * lq + 1)) = make_uint4(lw[4], lw[5], lw[6], lw[7]);
+            *reinterpret_cast<uint4*>(xa[0] + lp * kXrow + 32 * lq) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            *reinterpret_cast<uint4*>(xa[0] + lp * kXrow + 32 * lq + 16) = make_uint4(hw[4], hw[5], hw[6], hw[7]);
+            *reinterpret_cast<uint4*>(xa[1] + lp * kXrow + 32 * lq) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+            *reinterpret_cast<uint4*>(xa[1] + lp * kXrow + 32 * lq + 16) = make_uint4(lw[4], lw[5], lw[6], lw[7]);
         }
         load(u + gridDim.x, cur);                        // next unit's dA, dB, z, mask
         __syncthreads();
@@ -641,7 +680,7 @@ void k_projection_backward(
                 for (int i = 0; i < 16; ++i) ap[i] = ag[i] = 0.f;
 #pragma unroll
                 for (int ks = 0; ks < 8; ++ks) {
-                    const uint32_t o = arow(col, 2 * ks + hi);
+                    const uint32_t o = col * kXrow + 32 * ks + 16 * hi;
                     const bf16x8_t xhi = ld_frag(xa[0], o), xlo = ld_frag(xa[1], o);
                     ap = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xhi, wp[16 * h + ks], ap, 0, 0, 0);
                     ag = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xhi, wp[16 * h + 8 + ks], ag, 0, 0, 0);
@@ -665,8 +704,8 @@ void k_projection_backward(
                         const float s = sigmoidf_(ag[4 * a + i]);
                         vp[i] = m ? dd[i] * s : 0.f;
                         vg[i] = m ? dd[i] * ap[4 * a + i] * s * (1.f - s) : 0.f;
-                        st_hilo(d4[0], d4[1], drow(q, kp >> 3) + 2 * (kp & 7), vp[i]);
-                        st_hilo(d4[0], d4[1], drow(q, kg >> 3) + 2 * (kg & 7), vg[i]);
+                        *reinterpret_cast<bf16_t*>(d4 + q * kGrow + 2 * kp) = f2bf(vp[i]);
+                        *reinterpret_cast<bf16_t*>(d4 + q * kGrow + 2 * kg) = f2bf(vg[i]);
                     }
                     const int64_t bo = u * (kCh * kQ) + c * kQ + q0;
                     *reinterpret_cast<uint2*>(bp + bo) = pack4(vp[0], vp[1], vp[2], vp[3]);
@@ -681,15 +720,12 @@ void k_projection_backward(
 #pragma unroll
             for (int i = 0; i < 16; ++i) ax[i] = 0.f;
 #pragma unroll
-            for (int ks = 0; ks < 32; ++ks) {
-                const uint32_t o = drow(col, 2 * ks + hi);
-                ax = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(d4[0], o), wt[ks], ax, 0, 0, 0);
-                ax = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(d4[1], o), wt[ks], ax, 0, 0, 0);
-            }
+            for (int ks = 0; ks < 32; ++ks)
+                ax = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(d4, col * kGrow + 32 * ks + 16 * hi), wt[ks], ax, 0, 0, 0);
             const int to = opaque(threadIdx.x), sc = to >> 1, sh = to & 1;
             bf16_t* xb = b_x + u * (kCh * kQ) + sc * kQ + 16 * sh;
-            reinterpret_cast<uint4*>(xb)[0] = gather_col8(xa[0], 16 * sh, sc);
-            reinterpret_cast<uint4*>(xb)[1] = gather_col8(xa[0], 16 * sh + 8, sc);
+            reinterpret_cast<uint4*>(xb)[0] = gather_col8p(xa[0], 16 * sh, sc);
+            reinterpret_cast<uint4*>(xb)[1] = gather_col8p(xa[0], 16 * sh + 8, sc);
             const int d = 32 * w + col;
 #pragma unroll
             for (int i = 0; i < 16; ++i) dxs[(8 * (i >> 2) + 4 * hi + (i & 3)) * kPq4 + d] = ax[i];
@@ -729,11 +765,9 @@ void k_projection_backward(
                 o[i] = pack_bf16x2(rz * (dx[2 * i] * prm[0][d] - s1 - xh[2 * i] * s2),
                                    rz * (dx[2 * i + 1] * prm[0][d + 1] - s1 - xh[2 * i + 1] * s2));
             }
-            if (lp < np) {
-                uint4* dst = reinterpret_cast<uint4*>(dz + pair_of(r, k0 + lp) * kCz + 16 * lq);
-                dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
-                dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
-            }
+            const auto rd = make_rsrc(dz + pair_of(r, k0) * kCz, (np - 1) * step2 + kCz * 2);   // pairs past N: dropped
+            bst_u4(rd, lp * step2 + 32 * lq, make_uint4(o[0], o[1], o[2], o[3]));
+            bst_u4(rd, lp * step2 + 32 * lq + 16, make_uint4(o[4], o[5], o[6], o[7]));
         }
         load_dxg(u + gridDim.x, xg);
     }
