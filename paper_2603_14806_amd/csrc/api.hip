@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "tri_mul.h"
+#include "opm.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -18,6 +19,14 @@ struct tri_mul_handle_s {
     int c_z = 0, c = 0, dtype = 0, out_dtype = 0;
     int device = 0;
     DeviceWeights w;
+    std::vector<void*> allocations;
+};
+
+struct opm_handle_s {
+    int d = 0, c_z = 0, out_dtype = 0;
+    int device = 0, cus = 256;
+    uint16_t* wo = nullptr;   // [c_z][d * d] bf16
+    float* bo = nullptr;      // [c_z] fp32
     std::vector<void*> allocations;
 };
 
@@ -518,6 +527,179 @@ int tri_mul_outgoing_backward(tri_mul_handle_t h, const void* z, const uint8_t* 
 int tri_mul_incoming_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
                               void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream) {
     return run_backward(h, z, mask, N, dout, dz, grads, ws, ws_bytes, stream, 1);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- outer product mean
+
+namespace {
+
+constexpr int64_t kOpmMaxTile = 2048;    // tokens per tile side: rows * d <= 65536 contraction rows
+constexpr int64_t kOpmMaxSeq = 65536;    // sequences per step
+
+size_t opm_panel_bytes(int64_t rows, int64_t K) {
+    return round256((size_t)trimul::panel_elems(trimul::panel_geom(rows, K)) * 2);
+}
+size_t opm_sum_bytes(int64_t rows, int64_t cols) { return round256((size_t)rows * 32 * (size_t)cols * 32 * 4); }
+size_t opm_cnt_bytes(int64_t rows, int64_t cols) { return round256((size_t)rows * (size_t)((cols + 31) / 32 * 32) * 4); }
+
+int opm_check(opm_handle_t h) { return h ? TRI_MUL_OK : fail(TRI_MUL_EINVAL, "null handle"); }
+
+}  // namespace
+
+extern "C" {
+
+int opm_init(opm_handle_t* out, const opm_params_t* p, void* stream) {
+    if (!out || !p) return fail(TRI_MUL_EINVAL, "null handle or params pointer");
+    *out = nullptr;
+    if (p->out_dtype != TRI_MUL_F32 && p->out_dtype != TRI_MUL_BF16) return fail(TRI_MUL_EINVAL, "bad out_dtype %d", p->out_dtype);
+    if (p->d <= 0 || p->c_z <= 0) return fail(TRI_MUL_EINVAL, "d = %d, c_z = %d must be positive", p->d, p->c_z);
+    if (p->d != 32 || p->c_z != 128) return fail(TRI_MUL_EUNSUPPORTED, "only d = 32, c_z = 128 is supported (got %d, %d)", p->d, p->c_z);
+    if (!p->w_o) return fail(TRI_MUL_EINVAL, "null w_o");
+    opm_handle_t h = new (std::nothrow) opm_handle_s;
+    if (!h) return fail(TRI_MUL_ENOMEM, "host allocation failed");
+    h->d = p->d;
+    h->c_z = p->c_z;
+    h->out_dtype = p->out_dtype;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipGetDevice(&h->device);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, h->device);
+    const size_t nw = (size_t)h->c_z * h->d * h->d;
+    std::vector<uint16_t> bias_raw(h->c_z, 0);
+    if (e == hipSuccess && p->b_o) e = hipMemcpyAsync(bias_raw.data(), p->b_o, h->c_z * 2, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    int rc = e == hipSuccess ? TRI_MUL_OK : hip_fail(e, "opm init");
+    std::vector<float> bias(h->c_z);
+    for (int i = 0; i < h->c_z; ++i) bias[i] = (float)to_double(reinterpret_cast<unsigned char*>(&bias_raw[i]), TRI_MUL_BF16);
+    void* pw = nullptr;
+    if (!rc) {
+        e = hipMalloc(&pw, nw * 2);
+        if (e != hipSuccess) rc = fail(TRI_MUL_ENOMEM, "hipMalloc of %zu bytes: %s", nw * 2, hipGetErrorString(e));
+        else h->allocations.push_back(pw);
+    }
+    if (!rc) {
+        e = hipMemcpyAsync(pw, p->w_o, nw * 2, hipMemcpyDeviceToDevice, s);
+        if (e != hipSuccess) rc = hip_fail(e, "w_o copy");
+        h->wo = static_cast<uint16_t*>(pw);
+    }
+    void* pb = nullptr;
+    if (!rc) {
+        e = hipMalloc(&pb, h->c_z * 4);
+        if (e != hipSuccess) rc = fail(TRI_MUL_ENOMEM, "hipMalloc of %d bytes: %s", h->c_z * 4, hipGetErrorString(e));
+        else h->allocations.push_back(pb);
+    }
+    if (!rc) {
+        e = hipMemcpyAsync(pb, bias.data(), h->c_z * 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) rc = hip_fail(e, "b_o upload");
+        h->bo = static_cast<float*>(pb);
+    }
+    if (rc) {
+        for (void* q : h->allocations) (void)hipFree(q);
+        delete h;
+        return rc;
+    }
+    *out = h;
+    return ok();
+}
+
+int opm_destroy(opm_handle_t h) {
+    if (!h) return ok();
+    hipError_t e = hipDeviceSynchronize();
+    for (void* q : h->allocations) (void)hipFree(q);
+    delete h;
+    if (e != hipSuccess) return hip_fail(e, "destroy synchronisation");
+    return ok();
+}
+
+int opm_accumulator_size(opm_handle_t h, int64_t rows, int64_t cols, size_t* bytes) {
+    if (int rc = opm_check(h)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    if (rows < 1 || cols < 1 || rows > kOpmMaxTile || cols > kOpmMaxTile)
+        return fail(TRI_MUL_EINVAL, "tile %lld x %lld outside [1, %lld]^2", (long long)rows, (long long)cols, (long long)kOpmMaxTile);
+    *bytes = opm_sum_bytes(rows, cols) + opm_cnt_bytes(rows, cols);
+    return ok();
+}
+
+int opm_workspace_size(opm_handle_t h, int64_t rows, int64_t cols, int64_t slen, size_t* bytes) {
+    if (int rc = opm_check(h)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    if (rows < 1 || cols < 1 || rows > kOpmMaxTile || cols > kOpmMaxTile)
+        return fail(TRI_MUL_EINVAL, "tile %lld x %lld outside [1, %lld]^2", (long long)rows, (long long)cols, (long long)kOpmMaxTile);
+    if (slen < 1 || slen > kOpmMaxSeq) return fail(TRI_MUL_EINVAL, "slen = %lld outside [1, %lld]", (long long)slen, (long long)kOpmMaxSeq);
+    *bytes = opm_panel_bytes(rows * 32, slen) + opm_panel_bytes(cols * 32, slen) + opm_panel_bytes(rows, slen) +
+             opm_panel_bytes(cols, slen);
+    return ok();
+}
+
+int opm_block_accumulate(opm_handle_t h, const opm_block_view_t* v, const void* a, const void* b,
+                         const uint8_t* mask, float* acc, void* out_tile, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = opm_check(h)) return rc;
+    if (!v) return fail(TRI_MUL_EINVAL, "null view");
+    if (!a || !b || !acc || !ws) return fail(TRI_MUL_EINVAL, "null a, b, accumulator or workspace pointer");
+    if (v->n_total < 1 || v->s_total < 1 || v->rows < 1 || v->cols < 1 || v->slen < 1 || v->row0 < 0 || v->col0 < 0 ||
+        v->s0 < 0 || v->row0 + v->rows > v->n_total || v->col0 + v->cols > v->n_total || v->s0 + v->slen > v->s_total)
+        return fail(TRI_MUL_EINVAL, "view outside the %lld tokens x %lld sequences", (long long)v->n_total, (long long)v->s_total);
+    if (v->k_count < 1 || v->k_index < 0 || v->k_index >= v->k_count)
+        return fail(TRI_MUL_EINVAL, "bad k_index %d / k_count %d", v->k_index, v->k_count);
+    size_t need = 0;
+    if (int rc = opm_workspace_size(h, v->rows, v->cols, v->slen, &need)) return rc;
+    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed", ws_bytes, need);
+    if (!aligned16(a) || !aligned16(b) || !aligned16(acc)) return fail(TRI_MUL_EINVAL, "a, b and the accumulator must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
+    const bool last = v->k_index == v->k_count - 1;
+    if (last && (!out_tile || !aligned16(out_tile))) return fail(TRI_MUL_EINVAL, "the last step needs a 16-byte aligned out_tile");
+    char* p = static_cast<char*>(ws);
+    void* PA = p;
+    p += opm_panel_bytes(v->rows * 32, v->slen);
+    void* PB = p;
+    p += opm_panel_bytes(v->cols * 32, v->slen);
+    void* MA = p;
+    p += opm_panel_bytes(v->rows, v->slen);
+    void* MB = p;
+    float* sums = acc;
+    float* cnt = reinterpret_cast<float*>(reinterpret_cast<char*>(acc) + opm_sum_bytes(v->rows, v->cols));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = trimul::launch_opm_pack(a, mask, v->n_total, v->row0, v->rows, v->s0, v->slen, PA, MA, s);
+    if (e == hipSuccess) e = trimul::launch_opm_pack(b, mask, v->n_total, v->col0, v->cols, v->s0, v->slen, PB, MB, s);
+    if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
+    const int accumulate = v->k_index > 0;
+    e = trimul::launch_contract(TRI_MUL_BF16, 1, PA, PB, sums, v->rows * 32, v->cols * 32, v->slen, 0, 0, 0, 0, 0, 0,
+                                1, accumulate, nullptr, h->cus, s);
+    if (e == hipSuccess)
+        e = trimul::launch_contract(TRI_MUL_BF16, 1, MA, MB, cnt, v->rows, v->cols, v->slen, 0, 0, 0, 0, 0, 0, 1,
+                                    accumulate, nullptr, h->cus, s);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    if (last) {
+        e = trimul::launch_opm_epilogue(h->out_dtype == TRI_MUL_BF16, sums, cnt, v->rows, v->cols, h->wo, h->bo,
+                                        out_tile, h->cus, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    }
+    return ok();
+}
+
+int opm_forward_workspace_size(opm_handle_t h, int64_t S, int64_t N, size_t* bytes) {
+    if (int rc = opm_check(h)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    size_t accb = 0, wsb = 0;
+    if (int rc = opm_accumulator_size(h, N, N, &accb)) return rc;
+    if (int rc = opm_workspace_size(h, N, N, S, &wsb)) return rc;
+    *bytes = accb + wsb;
+    return ok();
+}
+
+int opm_forward(opm_handle_t h, const void* a, const void* b, const uint8_t* mask, int64_t S, int64_t N,
+                void* out, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = opm_check(h)) return rc;
+    if (!ws) return fail(TRI_MUL_EINVAL, "null workspace pointer");
+    size_t need = 0, accb = 0;
+    if (int rc = opm_forward_workspace_size(h, S, N, &need)) return rc;
+    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed", ws_bytes, need);
+    if (int rc = opm_accumulator_size(h, N, N, &accb)) return rc;
+    const opm_block_view_t v{N, S, 0, N, 0, N, 0, S, 0, 1};
+    return opm_block_accumulate(h, &v, a, b, mask, static_cast<float*>(ws), out, static_cast<char*>(ws) + accb,
+                                ws_bytes - accb, stream);
 }
 
 }  // extern "C"

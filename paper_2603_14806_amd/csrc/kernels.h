@@ -88,4 +88,15 @@ hipError_t launch_projection_backward(const DeviceWeights& w, const void* z, con
 hipError_t launch_wgrad(const bf16_t* U, const bf16_t* V, int64_t N, float* partial, int grid, hipStream_t s);
 hipError_t launch_sum_parts(const float* in, int parts, int64_t stride, int n, float* out, hipStream_t s);
 
+// Outer product mean (opm.hip).  Pack: tokens [tok0, tok0 + ntok) and
+// sequences [s0, s0 + slen) of a [S][n_total][32] bf16 tensor, masked, into
+// the blocked panel of ntok * 32 rows and K = slen (row token * 32 + c), and
+// the 0/1 mask into the blocked panel of ntok rows.  Epilogue: out[rows][cols][128]
+// from the sums O (result layout, [rows * 32][cols * 32]) and the counts
+// (result layout, [rows][32 * ceil(cols / 32)]).
+hipError_t launch_opm_pack(const void* a, const uint8_t* mask, int64_t n_total, int64_t tok0, int64_t ntok,
+                           int64_t s0, int64_t slen, void* P, void* Mp, hipStream_t s);
+hipError_t launch_opm_epilogue(int out_dtype, const float* O, const float* cnt, int64_t rows, int64_t cols,
+                               const uint16_t* wo, const float* bo, void* out, int cus, hipStream_t s);
+
 }  // namespace trimul

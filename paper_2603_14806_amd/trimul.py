@@ -1,8 +1,10 @@
-"""Thin Python binding of libtrimul.so (the C ABI in include/tri_mul.h).
+"""Thin Python binding of libtrimul.so (the C ABI in include/tri_mul.h and
+include/opm.h).
 
 Argument marshalling only: every step of the update runs in the library's HIP
 kernels.  PyTorch provides device memory and streams.  The functions keep the
-C names; TriMul is a small convenience wrapper that owns a handle.
+C names; TriMul and OuterProductMean are small convenience wrappers that own
+a handle.
 """
 import ctypes
 import os
@@ -37,6 +39,17 @@ class BlockView(ctypes.Structure):
                 ("k_index", _i32), ("k_count", _i32)]
 
 
+class OpmParams(ctypes.Structure):
+    """opm_params_t."""
+    _fields_ = [("d", _i32), ("c_z", _i32), ("out_dtype", _i32), ("w_o", _vp), ("b_o", _vp)]
+
+
+class OpmBlockView(ctypes.Structure):
+    """opm_block_view_t."""
+    _fields_ = [("n_total", _i64), ("s_total", _i64), ("row0", _i64), ("rows", _i64), ("col0", _i64),
+                ("cols", _i64), ("s0", _i64), ("slen", _i64), ("k_index", _i32), ("k_count", _i32)]
+
+
 class Grads(ctypes.Structure):
     """tri_mul_grads_t: device pointers of the float32 weight gradients."""
     _fields_ = [(name, _vp) for name in WEIGHT_FIELDS]
@@ -62,6 +75,14 @@ SIGNATURES = {
                                                  ctypes.c_size_t, _vp]),
     "tri_mul_incoming_backward": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.POINTER(Grads), _vp,
                                                  ctypes.c_size_t, _vp]),
+    "opm_init": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.POINTER(OpmParams), _vp]),
+    "opm_destroy": (ctypes.c_int, [_vp]),
+    "opm_accumulator_size": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "opm_workspace_size": (ctypes.c_int, [_vp, _i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "opm_block_accumulate": (ctypes.c_int, [_vp, ctypes.POINTER(OpmBlockView), _vp, _vp, _vp, _vp, _vp, _vp,
+                                            ctypes.c_size_t, _vp]),
+    "opm_forward_workspace_size": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "opm_forward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
 }
 
 _lib = None
@@ -338,3 +359,92 @@ def dense_to_result(C):
     Y = torch.zeros((c, N, J * 32), dtype=C.dtype, device=C.device)
     Y[:, :, :N] = C
     return Y.reshape(c, N, J, 32).permute(1, 2, 0, 3).contiguous().reshape(-1)
+
+
+# ---------------------------------------------------------------- outer product mean (include/opm.h)
+
+def opm_init(w_o, b_o=None, out_dtype="f32", d=32, c_z=128, stream=None):
+    """w_o: [c_z][d * d] bf16 device tensor; b_o: [c_z] bf16 device tensor or None."""
+    p = OpmParams(d, c_z, DTYPE_CODE[out_dtype], _ptr(w_o), _ptr(b_o))
+    h = _vp()
+    _check(lib().opm_init(ctypes.byref(h), ctypes.byref(p), _stream(stream)))
+    return h
+
+
+def opm_destroy(h):
+    _check(lib().opm_destroy(h))
+
+
+def opm_accumulator_size(h, rows, cols):
+    n = ctypes.c_size_t()
+    _check(lib().opm_accumulator_size(h, rows, cols, ctypes.byref(n)))
+    return n.value
+
+
+def opm_workspace_size(h, rows, cols, slen):
+    n = ctypes.c_size_t()
+    _check(lib().opm_workspace_size(h, rows, cols, slen, ctypes.byref(n)))
+    return n.value
+
+
+def opm_block_accumulate(h, view, a, b, mask, acc, out_tile, ws, ws_bytes, stream=None):
+    _check(lib().opm_block_accumulate(h, ctypes.byref(view), _ptr(a), _ptr(b), _ptr(mask), _ptr(acc),
+                                      _ptr(out_tile), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def opm_forward_workspace_size(h, S, N):
+    n = ctypes.c_size_t()
+    _check(lib().opm_forward_workspace_size(h, S, N, ctypes.byref(n)))
+    return n.value
+
+
+def opm_forward(h, a, b, mask, S, N, out, ws, ws_bytes, stream=None):
+    _check(lib().opm_forward(h, _ptr(a), _ptr(b), _ptr(mask), S, N, _ptr(out), _ptr(ws), ws_bytes,
+                             _stream(stream)))
+
+
+class OuterProductMean:
+    """Owns an opm handle and allocates outputs / workspaces with torch."""
+
+    def __init__(self, w_o, b_o=None, out_dtype="f32", device="cuda", stream=None):
+        self.out_dtype = out_dtype
+        self.device = torch.device(device)
+        self._w = w_o.to(self.device, torch.bfloat16).contiguous()
+        self._b = None if b_o is None else b_o.to(self.device, torch.bfloat16).contiguous()
+        self.h = opm_init(self._w, self._b, out_dtype, stream=stream)
+        torch.cuda.synchronize(self.device)
+
+    def close(self):
+        if self.h:
+            opm_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _out(self, rows, cols):
+        return torch.empty((rows, cols, 128), dtype=TORCH_DTYPE[DTYPE_CODE[self.out_dtype]], device=self.device)
+
+    def forward(self, a, b, mask=None, stream=None):
+        """a, b: [S][N][32] bf16 device tensors; mask: [S][N] uint8 or None -> out [N][N][128]."""
+        S, N = a.shape[0], a.shape[1]
+        if a.dtype != torch.bfloat16 or b.dtype != torch.bfloat16 or a.shape != b.shape or a.shape[2] != 32:
+            raise ValueError("a and b must be [S][N][32] bf16 tensors of the same shape")
+        if not (a.is_contiguous() and b.is_contiguous()):
+            raise ValueError("a and b must be contiguous")
+        out = self._out(N, N)
+        n = opm_forward_workspace_size(self.h, S, N)
+        ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+        opm_forward(self.h, a, b, mask, S, N, out, ws, n, stream)
+        return out
+
+    def accumulator(self, rows, cols):
+        return torch.empty(opm_accumulator_size(self.h, rows, cols) // 4, dtype=torch.float32, device=self.device)
+
+    def block_accumulate(self, view, a, b, mask, acc, out_tile=None, stream=None):
+        n = opm_workspace_size(self.h, view.rows, view.cols, view.slen)
+        ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+        opm_block_accumulate(self.h, view, a, b, mask, acc, out_tile, ws, n, stream)

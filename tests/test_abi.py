@@ -9,13 +9,16 @@ import pytest
 from paper_2603_14806_amd import trimul as T
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "tri_mul.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("tri_mul.h", "opm.h")]
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(tri_mul_[a-z_]+)\s*\(", text)))
+    names = set()
+    for header in HEADERS:
+        text = open(header).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b((?:tri_mul|opm)_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -42,6 +45,9 @@ def test_library_exports_every_declared_symbol(lib):
 def test_struct_layouts():
     assert ctypes.sizeof(T.Params) == 4 * 4 + 4 + 4 + 10 * 8   # 5 scalars, padding, 10 pointers
     assert ctypes.sizeof(T.BlockView) == 9 * 8 + 2 * 4
+    assert ctypes.sizeof(T.Grads) == 10 * 8
+    assert ctypes.sizeof(T.OpmParams) == 3 * 4 + 4 + 2 * 8      # 3 ints, padding, 2 pointers
+    assert ctypes.sizeof(T.OpmBlockView) == 8 * 8 + 2 * 4
 
 
 def test_null_arguments_rejected_without_gpu(lib):
@@ -56,6 +62,13 @@ def test_null_arguments_rejected_without_gpu(lib):
     assert lib.tri_mul_block_accumulate(None, None, 16, 16, 16, 0, 0, 0, None) == T.TRI_MUL_EINVAL
     assert lib.tri_mul_destroy(None) == T.TRI_MUL_OK
     assert T.last_error() == ""
+    assert lib.opm_init(ctypes.byref(h), None, None) == T.TRI_MUL_EINVAL
+    bad = T.OpmParams(16, 128, T.TRI_MUL_F32, 16, None)
+    assert lib.opm_init(ctypes.byref(h), ctypes.byref(bad), None) == T.TRI_MUL_EUNSUPPORTED
+    assert lib.opm_accumulator_size(None, 4, 4, ctypes.byref(n)) == T.TRI_MUL_EINVAL
+    assert lib.opm_block_accumulate(None, None, 16, 16, None, 16, 16, 16, 1 << 20, None) == T.TRI_MUL_EINVAL
+    assert lib.opm_forward(None, 16, 16, None, 4, 4, 16, 16, 1 << 20, None) == T.TRI_MUL_EINVAL
+    assert lib.opm_destroy(None) == T.TRI_MUL_OK
 
 
 def test_bad_params_rejected_without_gpu(lib):
