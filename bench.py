@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--N", type=int, default=4096)
     ap.add_argument("--cpu-sample", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the untimed extras (backward passes, outer product mean), e.g. for profiling runs "
+                         "that attribute the contraction kernel's statistics to the forward layer alone")
     ap.add_argument("--copy-calibration", type=float, default=0.0,
                     help="GiB moved by one plain device-to-device copy before the run (HBM counter calibration)")
     args = ap.parse_args()
@@ -180,39 +183,65 @@ def main():
     torch.cuda.synchronize()
     full_ms = f0.elapsed_time(f1) / 2
 
-    # the contraction backward (training), outside the timed region: both
-    # gradients of one direction, with C standing in for dC
-    dA, dB = torch.empty_like(C), torch.empty_like(C)
-    bws_n = T.tri_mul_contract_backward_workspace_size(h, N)
-    bws = torch.empty(bws_n, dtype=torch.uint8, device=dev)
-    T.tri_mul_contract_backward(h, C, A, B, N, dA, dB, bws, bws_n, stream)
-    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    b0.record(stream)
-    for _ in range(3):
+    bwd_ms = lbwd_ms = opm_ms = None
+    opm_flops = 2 * 4096 * (1024 * 32) ** 2
+    if not args.no_extras:
+        # the contraction backward (training), outside the timed region: both
+        # gradients of one direction, with C standing in for dC
+        dA, dB = torch.empty_like(C), torch.empty_like(C)
+        bws_n = T.tri_mul_contract_backward_workspace_size(h, N)
+        bws = torch.empty(bws_n, dtype=torch.uint8, device=dev)
         T.tri_mul_contract_backward(h, C, A, B, N, dA, dB, bws, bws_n, stream)
-    b1.record(stream)
-    torch.cuda.synchronize()
-    bwd_ms = b0.elapsed_time(b1) / 3
-    del dA, dB, bws
-    print(f"[bench] contraction backward {bwd_ms:.3f} ms", file=sys.stderr, flush=True)
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record(stream)
+        for _ in range(3):
+            T.tri_mul_contract_backward(h, C, A, B, N, dA, dB, bws, bws_n, stream)
+        b1.record(stream)
+        torch.cuda.synchronize()
+        bwd_ms = b0.elapsed_time(b1) / 3
+        del dA, dB, bws
+        print(f"[bench] contraction backward {bwd_ms:.3f} ms", file=sys.stderr, flush=True)
 
-    # the whole layer backward (outgoing), outside the timed region: dz and
-    # all weight gradients for an upstream gradient dout ~ N(0,1)
-    dout = synth.pair_tensor(N, dtype="f32", device=dev, name="dout")
-    dz = torch.empty_like(z)
-    grads = {k: torch.empty(v, dtype=torch.float32, device=dev) for k, v in T.WEIGHT_SHAPES.items()}
-    lws_n = T.tri_mul_backward_workspace_size(h, N)
-    lws = torch.empty(lws_n, dtype=torch.uint8, device=dev)
-    T.tri_mul_layer_backward(h, "outgoing", z, mask, N, dout, dz, grads, lws, lws_n, stream)
-    l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    l0.record(stream)
-    for _ in range(2):
+        # the whole layer backward (outgoing), outside the timed region: dz and
+        # all weight gradients for an upstream gradient dout ~ N(0,1)
+        dout = synth.pair_tensor(N, dtype="f32", device=dev, name="dout")
+        dz = torch.empty_like(z)
+        grads = {k: torch.empty(v, dtype=torch.float32, device=dev) for k, v in T.WEIGHT_SHAPES.items()}
+        lws_n = T.tri_mul_backward_workspace_size(h, N)
+        lws = torch.empty(lws_n, dtype=torch.uint8, device=dev)
         T.tri_mul_layer_backward(h, "outgoing", z, mask, N, dout, dz, grads, lws, lws_n, stream)
-    l1.record(stream)
-    torch.cuda.synchronize()
-    lbwd_ms = l0.elapsed_time(l1) / 2
-    del dout, dz, grads, lws
-    print(f"[bench] layer backward {lbwd_ms:.3f} ms", file=sys.stderr, flush=True)
+        l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        l0.record(stream)
+        for _ in range(2):
+            T.tri_mul_layer_backward(h, "outgoing", z, mask, N, dout, dz, grads, lws, lws_n, stream)
+        l1.record(stream)
+        torch.cuda.synchronize()
+        lbwd_ms = l0.elapsed_time(l1) / 2
+        del dout, dz, grads, lws
+        print(f"[bench] layer backward {lbwd_ms:.3f} ms", file=sys.stderr, flush=True)
+
+        # the outer product mean (a second op of the same ring archetype), outside
+        # the timed region: S = 4096 sequences, N = 1024 tokens, D = 32, c_z = 128
+        oS, oN = 4096, 1024
+        og = torch.Generator(device=dev).manual_seed(synth.SEED)
+        oa = torch.randn((oS, oN, 32), generator=og, device=dev).to(torch.bfloat16)
+        ob = torch.randn((oS, oN, 32), generator=og, device=dev).to(torch.bfloat16)
+        ow = (torch.randn((128, 1024), generator=og, device=dev) / 32).to(torch.bfloat16)
+        opm = T.OuterProductMean(ow, None, out_dtype="f32")
+        oout = torch.empty((oN, oN, 128), device=dev)
+        ows_n = T.opm_forward_workspace_size(opm.h, oS, oN)
+        ows = torch.empty(ows_n, dtype=torch.uint8, device=dev)
+        T.opm_forward(opm.h, oa, ob, None, oS, oN, oout, ows, ows_n, stream)
+        o0, o1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        o0.record(stream)
+        for _ in range(3):
+            T.opm_forward(opm.h, oa, ob, None, oS, oN, oout, ows, ows_n, stream)
+        o1.record(stream)
+        torch.cuda.synchronize()
+        opm_ms = o0.elapsed_time(o1) / 3
+        del oa, ob, oout, ows
+        opm.close()
+        print(f"[bench] outer product mean {opm_ms:.3f} ms", file=sys.stderr, flush=True)
 
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
@@ -240,11 +269,16 @@ def main():
             "epilogue": {"ms": round(k_ms["epilogue"], 4),
                          "GB_per_s": round(by["epilogue"] / (k_ms["epilogue"] * 1e-3) / 1e9, 1)},
         },
-        "backward_contract": {"ms": round(bwd_ms, 4),
+        "backward_contract": None if bwd_ms is None else {"ms": round(bwd_ms, 4),
                               "TFLOP_per_s": round(2 * fl["contract"] / (bwd_ms * 1e-3) / 1e12, 2),
                               "what": "dA = dC B and dB = dC^T A for all 128 channels (one direction), "
                                       "including the layout kernels; not part of ms_per_step"},
-        "backward_layer": {"ms": round(lbwd_ms, 4),
+        "outer_product_mean": None if opm_ms is None else {"ms": round(opm_ms, 4),
+                               "TFLOP_per_s": round(opm_flops / (opm_ms * 1e-3) / 1e12, 2),
+                               "what": "opm_forward, S=4096 sequences x N=1024 tokens, D=32, c_z=128, bf16 in, "
+                                       "fp32 out: 2*S*(N*D)^2 = 8.80 TFLOP contraction + counts + projection; "
+                                       "not part of ms_per_step"},
+        "backward_layer": None if lbwd_ms is None else {"ms": round(lbwd_ms, 4),
                            "what": "tri_mul_outgoing_backward: recompute of the forward projections and "
                                    "contraction, dz and all ten weight gradients; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
