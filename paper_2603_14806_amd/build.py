@@ -11,7 +11,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtrimul.so")
-SOURCES = ["api.hip", "project.hip", "contract.hip", "epilogue.hip", "backward.hip", "opm.hip"]
+SOURCES = ["api.hip", "project.hip", "contract.hip", "epilogue.hip", "backward.hip", "opm.hip", "triattn.hip"]
 ARCH = "gfx950"
 
 

@@ -10,6 +10,7 @@
 
 #include "tri_mul.h"
 #include "opm.h"
+#include "triattn.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -700,6 +701,69 @@ int opm_forward(opm_handle_t h, const void* a, const void* b, const uint8_t* mas
     const opm_block_view_t v{N, S, 0, N, 0, N, 0, S, 0, 1};
     return opm_block_accumulate(h, &v, a, b, mask, static_cast<float*>(ws), out, static_cast<char*>(ws) + accb,
                                 ws_bytes - accb, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- triangle attention core
+
+namespace {
+
+constexpr int64_t kTaMaxN = 16384;
+
+int ta_check(const tri_attn_view_t* v) {
+    if (!v) return fail(TRI_MUL_EINVAL, "null view");
+    if (v->rows < 1 || v->n < 1 || v->n > kTaMaxN) return fail(TRI_MUL_EINVAL, "rows = %lld, n = %lld outside [1, inf) x [1, %lld]", (long long)v->rows, (long long)v->n, (long long)kTaMaxN);
+    if (v->heads < 1 || v->heads > 16) return fail(TRI_MUL_EINVAL, "heads = %d outside [1, 16]", v->heads);
+    if (v->rows * (int64_t)v->heads * ((v->n + 127) / 128) > (int64_t)INT32_MAX) return fail(TRI_MUL_EUNSUPPORTED, "too many rows");
+    if (v->out_dtype != TRI_MUL_F32 && v->out_dtype != TRI_MUL_BF16) return fail(TRI_MUL_EINVAL, "bad out_dtype %d", v->out_dtype);
+    if (v->ld_bias < v->n || (v->ld_bias % 8)) return fail(TRI_MUL_EINVAL, "ld_bias = %lld must be >= n and a multiple of 8", (long long)v->ld_bias);
+    if (v->k0 < 0 || v->klen < 1 || v->k0 + v->klen > v->n || (v->k0 % 8)) return fail(TRI_MUL_EINVAL, "key range [%lld, +%lld) must lie in [0, n) with k0 %% 8 == 0", (long long)v->k0, (long long)v->klen);
+    if (v->k_count < 1 || v->k_index < 0 || v->k_index >= v->k_count) return fail(TRI_MUL_EINVAL, "bad k_index %d / k_count %d", v->k_index, v->k_count);
+    if (v->ld_bias > (int64_t)1 << 22) return fail(TRI_MUL_EUNSUPPORTED, "ld_bias = %lld above 2^22", (long long)v->ld_bias);
+    return TRI_MUL_OK;
+}
+
+size_t ta_sum_elems(const tri_attn_view_t* v) { return (size_t)v->rows * v->n * v->heads * 32; }
+size_t ta_ml_elems(const tri_attn_view_t* v) { return (size_t)v->rows * v->heads * v->n; }
+
+}  // namespace
+
+extern "C" {
+
+int tri_attn_state_size(const tri_attn_view_t* v, size_t* bytes) {
+    if (int rc = ta_check(v)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    *bytes = (ta_sum_elems(v) + 2 * ta_ml_elems(v)) * 4;
+    return ok();
+}
+
+int tri_attn_chunk(const tri_attn_view_t* v, const void* q, const void* k, const void* vv, const void* bias,
+                   const uint8_t* mask, float* state, void* out, void* stream) {
+    if (int rc = ta_check(v)) return rc;
+    if (!q || !k || !vv || !bias) return fail(TRI_MUL_EINVAL, "null q, k, v or bias pointer");
+    const bool last = v->k_index == v->k_count - 1;
+    const bool single = v->k_count == 1;
+    if (!single && !state) return fail(TRI_MUL_EINVAL, "a chunked attention needs a state");
+    if (last && !out) return fail(TRI_MUL_EINVAL, "the last step needs out");
+    if (!aligned16(q) || !aligned16(k) || !aligned16(vv) || !aligned16(bias) || (state && !aligned16(state)) ||
+        (out && !aligned16(out)))
+        return fail(TRI_MUL_EINVAL, "tensors must be 16-byte aligned");
+    float* stA = state;
+    float* stM = state ? state + ta_sum_elems(v) : nullptr;
+    float* stL = state ? stM + ta_ml_elems(v) : nullptr;
+    hipError_t e = trimul::launch_triattn(v->out_dtype == TRI_MUL_BF16, q, k, vv, bias, mask, v->rows, v->n,
+                                          v->heads, v->ld_bias, v->k0, v->k0 + v->klen, stA, stM, stL,
+                                          v->k_index > 0, last, out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "attention kernel launch");
+    return ok();
+}
+
+int tri_attn_forward(const void* q, const void* k, const void* v, const void* bias, const uint8_t* mask,
+                     int64_t rows, int64_t n, int32_t heads, int64_t ld_bias, int32_t out_dtype, void* out,
+                     void* stream) {
+    const tri_attn_view_t view{rows, n, heads, out_dtype, ld_bias, 0, n, 0, 1};
+    return tri_attn_chunk(&view, q, k, v, bias, mask, nullptr, out, stream);
 }
 
 }  // extern "C"

@@ -99,4 +99,13 @@ hipError_t launch_opm_pack(const void* a, const uint8_t* mask, int64_t n_total, 
 hipError_t launch_opm_epilogue(int out_dtype, const float* O, const float* cnt, int64_t rows, int64_t cols,
                                const uint16_t* wo, const float* bo, void* out, int cus, hipStream_t s);
 
+// Triangle attention core (triattn.hip): rows x heads x ceil(N / 128)
+// work-groups over keys [k0, kend); q, k, v [rows][N][H][32] bf16, bias
+// [H][N][ldb] bf16 (ldb % 8 == 0, k0 % 8 == 0), mask [N] or null.  State
+// (A [rows][N][H][32], M and L [rows][H][N], fp32) is read when load_state and
+// written unless finish; finish writes out [rows][N][H][32] (fp32 or bf16).
+hipError_t launch_triattn(int out_dtype, const void* q, const void* k, const void* v, const void* bias,
+                          const uint8_t* mask, int64_t rows, int64_t N, int H, int64_t ldb, int64_t k0, int64_t kend,
+                          float* stA, float* stM, float* stL, int load_state, int finish, void* out, hipStream_t s);
+
 }  // namespace trimul

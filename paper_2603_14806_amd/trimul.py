@@ -1,5 +1,5 @@
-"""Thin Python binding of libtrimul.so (the C ABI in include/tri_mul.h and
-include/opm.h).
+"""Thin Python binding of libtrimul.so (the C ABI in include/tri_mul.h,
+include/opm.h and include/triattn.h).
 
 Argument marshalling only: every step of the update runs in the library's HIP
 kernels.  PyTorch provides device memory and streams.  The functions keep the
@@ -50,6 +50,12 @@ class OpmBlockView(ctypes.Structure):
                 ("cols", _i64), ("s0", _i64), ("slen", _i64), ("k_index", _i32), ("k_count", _i32)]
 
 
+class TriAttnView(ctypes.Structure):
+    """tri_attn_view_t."""
+    _fields_ = [("rows", _i64), ("n", _i64), ("heads", _i32), ("out_dtype", _i32), ("ld_bias", _i64),
+                ("k0", _i64), ("klen", _i64), ("k_index", _i32), ("k_count", _i32)]
+
+
 class Grads(ctypes.Structure):
     """tri_mul_grads_t: device pointers of the float32 weight gradients."""
     _fields_ = [(name, _vp) for name in WEIGHT_FIELDS]
@@ -83,6 +89,10 @@ SIGNATURES = {
                                             ctypes.c_size_t, _vp]),
     "opm_forward_workspace_size": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
     "opm_forward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_attn_state_size": (ctypes.c_int, [ctypes.POINTER(TriAttnView), ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_attn_chunk": (ctypes.c_int, [ctypes.POINTER(TriAttnView), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "tri_attn_forward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, ctypes.c_int32, _i64, ctypes.c_int32,
+                                        _vp, _vp]),
 }
 
 _lib = None
@@ -448,3 +458,36 @@ class OuterProductMean:
         n = opm_workspace_size(self.h, view.rows, view.cols, view.slen)
         ws = torch.empty(n, dtype=torch.uint8, device=self.device)
         opm_block_accumulate(self.h, view, a, b, mask, acc, out_tile, ws, n, stream)
+
+
+# ---------------------------------------------------------------- triangle attention core (include/triattn.h)
+
+def tri_attn_state_size(view):
+    n = ctypes.c_size_t()
+    _check(lib().tri_attn_state_size(ctypes.byref(view), ctypes.byref(n)))
+    return n.value
+
+
+def tri_attn_chunk(view, q, k, v, bias, mask, state, out, stream=None):
+    _check(lib().tri_attn_chunk(ctypes.byref(view), _ptr(q), _ptr(k), _ptr(v), _ptr(bias), _ptr(mask), _ptr(state),
+                                _ptr(out), _stream(stream)))
+
+
+def tri_attn_forward(q, k, v, bias, mask, rows, n, heads, ld_bias, out_dtype, out, stream=None):
+    _check(lib().tri_attn_forward(_ptr(q), _ptr(k), _ptr(v), _ptr(bias), _ptr(mask), rows, n, heads, ld_bias,
+                                  DTYPE_CODE.get(out_dtype, out_dtype), _ptr(out), _stream(stream)))
+
+
+def triangle_attention(q, k, v, bias, mask=None, out_dtype="f32", stream=None):
+    """q, k, v: [rows][n][heads][32] bf16 device tensors; bias: [heads][n][ld] bf16 with ld % 8 == 0
+    (a view [heads][n][n] of such a tensor is fine); mask: [n] uint8 or None -> out [rows][n][heads][32]."""
+    rows, n, heads, d = q.shape
+    if d != 32 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must be [rows][n][heads][32] of one shape")
+    if not (q.is_contiguous() and k.is_contiguous() and v.is_contiguous()):
+        raise ValueError("q, k and v must be contiguous")
+    if bias.dim() != 3 or bias.shape[0] != heads or bias.shape[1] != n or bias.stride(2) != 1 or bias.stride(0) != n * bias.stride(1):
+        raise ValueError("bias must be [heads][n][ld] with unit column stride")
+    out = torch.empty((rows, n, heads, 32), dtype=TORCH_DTYPE[DTYPE_CODE[out_dtype]], device=q.device)
+    tri_attn_forward(q, k, v, bias, mask, rows, n, heads, bias.stride(1), out_dtype, out, stream)
+    return out

@@ -9,7 +9,7 @@ import pytest
 from paper_2603_14806_amd import trimul as T
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADERS = [os.path.join(ROOT, "include", h) for h in ("tri_mul.h", "opm.h")]
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("tri_mul.h", "opm.h", "triattn.h")]
 
 
 def declared_functions():
@@ -17,7 +17,7 @@ def declared_functions():
     for header in HEADERS:
         text = open(header).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-        names |= set(re.findall(r"\b((?:tri_mul|opm)_[a-z_]+)\s*\(", text))
+        names |= set(re.findall(r"\b((?:tri_mul|opm|tri_attn)_[a-z_]+)\s*\(", text))
     return sorted(names)
 
 
@@ -48,6 +48,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(T.Grads) == 10 * 8
     assert ctypes.sizeof(T.OpmParams) == 3 * 4 + 4 + 2 * 8      # 3 ints, padding, 2 pointers
     assert ctypes.sizeof(T.OpmBlockView) == 8 * 8 + 2 * 4
+    assert ctypes.sizeof(T.TriAttnView) == 2 * 8 + 2 * 4 + 3 * 8 + 2 * 4
 
 
 def test_null_arguments_rejected_without_gpu(lib):
@@ -69,6 +70,13 @@ def test_null_arguments_rejected_without_gpu(lib):
     assert lib.opm_block_accumulate(None, None, 16, 16, None, 16, 16, 16, 1 << 20, None) == T.TRI_MUL_EINVAL
     assert lib.opm_forward(None, 16, 16, None, 4, 4, 16, 16, 1 << 20, None) == T.TRI_MUL_EINVAL
     assert lib.opm_destroy(None) == T.TRI_MUL_OK
+    assert lib.tri_attn_chunk(None, 16, 16, 16, 16, None, None, 16, None) == T.TRI_MUL_EINVAL
+    bad = T.TriAttnView(1, 64, 4, T.TRI_MUL_F32, 60, 0, 64, 0, 1)        # ld_bias not a multiple of 8
+    assert lib.tri_attn_state_size(ctypes.byref(bad), ctypes.byref(n)) == T.TRI_MUL_EINVAL
+    good = T.TriAttnView(2, 64, 4, T.TRI_MUL_F32, 64, 0, 64, 0, 1)
+    assert lib.tri_attn_state_size(ctypes.byref(good), ctypes.byref(n)) == T.TRI_MUL_OK
+    assert n.value == (2 * 64 * 4 * 32 + 2 * 2 * 4 * 64) * 4
+    assert lib.tri_attn_forward(None, 16, 16, 16, None, 1, 64, 4, 64, 0, 16, None) == T.TRI_MUL_EINVAL
 
 
 def test_bad_params_rejected_without_gpu(lib):
