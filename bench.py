@@ -183,7 +183,8 @@ def main():
     torch.cuda.synchronize()
     full_ms = f0.elapsed_time(f1) / 2
 
-    bwd_ms = lbwd_ms = opm_ms = None
+    bwd_ms = lbwd_ms = opm_ms = ta_ms = None
+    ta_scores = 2048 * 4 * 2048 * 2048
     opm_flops = 2 * 4096 * (1024 * 32) ** 2
     if not args.no_extras:
         # the contraction backward (training), outside the timed region: both
@@ -243,6 +244,24 @@ def main():
         opm.close()
         print(f"[bench] outer product mean {opm_ms:.3f} ms", file=sys.stderr, flush=True)
 
+        # the triangle attention core (rows = n = 2048, 4 heads of 32), outside the timed region
+        tn, tH = 2048, 4
+        tq = torch.randn((tn, tn, tH, 32), generator=og, device=dev).to(torch.bfloat16)
+        tk = torch.randn((tn, tn, tH, 32), generator=og, device=dev).to(torch.bfloat16)
+        tv = torch.randn((tn, tn, tH, 32), generator=og, device=dev).to(torch.bfloat16)
+        tb = torch.randn((tH, tn, tn), generator=og, device=dev).to(torch.bfloat16)
+        tout = torch.empty((tn, tn, tH, 32), device=dev)
+        T.tri_attn_forward(tq, tk, tv, tb, None, tn, tn, tH, tn, "f32", tout, stream)
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        for _ in range(3):
+            T.tri_attn_forward(tq, tk, tv, tb, None, tn, tn, tH, tn, "f32", tout, stream)
+        a1.record(stream)
+        torch.cuda.synchronize()
+        ta_ms = a0.elapsed_time(a1) / 3
+        del tq, tk, tv, tb, tout
+        print(f"[bench] triangle attention {ta_ms:.3f} ms", file=sys.stderr, flush=True)
+
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
     layer_flops = 2 * fl["total"]
@@ -278,6 +297,12 @@ def main():
                                "what": "opm_forward, S=4096 sequences x N=1024 tokens, D=32, c_z=128, bf16 in, "
                                        "fp32 out: 2*S*(N*D)^2 = 8.80 TFLOP contraction + counts + projection; "
                                        "not part of ms_per_step"},
+        "triangle_attention": None if ta_ms is None else {"ms": round(ta_ms, 4),
+                               "G_scores_per_s": round(ta_scores / (ta_ms * 1e-3) / 1e9, 1),
+                               "TFLOP_per_s": round(4 * 32 * ta_scores / (ta_ms * 1e-3) / 1e12, 2),
+                               "what": "tri_attn_forward, rows = n = 2048, 4 heads of 32, bf16 in, fp32 out: "
+                                       "rows*H*n^2 = 34.4e9 scores (QK and PV 128 flop each); not part of "
+                                       "ms_per_step"},
         "backward_layer": None if lbwd_ms is None else {"ms": round(lbwd_ms, 4),
                            "what": "tri_mul_outgoing_backward: recompute of the forward projections and "
                                    "contraction, dz and all ten weight gradients; not part of ms_per_step"},
