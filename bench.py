@@ -78,6 +78,71 @@ def cpu_baseline(N, sample):
             "sample_seconds": round(t3 - t0, 2)}
 
 
+def gpu_state():
+    """Current clocks and socket power of GPU 0 as rocm-smi reports them (a
+    child process; None if the tool is missing or fails)."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "-d", "0", "-c", "-P", "--json"], capture_output=True, text=True, timeout=30)
+        card = next(iter(json.loads(r.stdout).values()))
+        keep = ("sclk", "mclk", "fclk", "socclk", "power")
+        return {k: v for k, v in card.items() if any(w in k.lower() for w in keep)}
+    except Exception:
+        return None
+
+
+def cpu_oracle_extras(timings):
+    """The fp64 oracle on bounded samples of the untimed extras' workloads,
+    extrapolated to the full workloads (each sample a few seconds):
+    - layer backward: the whole update backward at N = 128 (outgoing, all
+      pairs), scaled by the ratio of the flop counts of N = 4096 and N = 128;
+    - outer product mean: a 128 x 128 block of pairs over all S = 4096
+      sequences of the S = 4096, N = 1024 problem, scaled by the pair count;
+    - triangle attention: four rows i (all 2048 queries, 4 heads) of the
+      rows = n = 2048 problem, scaled by the row count."""
+    import numpy as np
+
+    import oracle
+    from paper_2603_14806_amd import perf, synth
+    rng = np.random.default_rng(synth.SEED)
+    out = {}
+    if "backward_layer" in timings:
+        n = 128
+        W = {k: oracle.f64(v) for k, v in synth.weights(dtype="bf16").items()}
+        z, dout = rng.standard_normal((n, n, 128)), rng.standard_normal((n, n, 128))
+        t0 = time.perf_counter()
+        oracle.tri_mul_backward(z, np.ones(n), W, "outgoing", dout)
+        t = time.perf_counter() - t0
+        ms = 1e3 * t * perf.flops(4096)["total"] / perf.flops(n)["total"]
+        out["backward_layer"] = {"ms_extrapolated": round(ms, 1), "sample_seconds": round(t, 2),
+                                 "sample": f"tri_mul_backward (fp64) of the whole update at N={n}, scaled by the "
+                                           f"flop ratio of N=4096 to N={n}"}
+    if "outer_product_mean" in timings:
+        S, n, blk = 4096, 1024, 128
+        # the block's tokens only: the tile [0, blk) x [0, blk) reads nothing else
+        a, b = rng.standard_normal((S, blk, 32)), rng.standard_normal((S, blk, 32))
+        w = rng.standard_normal((128, 1024)) / 32
+        t0 = time.perf_counter()
+        oracle.outer_product_mean_tile(a, b, None, w, np.zeros(128), 0, blk, 0, blk)
+        t = time.perf_counter() - t0
+        out["outer_product_mean"] = {"ms_extrapolated": round(1e3 * t * (n / blk) ** 2, 1),
+                                     "sample_seconds": round(t, 2),
+                                     "sample": f"outer_product_mean_tile (fp64), a {blk}x{blk} block of pairs over "
+                                               f"all S={S} sequences, scaled by the pair count ({(n // blk) ** 2}x)"}
+        del a, b
+    if "triangle_attention" in timings:
+        n, H, rows = 2048, 4, 4
+        q, k, v = (rng.standard_normal((rows, n, H, 32)) for _ in range(3))
+        bias = rng.standard_normal((H, n, n))
+        t0 = time.perf_counter()
+        oracle.triangle_attention(q, k, v, bias, None)
+        t = time.perf_counter() - t0
+        out["triangle_attention"] = {"ms_extrapolated": round(1e3 * t * n / rows, 1), "sample_seconds": round(t, 2),
+                                     "sample": f"triangle_attention (fp64) of {rows} rows (all {n} queries, {H} "
+                                               f"heads), scaled by the row count ({n // rows}x)"}
+    return out
+
+
 def measured_traffic():
     """HBM-side bytes per K2 launch from the committed rocprofv3 counter runs
     (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known size),
@@ -153,6 +218,7 @@ def main():
             if e: e[3].record(stream)
             if e: evs.append(e)
 
+    state_before = gpu_state()
     for _ in range(args.warmup):
         step(None)
     torch.cuda.synchronize()
@@ -170,6 +236,9 @@ def main():
     ms_step = t0.elapsed_time(t1) / args.steps
     k_ms = {name: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / len(evs)
             for i, name in enumerate(("project", "contract", "epilogue"))}
+    per_step = sorted(evs[2 * i][0].elapsed_time(evs[2 * i + 1][3]) for i in range(args.steps))
+    step_median = per_step[len(per_step) // 2] if len(per_step) % 2 else \
+        0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
     print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/layer; per kernel {k_ms}", file=sys.stderr, flush=True)
 
     # the full entry points (one call = the same three launches), outside the timed region
@@ -264,6 +333,13 @@ def main():
 
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
+    bw = perf.backward_layer_work(N)
+    opm_proj_flops = 2 * 1024 * 1024 * 1024 * 128
+
+    def mfma_roof(flop, ms):
+        a = flop / (ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": round(a, 2), "peak": perf.PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(a / perf.PEAK_BF16_TFLOPS, 4)}
     layer_flops = 2 * fl["total"]
     contract_tflops = fl["contract"] / (k_ms["contract"] * 1e-3) / 1e12
     result = {
@@ -279,6 +355,8 @@ def main():
                    "N": N, "c_z": 128, "c": 128, "parallelism": "none (one GPU)"},
         "ms_per_layer": round(ms_step, 4),
         "ms_per_layer_full_calls": round(full_ms, 4),
+        "ms_per_layer_median": round(step_median, 4), "ms_per_layer_min": round(per_step[0], 4),
+        "gpu_state": {"before": state_before, "after": gpu_state()},
         "contract_pct_of_bf16_peak": round(100 * contract_tflops / perf.PEAK_BF16_TFLOPS, 2),
         "kernels": {
             "project": {"ms": round(k_ms["project"], 4),
@@ -290,20 +368,33 @@ def main():
         },
         "backward_contract": None if bwd_ms is None else {"ms": round(bwd_ms, 4),
                               "TFLOP_per_s": round(2 * fl["contract"] / (bwd_ms * 1e-3) / 1e12, 2),
+                              "roofline": mfma_roof(2 * fl["contract"], bwd_ms),
                               "what": "dA = dC B and dB = dC^T A for all 128 channels (one direction), "
                                       "including the layout kernels; not part of ms_per_step"},
         "outer_product_mean": None if opm_ms is None else {"ms": round(opm_ms, 4),
                                "TFLOP_per_s": round(opm_flops / (opm_ms * 1e-3) / 1e12, 2),
+                               "roofline": mfma_roof(opm_flops + opm_proj_flops, opm_ms),
                                "what": "opm_forward, S=4096 sequences x N=1024 tokens, D=32, c_z=128, bf16 in, "
                                        "fp32 out: 2*S*(N*D)^2 = 8.80 TFLOP contraction + counts + projection; "
                                        "not part of ms_per_step"},
         "triangle_attention": None if ta_ms is None else {"ms": round(ta_ms, 4),
                                "G_scores_per_s": round(ta_scores / (ta_ms * 1e-3) / 1e9, 1),
                                "TFLOP_per_s": round(4 * 32 * ta_scores / (ta_ms * 1e-3) / 1e12, 2),
+                               "roofline": {"bound": "alu", "achieved": round(ta_scores / (ta_ms * 1e-3) / 1e12, 3),
+                                            "peak": round(perf.PEAK_LANE_OPS / perf.TRIATTN_SLOTS / 1e12, 3),
+                                            "unit": "T scores/s",
+                                            "frac": round(ta_scores / (ta_ms * 1e-3) / (perf.PEAK_LANE_OPS
+                                                                                         / perf.TRIATTN_SLOTS), 4),
+                                            "peak_basis": perf.TRIATTN_BASIS},
                                "what": "tri_attn_forward, rows = n = 2048, 4 heads of 32, bf16 in, fp32 out: "
                                        "rows*H*n^2 = 34.4e9 scores (QK and PV 128 flop each); not part of "
                                        "ms_per_step"},
         "backward_layer": None if lbwd_ms is None else {"ms": round(lbwd_ms, 4),
+                           "roofline": {"bound": "mfma + hbm", "floor_ms": round(bw["floor_ms"], 3),
+                                        "frac": round(bw["floor_ms"] / lbwd_ms, 4),
+                                        "mfma_flops": bw["mfma_flops"], "hbm_bytes": bw["hbm_bytes"],
+                                        "basis": "floor = three N^3 bf16 products at MFMA peak + the per-pair "
+                                                 "kernels' algorithmic bytes at HBM peak; frac = floor / ms"},
                            "what": "tri_mul_outgoing_backward: recompute of the forward projections and "
                                    "contraction, dz and all ten weight gradients; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
@@ -318,6 +409,13 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(N, args.cpu_sample)
+        extras = {k: result[k] for k in ("backward_layer", "outer_product_mean", "triangle_attention")
+                  if result[k] is not None}
+        if extras:
+            print("[bench] timing the CPU oracle on samples of the extras", file=sys.stderr, flush=True)
+            for k, v in cpu_oracle_extras(extras).items():
+                v["gpu_speedup"] = round(v["ms_extrapolated"] / extras[k]["ms"], 1)
+                extras[k]["cpu_oracle"] = v
     print(json.dumps(result), flush=True)
 
 
