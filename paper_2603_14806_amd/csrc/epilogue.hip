@@ -320,15 +320,20 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
 //
 // The full update's epilogue (C in the pair-blocked layout, z [N][N][c_z]).
 // Same work split and arithmetic as k3_epilogue_mfma, but C, z and the mask
-// bytes of the next unit arrive by direct-to-LDS loads into a 2-stage ring
-// while the current unit is computed, and the bf16 activations are written
-// back into the stage they were read from.  Every wave issues 7 loads and a
-// fixed number of range-checked buffer stores per unit (tail pairs are
-// dropped by the range check), so the vmcnt waits are constants.
+// bytes of later units arrive by direct-to-LDS loads into a ring (three
+// stages, two units ahead, with fp32 output; two with bf16 output, whose
+// staging takes the room) while the current unit is computed, and the bf16
+// activations are written back into the stage they were read from.  Masked
+// pairs get y = LN_out(C) = 0, so their outputs are exactly 0 without a
+// mask in the gating.  Every wave issues 7 loads and a fixed number of
+// range-checked buffer stores per unit (tail pairs are dropped by the range
+// check), so the vmcnt waits are constants.
 //
 // Stage layout (bytes):
 //   [0, 16384)      C of the unit, [128 channels][32 pairs] fp32: chunk q
-//                   (pairs 4q .. 4q + 3) of channel row c at slot q ^ (c & 7);
+//                   (pairs 4q .. 4q + 3) of channel row c at slot q ^ h(c),
+//                   h(c) = (c + c / 16) % 8, so that the 8 lanes reading
+//                   channels 16 l + k (l = 0..7) of one pair hit 8 slots;
 //                   afterwards y_hi [0, 8192) and y_lo [8192, 16384)
 //   [16384, 24576)  z of the unit, [32 pairs][128] bf16: chunk q of pair row p
 //                   at slot q ^ (p & 1); afterwards x_hi
@@ -343,21 +348,34 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
                       int N, int nunits, TO* __restrict__ out, const bf16_t* __restrict__ wepi,
                       const float* __restrict__ lnin_w, const float* __restrict__ lnin_b,
                       const float* __restrict__ lnout_w, const float* __restrict__ lnout_b, float eps) {
-    __shared__ __attribute__((aligned(16))) char ring[2 * kRSt];
+    // fp32 output leaves straight from the accumulators (a register holds 32
+    // consecutive channels of one pair per half-wave: two whole 128-byte
+    // rows per store), which frees the output staging for a third ring
+    // stage; bf16 output is staged as [p][d] for 16-byte stores.
+    constexpr bool kDirect = sizeof(TO) == 4;
+    constexpr int kStages = kDirect ? 3 : 2;
+    __shared__ __attribute__((aligned(16))) char ring[kStages * kRSt];
     __shared__ __attribute__((aligned(16))) float prm[4][128];               // LN gains and biases
-    __shared__ __attribute__((aligned(16))) float os[kP3 * kOsRow];          // outputs as [p][d]
+    __shared__ __attribute__((aligned(16))) float os[kDirect ? 4 : kP3 * kOsRow];   // outputs as [p][d]
     const int t = threadIdx.x, lane = t & 63;
     const int w = __builtin_amdgcn_readfirstlane(t >> 6);
     const int lp = t >> 3, lq = t & 7;     // LayerNorms: pair lp, 8 lanes per pair
     const int G = gridDim.x;
     const int first = (G & 7) == 0 ? (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3) : blockIdx.x;
     const int nchunk = (N + kP3 - 1) / kP3;
-    constexpr int kStores = (int)(kP3 * kCz * sizeof(TO)) / (4 * 1024);   // 16-byte stores per lane per unit
+    constexpr int kStores = (int)(kP3 * kCz * sizeof(TO)) / (4 * 1024);   // staged path: 16-byte stores per lane
+    constexpr int kS = kDirect ? 16 : kStores;                             // stores per lane per unit
 
-    // Ring fill.  C: load k of wave w covers channel rows 8 (4 w + k) .. + 7,
-    // lane -> row + lane / 8, slot lane % 8.  z and mask as in the projection.
+    // Ring fill.  C: load k of wave w covers channel rows c = 8 (4 w + k) .. + 7,
+    // lane -> row c + lane / 8 at slot lane % 8, which holds chunk
+    // (lane % 8) ^ h(c) (h(c) = (lane / 8 + 2 w + k / 2) % 8 for these rows).
+    // z and mask as in the projection.
     const uint32_t ring_base = lds_addr(ring);
-    const uint32_t cvo = (uint32_t)((lane >> 3) * 128 + (((lane & 7) ^ (lane >> 3)) << 4)) + (uint32_t)w * 4096;
+    uint32_t cvo[2];
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
+        cvo[kh] = (uint32_t)((lane >> 3) * 128 + (((lane & 7) ^ (((lane >> 3) + 2 * w + kh) & 7)) << 4)) +
+                  (uint32_t)w * 4096;
     const int drow = w * 8 + (lane >> 4);
     const uint32_t dchunk = (uint32_t)(((lane & 15) ^ (drow & 1)) << 4);
     const uint32_t dv0 = (uint32_t)drow * kYRow + dchunk, dv1 = (uint32_t)(drow + 4) * kYRow + dchunk;
@@ -374,7 +392,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         const uint32_t st = ring_base + (uint32_t)(stage * kRSt);
         const v4i_t rc = buffer_desc(C + result_off(nchunk, kCh, 0, i, j0), valid ? (uint32_t)kRC : 0u);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) lds_load16(rc, cvo + k * 1024, 0, st + w * 4096 + k * 1024);
+        for (int k = 0; k < 4; ++k) lds_load16(rc, cvo[k >> 1] + k * 1024, 0, st + w * 4096 + k * 1024);
         const v4i_t rz = buffer_desc(z + ((int64_t)i * N + j0) * kCz, (uint32_t)np * kYRow);
         lds_load16(rz, dv0, 0, st + kRC + w * 2048);
         lds_load16(rz, dv1, 0, st + kRC + w * 2048 + 1024);
@@ -383,6 +401,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         lds_load4(rm, mo, 0, st + kRC + kRZ + w * 256);
     };
     issue(first, 0);
+    if (kStages == 3) issue(first + G, 1);
 
     bf16x8_t wo[8], wg[8];
 #pragma unroll
@@ -398,23 +417,34 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         prm[3][t] = lnin_b[t];
     }
 
+    int stage = 0;
     for (int it = 0, u = first; u < nunits; ++it, u += G) {
-        // Wait for this unit's loads: issued after them are only the stores
-        // of the previous unit.
-        if (it == 0) wait_vmcnt_pinned<0>();
-        else wait_vmcnt_pinned<kStores>();
+        // Wait for this unit's loads.  Issued after them: two stages, the
+        // stores of the previous unit; three stages, the next unit's loads
+        // (7) and the stores of the units in between.
+        if (kStages == 2) {
+            if (it == 0) wait_vmcnt_pinned<0>();
+            else wait_vmcnt_pinned<kS>();
+        } else {
+            if (it == 0) wait_vmcnt_pinned<7>();
+            else if (it == 1) wait_vmcnt_pinned<7 + kS>();
+            else wait_vmcnt_pinned<kS + 7 + kS>();
+        }
         __syncthreads();
-        issue(u + G, (it + 1) & 1);   // into the stage of the previous unit
-        char* st = ring + (it & 1) * kRSt;
+        // into the stage of the previous unit
+        issue(u + (kStages - 1) * G, stage == 0 ? kStages - 1 : stage - 1);
+        char* st = ring + stage * kRSt;
+        stage = stage == kStages - 1 ? 0 : stage + 1;
 
-        // LN_out over the 128 hidden channels of pair lp (lane lq holds
-        // c = lq + 8 k) and LN_in over the 128 pair channels (lane lq holds
-        // 16 lq .. 16 lq + 15), both from the stage.
+        // LN_out over the 128 hidden channels of pair lp and LN_in over the
+        // 128 pair channels, both from the stage; lane lq holds channels
+        // 16 lq .. 16 lq + 15 of each.
         float v[16];
         {
-            const char* crow = st + (((lp >> 2) ^ lq) << 4) + (lp & 3) * 4;
+            const char* crow = st + (16 * lq) * 128 + (lp & 3) * 4;
 #pragma unroll
-            for (int k = 0; k < 16; ++k) v[k] = *reinterpret_cast<const float*>(crow + (lq + 8 * k) * 128);
+            for (int k = 0; k < 16; ++k)
+                v[k] = *reinterpret_cast<const float*>(crow + k * 128 + (((lp >> 2) ^ ((k + lq) & 7)) << 4));
         }
         float zv[16];
         {
@@ -431,7 +461,9 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         const uint8_t* ms = reinterpret_cast<const uint8_t*>(st + kRC + kRZ + w * 256);
         int ui, uj0;
         decode(u, ui, uj0);
-        const uint32_t mrow = ms[32 + (ui & 3)];
+        // Masked pairs (and tail pairs, whose staged mask is zero) get y = 0:
+        // W_o y, and so the output, is then exactly 0 (no bias).
+        const uint32_t keep = (ms[lp] & ms[32 + (ui & 3)]) ? 0xffffffffu : 0u;
         __syncthreads();   // every thread has read its C and z; the stage becomes y_hi, y_lo, x_hi
 
         {
@@ -448,15 +480,20 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
             }
             q2 = sum_lanes8(q2);
             const float rs = rsqrtf(q2 * (1.0f / kCh) + eps);
+            uint32_t yh[8], yl[8];
 #pragma unroll
-            for (int k = 0; k < 16; ++k) {
-                const int c = lq + 8 * k;
-                const float y = v[k] * rs * prm[0][c] + prm[1][c];
-                const bf16_t h = f2bf(y);
-                const uint32_t o = yoff(lp, c >> 3) + 2 * (c & 7);
-                *reinterpret_cast<bf16_t*>(st + o) = h;
-                *reinterpret_cast<bf16_t*>(st + 8192 + o) = f2bf(y - bf2f(h));
+            for (int k = 0; k < 8; ++k) {
+                const int c = 16 * lq + 2 * k;
+                const float y0 = v[2 * k] * rs * prm[0][c] + prm[1][c];
+                const float y1 = v[2 * k + 1] * rs * prm[0][c + 1] + prm[1][c + 1];
+                const uint32_t h = pack_bf16x2(y0, y1);
+                yh[k] = h & keep;
+                yl[k] = pack_bf16x2(y0 - __uint_as_float(h << 16), y1 - __uint_as_float(h & 0xffff0000u)) & keep;
             }
+            *reinterpret_cast<uint4*>(st + yoff(lp, 2 * lq)) = make_uint4(yh[0], yh[1], yh[2], yh[3]);
+            *reinterpret_cast<uint4*>(st + yoff(lp, 2 * lq + 1)) = make_uint4(yh[4], yh[5], yh[6], yh[7]);
+            *reinterpret_cast<uint4*>(st + 8192 + yoff(lp, 2 * lq)) = make_uint4(yl[0], yl[1], yl[2], yl[3]);
+            *reinterpret_cast<uint4*>(st + 8192 + yoff(lp, 2 * lq + 1)) = make_uint4(yl[4], yl[5], yl[6], yl[7]);
         }
         {
             float s1 = 0.f;
@@ -499,37 +536,42 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         }
 
         // Lane holds output channel 32 w + (lane & 31); register r holds pair
-        // 8 (r / 4) + 4 (lane / 32) + r % 4.  The staged mask is zero past N,
-        // so tail pairs come out as zeros (and are not stored).
+        // 8 (r / 4) + 4 (lane / 32) + r % 4 (tail pairs come out as zeros and
+        // are not stored).
         const int d = w * 32 + (lane & 31);
+        const int np = min(kP3, N - uj0);
+        if constexpr (kDirect) {
+            // bytes past the row's last pair fall outside the descriptor
+            const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * N + uj0) * kCz,
+                                                        (uint32_t)(np * kCz * 4));
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int p = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sigmoidf_(ag[r]) * ay[r]), ro,
+                                                      (p * kCz + d) * 4, 0, 0);
+            }
+            continue;
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int p = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            const uint32_t keep = (ms[p] & mrow) ? 0xffffffffu : 0u;
-            os[p * kOsRow + d] = __uint_as_float(__float_as_uint(sigmoidf_(ag[r]) * ay[r]) & keep);
+            os[p * kOsRow + d] = sigmoidf_(ag[r]) * ay[r];
         }
         __syncthreads();
 
-        // The unit's [32 pairs][128] block is contiguous in out: store k of
-        // the work-group covers its bytes [4096 k, 4096 k + 4096), 16 per
+        // bf16: the unit's [32 pairs][128] block is contiguous in out: store k
+        // of the work-group covers its bytes [4096 k, 4096 k + 4096), 16 per
         // thread; bytes past the row's last pair fall outside the descriptor.
-        const int np = min(kP3, N - uj0);
         const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * N + uj0) * kCz,
                                                     (uint32_t)(np * kCz * (int)sizeof(TO)));
 #pragma unroll
         for (int k = 0; k < kStores; ++k) {
             const uint32_t off = (uint32_t)(k * 4096 + t * 16);
-            uint4 pk;
-            if (sizeof(TO) == 4) {
-                const int p = off / 512, d4 = (off % 512) / 4;
-                pk = __builtin_bit_cast(uint4, *reinterpret_cast<const float4*>(&os[p * kOsRow + d4]));
-            } else {
-                const int p = off / 256, d8 = (off % 256) / 2;
-                const float4 f0 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8]);
-                const float4 f1 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8 + 4]);
-                pk = make_uint4(pack_bf16x2(f0.x, f0.y), pack_bf16x2(f0.z, f0.w), pack_bf16x2(f1.x, f1.y),
-                                pack_bf16x2(f1.z, f1.w));
-            }
+            const int p = off / 256, d8 = (off % 256) / 2;
+            const float4 f0 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8]);
+            const float4 f1 = *reinterpret_cast<const float4*>(&os[p * kOsRow + d8 + 4]);
+            const uint4 pk = make_uint4(pack_bf16x2(f0.x, f0.y), pack_bf16x2(f0.z, f0.w), pack_bf16x2(f1.x, f1.y),
+                                        pack_bf16x2(f1.z, f1.w));
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i_t, pk), ro, off, 0, 0);
         }
     }
