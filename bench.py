@@ -399,7 +399,7 @@ def main():
                                    "contraction, dz and all ten weight gradients; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(), "kernel": "k2_contract_w8",
+                     "traffic": measured_traffic(), "kernel": "k2_contract_ws",
                      "per_launch": f"2*N^3*c = {fl['contract']:.4e} flop (128 channels of one {N}^3 product)"},
         "cpu_baseline": None,
     }

@@ -275,21 +275,25 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
     wait_vmcnt<0>();   // the zero-size loads of the last steps land before the work-group ends
 }
 
-// ------------------------------------------------------ bf16 MFMA, 8 waves
+// ------------------------------------------- bf16 MFMA, 8 + 4 specialised waves
 //
 // The same contraction for blocked operands without a k-mask (the full
-// update), with two waves per SIMD: 8 waves per work-group, each owning a
-// 64 x 128 sub-tile (2 x 4 MFMA blocks, 128 accumulator registers), and each
-// issuing 4 of the 32 direct-to-LDS loads of a k-step.  A wave that stalls
-// while issuing a load leaves the matrix core to the other wave on its SIMD.
-// LDS ring, swizzle, tile order and step schedule as in k2_contract_mfma.
-__global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2)))
-void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
+// update), with the loads taken off the MFMA waves: 12 waves per work-group
+// (three per SIMD); waves 0-7 each own a 64 x 128 sub-tile (2 x 4 MFMA
+// blocks, 128 accumulator registers) and issue only LDS reads and MFMAs,
+// waves 8-11 issue all 32 direct-to-LDS loads of a k-step (64 A rows and
+// 64 B rows each) and wait for them, so a load that stalls in a busy L2
+// never stops a matrix-core stream.  The one barrier per k-step hands a
+// filled stage from the loaders to the MFMA waves and a consumed stage back.
+// LDS ring (5 stages), swizzle, tile order and step schedule as in
+// k2_contract_mfma.
+__global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_per_eu(3, 3)))
+void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
                     int N, int K, int tiles_m, int tiles_n, int total, int accumulate) {
-    constexpr int BM = 256, MI = 2;              // per wave: MI x 4 blocks of 32 x 32
+    constexpr int BM = 256, MI = 2;
     constexpr int A_ST = BM * ROWB, ST_BYTES = A_ST + B_ST;
     constexpr int STAGES = kLdsBytes / ST_BYTES;  // 5
-    constexpr int LOADS = 4;                     // direct-to-LDS loads per wave per step
+    constexpr int LOADS = 8;                     // direct-to-LDS loads per loader wave per step
     __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
 
     const int G = gridDim.x, wg = blockIdx.x;
@@ -301,9 +305,7 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
     const int nchan = total / tiles;
 
     const int t = threadIdx.x, lane = t & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // 0 .. 7
-    const int wm = wave >> 1, wn = wave & 1;                   // rows 64 wm, columns 128 wn
-    const int rl = lane & 31, hi = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // 0 .. 11
 
     auto decode = [&](int it, int& ch, int& m0, int& n0) {
         const int L = it * G + perm;
@@ -317,36 +319,63 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         m0 = (first_m + in_g % gsz) * BM;
         n0 = (in_g / gsz) * BN;
     };
-
-    // Wave w loads rows 32 w .. 32 w + 31 of the A block and of the B block
-    // (two 16-row loads each); lane i -> row (i >> 2), slot (i & 3), chunk
-    // (i & 3) ^ ((row >> 2) & 3).
-    const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
-    const uint32_t vo = (uint32_t)(((wave * 32 + (lane >> 2)) * BK + lkc * 8) * 2);
     const uint32_t lds_base = lds_addr(smem);
-    int l_it = 0, l_kt = 0, l_stage = 0;
-    v4i_t ra, rb;
-    const v4i_t rnone = buffer_desc(A, 0u);
-    auto load_tile = [&]() {
-        int ch, m0, n0;
-        decode(l_it, ch, m0, n0);
-        ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK), (uint32_t)(nk * BM * BK * 2));
-        rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK), (uint32_t)(nk * BN * BK * 2));
-    };
-    auto issue_part = [&](int j, bool live) {   // j: 0, 1 A halves, 2, 3 B halves
-        const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
-        const uint32_t koff = (uint32_t)l_kt * (BM * BK * 2) + (uint32_t)(j & 1) * (16 * BK * 2);
-        const uint32_t dst = st + (j >> 1) * A_ST + (uint32_t)(wave * 32 + 16 * (j & 1)) * ROWB;
-        lds_load16(live ? ((j >> 1) ? rb : ra) : rnone, vo, koff, dst);
-    };
-    auto advance = [&]() {
-        l_stage = l_stage == STAGES - 1 ? 0 : l_stage + 1;
-        if (++l_kt == nk) {
-            l_kt = 0;
-            if (++l_it < my_tiles) load_tile();
-        }
-    };
 
+    if (wave >= 8) {
+        // Loader wave lw: rows 64 lw .. 64 lw + 63 of the A and B blocks as four
+        // 16-row loads each; lane i -> row (i >> 2) of a group, slot (i & 3),
+        // chunk (i & 3) ^ ((row >> 2) & 3).
+        const int lw = wave - 8;
+        const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
+        const uint32_t vo = (uint32_t)(((lw * 64 + (lane >> 2)) * BK + lkc * 8) * 2);
+        int l_it = 0, l_kt = 0, l_stage = 0;
+        v4i_t ra = buffer_desc(A, 0u), rb = buffer_desc(B, 0u);
+        const v4i_t rnone = buffer_desc(A, 0u);
+        auto load_tile = [&]() {
+            int ch, m0, n0;
+            decode(l_it, ch, m0, n0);
+            ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK), (uint32_t)(nk * BM * BK * 2));
+            rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK), (uint32_t)(nk * BN * BK * 2));
+        };
+        auto issue_step = [&](bool live) {
+            const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
+#pragma unroll
+            for (int j = 0; j < LOADS; ++j) {   // j < 4: A groups, j >= 4: B groups
+                const uint32_t koff = (uint32_t)l_kt * (BM * BK * 2) + (uint32_t)(j & 3) * (16 * BK * 2);
+                const uint32_t dst = st + (j >> 2) * A_ST + (uint32_t)(lw * 64 + 16 * (j & 3)) * ROWB;
+                lds_load16(live ? ((j >> 2) ? rb : ra) : rnone, vo, koff, dst);
+            }
+        };
+        auto advance = [&]() {
+            l_stage = l_stage == STAGES - 1 ? 0 : l_stage + 1;
+            if (++l_kt == nk) {
+                l_kt = 0;
+                if (++l_it < my_tiles) load_tile();
+            }
+        };
+        if (my_tiles > 0) load_tile();
+        const int pro = min(STAGES - 1, steps);
+        for (int s0 = 0; s0 < pro; ++s0) {
+            issue_step(true);
+            advance();
+        }
+        for (int s = 0; s < steps; ++s) {
+            const int ahead = min(STAGES - 2, steps - 1 - s);   // later steps already in flight
+            if (ahead >= 3) wait_vmcnt<3 * LOADS>();
+            else if (ahead == 2) wait_vmcnt<2 * LOADS>();
+            else if (ahead == 1) wait_vmcnt<LOADS>();
+            else wait_vmcnt<0>();
+            __syncthreads();
+            const bool fetch = s + STAGES - 1 < steps;
+            issue_step(fetch);
+            if (fetch) advance();
+        }
+        wait_vmcnt<0>();
+        return;
+    }
+
+    const int wm = wave >> 1, wn = wave & 1;                   // rows 64 wm, columns 128 wn
+    const int rl = lane & 31, hi = lane >> 5;
     const int q = (rl >> 2) & 3;
     uint32_t rdA[2], rdB[2];
 #pragma unroll
@@ -355,16 +384,7 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         rdA[sub] = (wm * 64 + rl) * ROWB + x;
         rdB[sub] = A_ST + (wn * 128 + rl) * ROWB + x;
     }
-
-    if (my_tiles > 0) load_tile();
-    const int pro = min(STAGES - 1, steps);
-    for (int s0 = 0; s0 < pro; ++s0) {
-#pragma unroll
-        for (int j = 0; j < LOADS; ++j) issue_part(j, true);
-        advance();
-    }
     int c_stage = 0;
-
     for (int it = 0; it < my_tiles; ++it) {
         f32x16_t acc[MI][4];
 #pragma unroll
@@ -375,18 +395,10 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
         for (int kt = 0; kt < nk; ++kt) {
-            const int s = it * nk + kt;
-            const int ahead = min(STAGES - 2, steps - 1 - s);   // later steps already in flight
-            if (ahead >= 3) wait_vmcnt<3 * LOADS>();
-            else if (ahead == 2) wait_vmcnt<2 * LOADS>();
-            else if (ahead == 1) wait_vmcnt<LOADS>();
-            else wait_vmcnt<0>();
             __syncthreads();
-            const bool fetch = s + STAGES - 1 < steps;
             const char* st = smem + c_stage * ST_BYTES;
             c_stage = c_stage == STAGES - 1 ? 0 : c_stage + 1;
             const bool tail = (kt == nk - 1) && (K % BK) != 0;
-
             auto mask_tail = [&](int sub, bf16x8_t (&af)[MI], bf16x8_t (&bfr)[4]) {
                 const int kk = kt * BK + sub * 16 + hi * 8;
                 uint32_t keep[4];
@@ -406,26 +418,21 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                     bfr[j] = __builtin_bit_cast(bf16x8_t, v);
                 }
             };
-
             bf16x8_t a0[MI], b0[4], a1[MI], b1[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) b0[j] = *reinterpret_cast<const bf16x8_t*>(st + rdB[0] + j * 32 * ROWB);
 #pragma unroll
             for (int i = 0; i < MI; ++i) a0[i] = *reinterpret_cast<const bf16x8_t*>(st + rdA[0] + i * 32 * ROWB);
             if (tail) mask_tail(0, a0, b0);
-            // Sub-step 0: after MFMA x, fetch part x / 2 (even x) or the
-            // operand read x / 2 of sub-step 1 (odd x) -- 4 parts, 6 reads.
 #pragma unroll
             for (int x = 0; x < 4 * MI; ++x) {
                 const int i = x >> 2, j = x & 3;
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
-                if (x < 2 * LOADS && (x & 1) == 0) issue_part(x >> 1, fetch);
-                const int y = x - 2;   // reads start after the first two MFMAs
+                const int y = x - 2;   // reads of sub-step 1 start after the first two MFMAs
                 if (y >= 0 && y < 4) b1[y] = *reinterpret_cast<const bf16x8_t*>(st + rdB[1] + y * 32 * ROWB);
                 else if (y >= 4 && y < 4 + MI)
                     a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
             }
-            if (fetch) advance();
             if (tail) mask_tail(1, a1, b1);
 #pragma unroll
             for (int x = 0; x < 4 * MI; ++x) {
@@ -440,7 +447,7 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         const bool full = m0 + BM <= M && n0 + BN <= N;
         const int64_t jblocks = (N + kResJ - 1) / kResJ;
         float* Cb = C + result_off(jblocks, nchan, ch, row0, col0);
-        const int64_t row_step = jblocks * nchan * kResJ;   // elements between rows
+        const int64_t row_step = jblocks * nchan * kResJ;
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -456,7 +463,6 @@ void k2_contract_w8(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                     }
                 }
     }
-    wait_vmcnt<0>();
 }
 
 // ---------------------------------------------------------------- fp32 VALU
@@ -554,7 +560,7 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
         else K2_LAUNCH(true, false);
     } else {
         if (blocked)
-            hipLaunchKernelGGL(k2_contract_w8, dim3(grid), dim3(512), 0, s, a, b, C, (int)M, (int)N, (int)K, tm, tn,
+            hipLaunchKernelGGL(k2_contract_ws, dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K, tm, tn,
                                total, accumulate);
         else K2_LAUNCH(false, false);
     }

@@ -7,7 +7,7 @@
 // is one NT product with M = rows * D, N = cols * D, K = slen, and the pair
 // counts n_ij = sum_s m_si m_sj another with M = rows, N = cols (0/1
 // operands: exact in fp32 up to 2^24); both run on the contraction kernel
-// (k2_contract_w8), accumulating over the steps of a tile.
+// (k2_contract_ws), accumulating over the steps of a tile.
 #include "common.h"
 #include "kernels.h"
 
