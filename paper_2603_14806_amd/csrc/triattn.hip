@@ -33,7 +33,7 @@ struct TaChunk {                 // one chunk's global loads (registers)
 };
 
 template <typename TO>
-__global__ __launch_bounds__(256) void k_triattn(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(3, 3))) void k_triattn(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                                                  const bf16_t* __restrict__ v, const bf16_t* __restrict__ bias,
                                                  const uint8_t* __restrict__ mask, int N, int H, int64_t ldb, int k0,
                                                  int kend,
@@ -147,34 +147,45 @@ __global__ __launch_bounds__(256) void k_triattn(const bf16_t* __restrict__ q, c
                 s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s2], s[b], 0, 0, 0);
             }
         }
-        // scale, bias, mask; chunk maximum
+        // scale, bias, mask (only a chunk that can hold absent keys: a mask
+        // is given, or the chunk runs past the range); chunk maximum
         float cm = -INFINITY;
         const int qrow = 32 * w + ql;
+        auto scores = [&](bool masked) {
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+            for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int a = 0; a < 4; ++a) {
-                const int kk = 32 * b + 8 * a + 4 * hi;
-                const uint2 bw = *reinterpret_cast<const uint2*>(&bt[buf][qrow * kBRow + kk]);
-                const float bv[4] = {__uint_as_float(bw.x << 16), __uint_as_float(bw.x & 0xffff0000u),
-                                     __uint_as_float(bw.y << 16), __uint_as_float(bw.y & 0xffff0000u)};
+                for (int a = 0; a < 4; ++a) {
+                    const int kk = 32 * b + 8 * a + 4 * hi;
+                    const uint2 bw = *reinterpret_cast<const uint2*>(&bt[buf][qrow * kBRow + kk]);
+                    const float bv[4] = {__uint_as_float(bw.x << 16), __uint_as_float(bw.x & 0xffff0000u),
+                                         __uint_as_float(bw.y << 16), __uint_as_float(bw.y & 0xffff0000u)};
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float x = s[b][4 * a + e] * scale + bv[e] + mb[buf][kk + e];
-                    s[b][4 * a + e] = x;
-                    cm = fmaxf(cm, x);
+                    for (int e = 0; e < 4; ++e) {
+                        float x = s[b][4 * a + e] * scale + bv[e];
+                        if (masked) x += mb[buf][kk + e];
+                        s[b][4 * a + e] = x;
+                        cm = fmaxf(cm, x);
+                    }
                 }
-            }
+        };
+        if (mask != nullptr || k0 + (c + 1) * kKc > kend) scores(true);
+        else scores(false);
         cm = fmaxf(cm, xor32(cm));
         const float Mn = fmaxf(M, cm);
         const bool live = Mn != -INFINITY;                    // some present key so far
         const float alpha = (live && M != -INFINITY) ? __expf(M - Mn) : 0.f;
+        // p = exp(x - Mn) = exp2(x log2 e - Mn log2 e), one FMA and one
+        // v_exp_f32; with no present key yet the shift is 0 and every x is
+        // -inf, so p = 0 without a select
+        constexpr float kLog2e = 1.4426950408889634f;
+        const float nsh = live ? -Mn * kLog2e : 0.f;
         float ps = 0.f;
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const float p = live ? __expf(s[b][r] - Mn) : 0.f;
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r], kLog2e, nsh));
                 s[b][r] = p;
                 ps += p;
             }
