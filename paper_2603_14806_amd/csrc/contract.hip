@@ -360,9 +360,10 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             advance();
         }
         for (int s = 0; s < steps; ++s) {
-            const int ahead = min(STAGES - 2, steps - 1 - s);   // later steps already in flight
-            if (ahead >= 3) wait_vmcnt<3 * LOADS>();
-            else if (ahead == 2) wait_vmcnt<2 * LOADS>();
+            // steps s and s + 1 complete at barrier s (the MFMA waves read
+            // step s + 1's first operands during step s); later ones in flight
+            const int ahead = min(STAGES - 3, steps - 2 - s);
+            if (ahead >= 2) wait_vmcnt<2 * LOADS>();
             else if (ahead == 1) wait_vmcnt<LOADS>();
             else wait_vmcnt<0>();
             __syncthreads();
@@ -386,6 +387,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
     }
     int c_stage = 0;
     for (int it = 0; it < my_tiles; ++it) {
+        bf16x8_t a0[MI], b0[4];  // sub-step 0 operands, read one step ahead within a tile
         f32x16_t acc[MI][4];
 #pragma unroll
         for (int i = 0; i < MI; ++i)
@@ -394,10 +396,20 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+        // a tile's first step: barrier, then its sub-step 0 operands (nothing
+        // is read ahead across the C stores)
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            b0[j] = *reinterpret_cast<const bf16x8_t*>(smem + c_stage * ST_BYTES + rdB[0] + j * 32 * ROWB);
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+            a0[i] = *reinterpret_cast<const bf16x8_t*>(smem + c_stage * ST_BYTES + rdA[0] + i * 32 * ROWB);
         for (int kt = 0; kt < nk; ++kt) {
-            __syncthreads();
+            if (kt > 0) __syncthreads();
             const char* st = smem + c_stage * ST_BYTES;
             c_stage = c_stage == STAGES - 1 ? 0 : c_stage + 1;
+            const char* stn = smem + c_stage * ST_BYTES;             // the next step
             const bool tail = (kt == nk - 1) && (K % BK) != 0;
             auto mask_tail = [&](int sub, bf16x8_t (&af)[MI], bf16x8_t (&bfr)[4]) {
                 const int kk = kt * BK + sub * 16 + hi * 8;
@@ -418,11 +430,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                     bfr[j] = __builtin_bit_cast(bf16x8_t, v);
                 }
             };
-            bf16x8_t a0[MI], b0[4], a1[MI], b1[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) b0[j] = *reinterpret_cast<const bf16x8_t*>(st + rdB[0] + j * 32 * ROWB);
-#pragma unroll
-            for (int i = 0; i < MI; ++i) a0[i] = *reinterpret_cast<const bf16x8_t*>(st + rdA[0] + i * 32 * ROWB);
+            bf16x8_t a1[MI], b1[4];
             if (tail) mask_tail(0, a0, b0);
 #pragma unroll
             for (int x = 0; x < 4 * MI; ++x) {
@@ -434,10 +442,18 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                     a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
             }
             if (tail) mask_tail(1, a1, b1);
+            // sub-step 1; after MFMA x, the operand read x - 2 of the next
+            // step's sub-step 0 (its stage is complete since this step's
+            // barrier; after a tile's last step the values go unused)
 #pragma unroll
             for (int x = 0; x < 4 * MI; ++x) {
                 const int i = x >> 2, j = x & 3;
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+                const int y = x - 2;
+                if (y >= 0 && y < 4)
+                    b0[y] = *reinterpret_cast<const bf16x8_t*>(stn + rdB[0] + y * 32 * ROWB);
+                else if (y >= 4 && y < 4 + MI)
+                    a0[y - 4] = *reinterpret_cast<const bf16x8_t*>(stn + rdA[0] + (y - 4) * 32 * ROWB);
             }
         }
 
