@@ -103,7 +103,9 @@ __global__ __launch_bounds__(256) void k1_project_valu(
 //
 // Precision: the LayerNormed input x (fp32) is split into x_hi = bf16(x) and
 // x_lo = bf16(x - x_hi); with exact bf16 weights W x_hi + W x_lo carries ~16
-// mantissa bits, so a and b see one bf16 rounding only (their store).
+// mantissa bits for the projections W_a x and W_b x, so their main error is
+// one bf16 rounding (the store of a and b).  The gates take x_hi alone, as
+// in the epilogue: the logistic's slope (<= 1/4) scales that rounding down.
 constexpr int kP1 = 32;                 // pairs per line
 constexpr int kXRow = kCz * 2;          // bytes of one bf16 row of 128 channels (256)
 constexpr int kZSt = kP1 * kXRow;       // z bytes of one line (8 KB)
@@ -246,7 +248,9 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         *reinterpret_cast<uint4*>(xs[1] + xoff(lp, 2 * lq + 1)) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
         __syncthreads();
 
-        // [W_a; W_ga; W_b; W_gb](32 channels) x [x_hi + x_lo](32 pairs)
+        // [W_a; W_b](32 channels) x [x_hi + x_lo](32 pairs); the gates
+        // [W_ga; W_gb] x x_hi (the logistic's slope <= 1/4 damps x_hi's
+        // rounding below that of the bf16 store of a and b)
         f32x16_t acc[4];
 #pragma unroll
         for (int ob = 0; ob < 4; ++ob)
@@ -260,7 +264,7 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
 #pragma unroll
             for (int ob = 0; ob < 4; ++ob) {
                 acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xh, acc[ob], 0, 0, 0);
-                acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xl, acc[ob], 0, 0, 0);
+                if ((ob & 1) == 0) acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xl, acc[ob], 0, 0, 0);
             }
         }
 

@@ -76,6 +76,20 @@ def test_project_matches_oracle(dtype, N, direction):
     A, B = layer.project(z.cuda(), mask.cuda(), direction)
     torch.cuda.synchronize()
     rA, rB = oracle.projected_panels(z, mask, W, direction)
+    # Per-element error terms of the bf16 path, from the oracle's pieces: the
+    # values W x run on x_hi + x_lo (residual <= 2^-16 |x|), the gates on
+    # x_hi alone (|x - x_hi| <= 2^-8 |x|, and the logistic is 1/4-Lipschitz),
+    # then one bf16 rounding of the product (<= 2^-8 relative).
+    x = oracle.layer_norm(oracle.f64(z), W["ln_in_w"], W["ln_in_b"])
+    ax = np.abs(x)
+    m = oracle.pair_mask(mask)[..., None]
+    lay = (2, 0, 1) if direction == "outgoing" else (2, 1, 0)
+    extra = {}
+    for name, wv, wg in (("A", "w_a", "w_ga"), ("B", "w_b", "w_gb")):
+        p = np.abs(oracle.linear(x, W[wv]))
+        gate = 2.0 ** -10 * (ax @ np.abs(oracle.f64(W[wg])).T)
+        vals = 2.0 ** -16 * (ax @ np.abs(oracle.f64(W[wv])).T)
+        extra[name] = (m * (gate * p + vals)).transpose(lay)
     for got, ref, name in ((A, rA, "A"), (B, rB, "B")):
         got = host(T.panel_to_dense(got, N))
         if dtype == "f32":
@@ -83,10 +97,11 @@ def test_project_matches_oracle(dtype, N, direction):
             say(f"  {name}: max_abs={mx:.2e} rel_fro={rel:.2e}")
             assert rel <= 1e-6
         else:
-            # one rounding to bf16 (half an ulp, <= 2^-8 relative) plus fp32 error
-            bound = 2.0 ** -8 * np.abs(ref) + 1e-5
+            bound = 2.0 ** -8 * np.abs(ref) + (1 + 2.0 ** -8) * extra[name] + 1e-5
             bad = np.abs(got - ref) > bound
-            assert not bad.any(), f"{name}: {bad.sum()} elements beyond one bf16 rounding"
+            mx, rel = errors(got, ref)
+            say(f"  {name}: max_abs={mx:.2e} rel_fro={rel:.2e}")
+            assert not bad.any(), f"{name}: {bad.sum()} elements beyond the bound"
         # masked pairs are exact zeros
         m = oracle.pair_mask(mask)
         mm = m if direction == "outgoing" else m.T
