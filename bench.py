@@ -175,7 +175,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU path; "
-              "the per-device tile of a sharded run is measured by the block benchmark.", file=sys.stderr)
+              "one device's tile of a sharded run is timed by the ring_tile field (tile (7,7) of an 8x8 grid at N=30000).", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -252,7 +252,7 @@ def main():
     torch.cuda.synchronize()
     full_ms = f0.elapsed_time(f1) / 2
 
-    bwd_ms = lbwd_ms = opm_ms = ta_ms = None
+    bwd_ms = lbwd_ms = opm_ms = ta_ms = tile_ms = None
     ta_scores = 2048 * 4 * 2048 * 2048
     opm_flops = 2 * 4096 * (1024 * 32) ** 2
     if not args.no_extras:
@@ -331,10 +331,46 @@ def main():
         del tq, tk, tv, tb, tout
         print(f"[bench] triangle attention {ta_ms:.3f} ms", file=sys.stderr, flush=True)
 
+        # one device's share of the paper's 2-D ring, outside the timed region:
+        # tile (7, 7) of an 8 x 8 grid at N = 30000 (3750 x 3750 pairs, the last
+        # 300 tokens padded), 8 ring steps of block_accumulate over 3750-token
+        # k-panels, the last running the epilogue.  Two panel pairs alternate
+        # (3.6 GB each, far beyond any cache, so every step streams its panels
+        # from HBM as 8 distinct ones would).
+        bn, bg = 30000, 8
+        bb = bn // bg
+        brow, bld = 7 * bb, (bb + 7) // 8 * 8
+        bmask = synth.token_mask(bn, 300, device=dev)
+        bpa = [synth.pair_tensor(0, dtype="bf16", device=dev, name="a_panel", seed=synth.SEED + p,
+                                 shape=(128, bb, bld)) for p in range(2)]
+        bpb = [synth.pair_tensor(0, dtype="bf16", device=dev, name="b_panel", seed=synth.SEED + p,
+                                 shape=(128, bb, bld)) for p in range(2)]
+        bz = synth.pair_tensor(0, dtype="bf16", device=dev, name="z_tile", shape=(bb, bb, 128))
+        bacc = torch.empty((128, bb, bb), dtype=torch.float32, device=dev)
+        bout = torch.empty((bb, bb, 128), dtype=torch.float32, device=dev)
+
+        def ring_tile():
+            for p in range(bg):
+                v = T.BlockView(bn, brow, brow, bb, bb, p * bb, bb, bld, bld, p, bg)
+                layer.block_accumulate(v, bpa[p & 1], bpb[p & 1], bacc, bmask, bz, bout, stream)
+
+        ring_tile()
+        t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0e.record(stream)
+        for _ in range(2):
+            ring_tile()
+        t1e.record(stream)
+        torch.cuda.synchronize()
+        tile_ms = t0e.elapsed_time(t1e) / 2
+        del bpa, bpb, bz, bacc, bout
+        torch.cuda.empty_cache()
+        print(f"[bench] ring tile {tile_ms:.3f} ms", file=sys.stderr, flush=True)
+
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
     bw = perf.backward_layer_work(N)
     opm_proj_flops = 2 * 1024 * 1024 * 1024 * 128
+    tile_flops = 2.0 * 3750 * 3750 * 30000 * 128
 
     def mfma_roof(flop, ms):
         a = flop / (ms * 1e-3) / 1e12
@@ -389,6 +425,12 @@ def main():
                                "what": "tri_attn_forward, rows = n = 2048, 4 heads of 32, bf16 in, fp32 out: "
                                        "rows*H*n^2 = 34.4e9 scores (QK and PV 128 flop each); not part of "
                                        "ms_per_step"},
+        "ring_tile": None if tile_ms is None else {"ms": round(tile_ms, 4),
+                      "TFLOP_per_s": round(tile_flops / (tile_ms * 1e-3) / 1e12, 2),
+                      "roofline": mfma_roof(tile_flops, tile_ms),
+                      "what": "tile (7,7) of an 8x8 grid at N=30000: 8 block_accumulate ring steps (3750x3750 "
+                              "outputs, 3750-token k-panels, 128 channels; 108.0 TFLOP contraction) with the "
+                              "epilogue on the last step; fp32 accumulator and output; not part of ms_per_step"},
         "backward_layer": None if lbwd_ms is None else {"ms": round(lbwd_ms, 4),
                            "roofline": {"bound": "mfma + hbm", "floor_ms": round(bw["floor_ms"], 3),
                                         "frac": round(bw["floor_ms"] / lbwd_ms, 4),

@@ -277,19 +277,30 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
 
 // ------------------------------------------- bf16 MFMA, 8 + 4 specialised waves
 //
-// The same contraction for blocked operands without a k-mask (the full
-// update), with the loads taken off the MFMA waves: 12 waves per work-group
-// (three per SIMD); waves 0-7 each own a 64 x 128 sub-tile (2 x 4 MFMA
-// blocks, 128 accumulator registers) and issue only LDS reads and MFMAs,
-// waves 8-11 issue all 32 direct-to-LDS loads of a k-step (64 A rows and
-// 64 B rows each) and wait for them, so a load that stalls in a busy L2
-// never stops a matrix-core stream.  The one barrier per k-step hands a
-// filled stage from the loaders to the MFMA waves and a consumed stage back.
-// LDS ring (5 stages), swizzle, tile order and step schedule as in
-// k2_contract_mfma.
+// The contraction with the loads taken off the MFMA waves: 12 waves per
+// work-group (three per SIMD); waves 0-7 each own a 64 x 128 sub-tile (2 x 4
+// MFMA blocks, 128 accumulator registers) and issue only LDS reads and
+// MFMAs, waves 8-11 issue all 32 direct-to-LDS loads of a k-step (64 A rows
+// and 64 B rows each) and wait for them, so a load that stalls in a busy L2
+// never stops a matrix-core stream.  The one barrier per k-step hands
+// filled stages from the loaders to the MFMA waves and a consumed one back;
+// at barrier s steps s and s + 1 are complete, and the MFMA waves read step
+// s + 1's first operands behind step s's last MFMAs.
+//
+// Operands either blocked (the full update: one tile's k-step is a
+// contiguous 16 KB block, C in the pair-blocked result layout) or row-major
+// (a device tile's caller panels [ch][rows][ld] and accumulator
+// [ch][rows][ldc]).  k values that must not reach the sums -- masked by the
+// optional k-mask, or past K in the last step (row-major padding columns
+// hold arbitrary data) -- are zeroed in LDS by the loader waves, in the rows
+// each loaded, before the barrier that publishes the stage: only steps that
+// hold such k pay, and the MFMA waves never mask.
+// LDS ring (5 stages), swizzle and tile order as in k2_contract_mfma.
+template <bool BLOCKED, bool KMASK>
 __global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_per_eu(3, 3)))
 void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
-                    int N, int K, int tiles_m, int tiles_n, int total, int accumulate) {
+                    int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB, int64_t sC, int tiles_m,
+                    int tiles_n, int total, int accumulate, const uint8_t* __restrict__ kmask) {
     constexpr int BM = 256, MI = 2;
     constexpr int A_ST = BM * ROWB, ST_BYTES = A_ST + B_ST;
     constexpr int STAGES = kLdsBytes / ST_BYTES;  // 5
@@ -327,23 +338,36 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         // chunk (i & 3) ^ ((row >> 2) & 3).
         const int lw = wave - 8;
         const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
-        const uint32_t vo = (uint32_t)(((lw * 64 + (lane >> 2)) * BK + lkc * 8) * 2);
+        const int rsa = BLOCKED ? BK : lda, rsb = BLOCKED ? BK : ldb;   // elements between rows
+        const uint32_t va = (uint32_t)(((lw * 64 + (lane >> 2)) * rsa + lkc * 8) * 2);
+        const uint32_t vb = (uint32_t)(((lw * 64 + (lane >> 2)) * rsb + lkc * 8) * 2);
+        const uint32_t a_j = (uint32_t)(16 * rsa * 2), b_j = (uint32_t)(16 * rsb * 2);   // bytes per 16 rows
+        const uint32_t a_k = BLOCKED ? (uint32_t)(BM * BK * 2) : (uint32_t)ROWB;       // bytes per k-step
+        const uint32_t b_k = BLOCKED ? (uint32_t)(BN * BK * 2) : (uint32_t)ROWB;
         int l_it = 0, l_kt = 0, l_stage = 0;
         v4i_t ra = buffer_desc(A, 0u), rb = buffer_desc(B, 0u);
         const v4i_t rnone = buffer_desc(A, 0u);
         auto load_tile = [&]() {
             int ch, m0, n0;
             decode(l_it, ch, m0, n0);
-            ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK), (uint32_t)(nk * BM * BK * 2));
-            rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK), (uint32_t)(nk * BN * BK * 2));
+            if (BLOCKED) {
+                ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK),
+                                 (uint32_t)(nk * BM * BK * 2));
+                rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK),
+                                 (uint32_t)(nk * BN * BK * 2));
+            } else {   // rows past M (N) fall outside the descriptor and load as zero
+                ra = buffer_desc(A + ch * sA + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 2));
+                rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
+            }
         };
         auto issue_step = [&](bool live) {
             const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
 #pragma unroll
             for (int j = 0; j < LOADS; ++j) {   // j < 4: A groups, j >= 4: B groups
-                const uint32_t koff = (uint32_t)l_kt * (BM * BK * 2) + (uint32_t)(j & 3) * (16 * BK * 2);
-                const uint32_t dst = st + (j >> 2) * A_ST + (uint32_t)(lw * 64 + 16 * (j & 3)) * ROWB;
-                lds_load16(live ? ((j >> 2) ? rb : ra) : rnone, vo, koff, dst);
+                const bool isb = j >= 4;
+                const uint32_t soff = (uint32_t)(j & 3) * (isb ? b_j : a_j) + (uint32_t)l_kt * (isb ? b_k : a_k);
+                const uint32_t dst = st + (isb ? A_ST : 0) + (uint32_t)(lw * 64 + 16 * (j & 3)) * ROWB;
+                lds_load16(live ? (isb ? rb : ra) : rnone, isb ? vb : va, soff, dst);
             }
         };
         auto advance = [&]() {
@@ -353,6 +377,53 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 if (++l_it < my_tiles) load_tile();
             }
         };
+        // Dead-k bitmaps of the k-mask (bit k of step kt set if k-mask byte
+        // kt * 32 + k is 0), computed once before any load is in flight:
+        // lane l holds steps l + 64 j in mwords[j] (K <= 65536 -> j < 32).
+        uint32_t mwords[KMASK ? 32 : 1];
+        if (KMASK) {
+            const uint32_t* km4 = reinterpret_cast<const uint32_t*>(kmask);   // staged: 0/1 bytes, padded to 32
+#pragma unroll
+            for (int j = 0; j < 32; ++j) {
+                const int kt = lane + 64 * j;
+                uint32_t wbits = 0;
+                if (kt < nk) {
+#pragma unroll
+                    for (int d = 0; d < 8; ++d) {
+                        const uint32_t m4 = km4[kt * 8 + d];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (((m4 >> (8 * e)) & 0xffu) == 0) wbits |= 1u << (4 * d + e);
+                    }
+                }
+                mwords[j] = wbits;
+            }
+        }
+        // Zero, in this wave's 64 A and 64 B rows of step u's stage, the k
+        // values of the step that are masked out or past K.
+        auto zero_dead = [&](int u) {
+            const int kt = u % nk;
+            const int kv = K - kt * BK;                   // valid k of the step
+            uint32_t bits = kv >= BK ? 0u : ~((1u << kv) - 1u);
+            if (KMASK) {
+                uint32_t wsel = 0;
+#pragma unroll
+                for (int j = 0; j < 32; ++j) wsel = (j == (kt >> 6)) ? mwords[j] : wsel;
+                bits |= (uint32_t)__builtin_amdgcn_readlane((int)wsel, kt & 63);
+            }
+            bits = __builtin_amdgcn_readfirstlane(bits);
+            if (bits == 0) return;
+            char* st = smem + (u % STAGES) * ST_BYTES;
+            const int r = lw * 64 + lane;                 // this lane's row of the A and of the B block
+            const int sw = (r >> 2) & 3;
+            while (bits) {
+                const int k = __builtin_ctz(bits);
+                bits &= bits - 1;
+                const uint32_t o = (uint32_t)(r * ROWB + ((((k >> 3) ^ sw)) << 4) + (k & 7) * 2);
+                *reinterpret_cast<bf16_t*>(st + o) = 0;
+                *reinterpret_cast<bf16_t*>(st + A_ST + o) = 0;
+            }
+        };
         if (my_tiles > 0) load_tile();
         const int pro = min(STAGES - 1, steps);
         for (int s0 = 0; s0 < pro; ++s0) {
@@ -360,12 +431,13 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             advance();
         }
         for (int s = 0; s < steps; ++s) {
-            // steps s and s + 1 complete at barrier s (the MFMA waves read
-            // step s + 1's first operands during step s); later ones in flight
+            // steps s and s + 1 complete at barrier s; later ones in flight
             const int ahead = min(STAGES - 3, steps - 2 - s);
             if (ahead >= 2) wait_vmcnt<2 * LOADS>();
             else if (ahead == 1) wait_vmcnt<LOADS>();
             else wait_vmcnt<0>();
+            if (s == 0) zero_dead(0);
+            if (s + 1 < steps) zero_dead(s + 1);
             __syncthreads();
             const bool fetch = s + STAGES - 1 < steps;
             issue_step(fetch);
@@ -410,28 +482,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             const char* st = smem + c_stage * ST_BYTES;
             c_stage = c_stage == STAGES - 1 ? 0 : c_stage + 1;
             const char* stn = smem + c_stage * ST_BYTES;             // the next step
-            const bool tail = (kt == nk - 1) && (K % BK) != 0;
-            auto mask_tail = [&](int sub, bf16x8_t (&af)[MI], bf16x8_t (&bfr)[4]) {
-                const int kk = kt * BK + sub * 16 + hi * 8;
-                uint32_t keep[4];
-#pragma unroll
-                for (int h = 0; h < 4; ++h)
-                    keep[h] = (kk + 2 * h < K ? 0xffffu : 0u) | (kk + 2 * h + 1 < K ? 0xffff0000u : 0u);
-#pragma unroll
-                for (int i = 0; i < MI; ++i) {
-                    uint4 u = __builtin_bit_cast(uint4, af[i]);
-                    u.x &= keep[0]; u.y &= keep[1]; u.z &= keep[2]; u.w &= keep[3];
-                    af[i] = __builtin_bit_cast(bf16x8_t, u);
-                }
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    uint4 v = __builtin_bit_cast(uint4, bfr[j]);
-                    v.x &= keep[0]; v.y &= keep[1]; v.z &= keep[2]; v.w &= keep[3];
-                    bfr[j] = __builtin_bit_cast(bf16x8_t, v);
-                }
-            };
             bf16x8_t a1[MI], b1[4];
-            if (tail) mask_tail(0, a0, b0);
 #pragma unroll
             for (int x = 0; x < 4 * MI; ++x) {
                 const int i = x >> 2, j = x & 3;
@@ -441,7 +492,6 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 else if (y >= 4 && y < 4 + MI)
                     a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
             }
-            if (tail) mask_tail(1, a1, b1);
             // sub-step 1; after MFMA x, the operand read x - 2 of the next
             // step's sub-step 0 (its stage is complete since this step's
             // barrier; after a tile's last step the values go unused)
@@ -457,13 +507,15 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             }
         }
 
+        // 32x32 accumulator layout: lane holds column (lane & 31) and, in
+        // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.
         int ch, m0, n0;
         decode(it, ch, m0, n0);
         const int row0 = m0 + wm * 64 + 4 * hi, col0 = n0 + wn * 128 + rl;
         const bool full = m0 + BM <= M && n0 + BN <= N;
         const int64_t jblocks = (N + kResJ - 1) / kResJ;
-        float* Cb = C + result_off(jblocks, nchan, ch, row0, col0);
-        const int64_t row_step = jblocks * nchan * kResJ;
+        float* Cb = BLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0) : C + ch * sC + (int64_t)row0 * ldc + col0;
+        const int64_t row_step = BLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -471,7 +523,8 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
-                    float* p = Cb + (int64_t)dr * row_step + (int64_t)j * nchan * kResJ;
+                    // column block j*32 of a blocked C is (j * nchan * 32) floats further on
+                    float* p = Cb + (int64_t)dr * row_step + (BLOCKED ? (int64_t)j * nchan * kResJ : j * 32);
                     if (full || (row0 + dr < M && col0 + j * 32 < N)) {
                         float v = acc[i][j][r];
                         if (accumulate) v += *p;
@@ -571,15 +624,17 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
 #define K2_LAUNCH(KM, BL)                                                                                      \
     hipLaunchKernelGGL((k2_contract_mfma<BM, KM, BL>), dim3(grid), dim3(256), 0, s, a, b, C, (int)M, (int)N, \
                        (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
+#define K2_WS(BL, KM)                                                                                           \
+    hipLaunchKernelGGL((k2_contract_ws<BL, KM>), dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K,  \
+                       (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
     if (kmask) {
         if (blocked) K2_LAUNCH(true, true);
-        else K2_LAUNCH(true, false);
+        else K2_WS(false, true);
     } else {
-        if (blocked)
-            hipLaunchKernelGGL(k2_contract_ws, dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K, tm, tn,
-                               total, accumulate);
-        else K2_LAUNCH(false, false);
+        if (blocked) K2_WS(true, false);
+        else K2_WS(false, false);
     }
+#undef K2_WS
 #undef K2_LAUNCH
     return hipGetLastError();
 }
