@@ -16,13 +16,11 @@ namespace {
 
 // ---------------------------------------------------------------- bf16 MFMA
 //
-// Persistent kernel: one work-group (4 waves) per CU, each looping over
-// 256 x 256 output tiles; a wave owns a 128 x 128 sub-tile = 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16.  The k loop runs in steps of 32 through an LDS
-// ring of 32 KB stages (5 stages without a k-mask, 4 with one) filled by
-// direct-to-LDS buffer loads (no VGPR staging), STAGES - 1 steps ahead of
-// the step being multiplied.  The ring flows straight from one output tile
-// into the next.
+// Persistent kernel, one work-group per CU, looping over 256 x 256 output
+// tiles.  The k loop runs in steps of 32 through an LDS ring of 32 KB stages
+// filled by direct-to-LDS buffer loads (no VGPR staging) several steps ahead
+// of the step being multiplied; the ring flows straight from one output
+// tile into the next.
 //
 // Tile order: in round r the work-groups on XCD x take 32 consecutive
 // logical tiles, i.e. a 4 x 8 block of one channel, so the A row panels and B
@@ -36,244 +34,7 @@ namespace {
 constexpr int BN = 256, BK = 32;
 constexpr int ROWB = BK * 2;                    // 64 bytes per row per stage
 constexpr int B_ST = BN * ROWB;                 // 16 KB
-constexpr int MASK_ST = 4 * 256;                // per-wave k-mask bytes (KMASK only)
 constexpr int kLdsBytes = 160 * 1024;           // gfx950 LDS per work-group
-
-// Tile geometry for BM output rows per work-group (256 or 384): each wave owns
-// BM/2 x 128 outputs = MI x 4 MFMA blocks, and loads LA blocks of 16 A rows
-// and 4 blocks of 16 B rows per k-step.
-template <int BM, bool KMASK> struct Geo {
-    static constexpr int MI = BM / 64;
-    static constexpr int LA = BM / 64;
-    static constexpr int A_ST = BM * ROWB;
-    static constexpr int ST_BYTES = A_ST + B_ST + (KMASK ? MASK_ST : 0);
-    static constexpr int STAGES = kLdsBytes / ST_BYTES >= 5 ? 5 : kLdsBytes / ST_BYTES >= 4 ? 4 : 3;
-};
-
-template <int BM, bool KMASK, bool BLOCKED>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
-void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C,
-                      int M, int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB,
-                      int64_t sC, int tiles_m, int tiles_n, int total, int accumulate,
-                      const uint8_t* __restrict__ kmask) {
-    using GG = Geo<BM, KMASK>;
-    constexpr int MI = GG::MI, LA = GG::LA, A_ST = GG::A_ST, ST_BYTES = GG::ST_BYTES, STAGES = GG::STAGES;
-    constexpr int NPART = LA + 4;                // buffer loads of A and B per wave per step
-    __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
-    constexpr int LOADS = NPART + (KMASK ? 1 : 0);  // buffer loads per wave per step
-
-    const int G = gridDim.x, wg = blockIdx.x;
-    const int perm = (G & 7) == 0 ? (wg & 7) * (G >> 3) + (wg >> 3) : wg;
-    const int my_tiles = perm < total ? (total - 1 - perm) / G + 1 : 0;
-    const int nk = (K + BK - 1) / BK;
-    const int steps = my_tiles * nk;
-    const int tiles = tiles_m * tiles_n;
-    const int nchan = total / tiles;
-
-    const int t = threadIdx.x, lane = t & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // uniform per wave
-    const int wm = wave >> 1, wn = wave & 1;
-    const int rl = lane & 31, hi = lane >> 5;
-
-    auto decode = [&](int it, int& ch, int& m0, int& n0) {
-        const int L = it * G + perm;
-        ch = L / tiles;
-        const int rem = L - ch * tiles;
-        constexpr int GR = 4;   // tile rows per group: 32 consecutive tiles form a 4 x 8 block
-        const int gid = rem / (GR * tiles_n);
-        const int first_m = gid * GR;
-        const int gsz = min(tiles_m - first_m, GR);
-        const int in_g = rem - gid * GR * tiles_n;
-        m0 = (first_m + in_g % gsz) * BM;
-        n0 = (in_g / gsz) * BN;
-    };
-
-    // Direct-to-LDS: lane i of a load writes 16 bytes at (instruction base + 16 i),
-    // i.e. row (i >> 2) of the 16 rows the instruction covers, slot (i & 3);
-    // it therefore fetches chunk (i & 3) ^ ((row >> 2) & 3) of that row.
-    const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
-    // Row-major operands: row r at r * ld elements.  Blocked operands: one
-    // tile's k-step is a contiguous [256 rows][32] block (row r at r * 32).
-    const int rsa = BLOCKED ? BK : lda, rsb = BLOCKED ? BK : ldb;
-    const uint32_t va = (uint32_t)(((wave * (BM / 4) + (lane >> 2)) * rsa + lkc * 8) * 2);
-    const uint32_t vb = (uint32_t)(((wave * 64 + (lane >> 2)) * rsb + lkc * 8) * 2);
-    const uint32_t a_j = (uint32_t)(16 * rsa * 2), b_j = (uint32_t)(16 * rsb * 2);
-    const uint32_t a_k = BLOCKED ? (uint32_t)(BM * BK * 2) : (uint32_t)ROWB;   // bytes per k-step
-    const uint32_t b_k = BLOCKED ? (uint32_t)(BN * BK * 2) : (uint32_t)ROWB;
-    // kmask is the staged copy: 0/1 bytes, zero-padded to a multiple of 32
-    const v4i_t rmask = buffer_desc(kmask, KMASK ? (uint32_t)((K + 31) / 32 * 32) : 0u);
-
-    // Load cursor: the tile and k-step of the next step to be fetched.  The
-    // tile decode and buffer descriptors change once per tile, not per step.
-    const uint32_t lds_base = lds_addr(smem);
-    int l_it = 0, l_kt = 0, l_stage = 0;
-    v4i_t ra, rb;
-    auto load_tile = [&]() {
-        int ch, m0, n0;
-        decode(l_it, ch, m0, n0);
-        if (BLOCKED) {   // the tile-row's blocks for all k-steps; rows past M are padding, never stored
-            ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK), (uint32_t)(nk * BM * BK * 2));
-            rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK), (uint32_t)(nk * BN * BK * 2));
-        } else {         // rows past M (N) fall outside the descriptor and load as zero
-            ra = buffer_desc(A + ch * sA + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 2));
-            rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
-        }
-    };
-    // Part j of the next step's fetch: j < LA are A row blocks, then 4 B row
-    // blocks (16 rows each per wave); part NPART is the k-mask.
-    // With live == false the part is still issued, through a zero-size
-    // descriptor: it reads nothing, and keeps the k loop free of branches.
-    // (Past the last step the cursor no longer advances, so such loads go to
-    // the stage after the last fetched step, which no later step uses.)
-    const v4i_t rnone = buffer_desc(A, 0u);
-    auto issue_part = [&](int j, bool live) {
-        const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
-        if (j < LA) lds_load16(live ? ra : rnone, va, j * a_j + l_kt * a_k, st + (wave * (BM / 4) + 16 * j) * ROWB);
-        else if (j < NPART)
-            lds_load16(live ? rb : rnone, vb, (j - LA) * b_j + l_kt * b_k, st + A_ST + (wave * 64 + 16 * (j - LA)) * ROWB);
-        else if (KMASK)   // bytes [kt*32, kt*32 + 256) of the staged k-mask; past its end reads as 0
-            lds_load4(live ? rmask : rnone, (uint32_t)lane * 4, (uint32_t)l_kt * BK, st + A_ST + B_ST + wave * 256);
-    };
-    auto advance = [&]() {
-        l_stage = l_stage == STAGES - 1 ? 0 : l_stage + 1;
-        if (++l_kt == nk) {
-            l_kt = 0;
-            if (++l_it < my_tiles) load_tile();
-        }
-    };
-    auto issue_next = [&]() {
-#pragma unroll
-        for (int j = 0; j <= NPART; ++j) issue_part(j, true);
-        advance();
-    };
-
-    const int q = (rl >> 2) & 3;
-    uint32_t rdA[2], rdB[2];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-        const uint32_t x = (uint32_t)(((2 * sub + hi) ^ q) << 4);
-        rdA[sub] = (wm * (BM / 2) + rl) * ROWB + x;
-        rdB[sub] = A_ST + (wn * 128 + rl) * ROWB + x;
-    }
-
-    if (my_tiles > 0) load_tile();
-    const int pro = min(STAGES - 1, steps);
-    for (int s = 0; s < pro; ++s) issue_next();
-    int c_stage = 0;
-
-    for (int it = 0; it < my_tiles; ++it) {
-        f32x16_t acc[MI][4];
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-        for (int kt = 0; kt < nk; ++kt) {
-            const int s = it * nk + kt;
-            const int ahead = min(STAGES - 2, steps - 1 - s);   // later steps already in flight
-            if (ahead >= 3) wait_vmcnt<3 * LOADS>();
-            else if (ahead == 2) wait_vmcnt<2 * LOADS>();
-            else if (ahead == 1) wait_vmcnt<LOADS>();
-            else wait_vmcnt<0>();
-            __syncthreads();
-            const bool fetch = s + STAGES - 1 < steps;
-
-            const char* st = smem + c_stage * ST_BYTES;
-            c_stage = c_stage == STAGES - 1 ? 0 : c_stage + 1;
-            const bool tail = (kt == nk - 1) && (K % BK) != 0;
-
-            // Zero the operands of k past K or masked out (0 * garbage must not
-            // reach the sum); only on the last step of a ragged K or with a k-mask.
-            auto mask_frags = [&](int sub, bf16x8_t (&af)[MI], bf16x8_t (&bfr)[4]) {
-                const int kl = sub * 16 + hi * 8;   // lane's first k within the step
-                uint32_t keep[4];
-                if (KMASK) {
-                    const uint2 mb = *reinterpret_cast<const uint2*>(st + A_ST + B_ST + wave * 256 + kl);
-#pragma unroll
-                    for (int h = 0; h < 4; ++h) {
-                        const uint32_t b2 = h < 2 ? (mb.x >> (16 * h)) : (mb.y >> (16 * (h - 2)));
-                        keep[h] = ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
-                    }
-                } else {
-                    const int kk = kt * BK + kl;
-#pragma unroll
-                    for (int h = 0; h < 4; ++h)
-                        keep[h] = (kk + 2 * h < K ? 0xffffu : 0u) | (kk + 2 * h + 1 < K ? 0xffff0000u : 0u);
-                }
-#pragma unroll
-                for (int i = 0; i < MI; ++i) {
-                    uint4 u = __builtin_bit_cast(uint4, af[i]);
-                    u.x &= keep[0]; u.y &= keep[1]; u.z &= keep[2]; u.w &= keep[3];
-                    af[i] = __builtin_bit_cast(bf16x8_t, u);
-                }
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    uint4 v = __builtin_bit_cast(uint4, bfr[j]);
-                    v.x &= keep[0]; v.y &= keep[1]; v.z &= keep[2]; v.w &= keep[3];
-                    bfr[j] = __builtin_bit_cast(bf16x8_t, v);
-                }
-            };
-
-            bf16x8_t a0[MI], b0[4], a1[MI], b1[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) b0[j] = *reinterpret_cast<const bf16x8_t*>(st + rdB[0] + j * 32 * ROWB);
-#pragma unroll
-            for (int i = 0; i < MI; ++i) a0[i] = *reinterpret_cast<const bf16x8_t*>(st + rdA[0] + i * 32 * ROWB);
-            if (KMASK || tail) mask_frags(0, a0, b0);
-            // Sub-step 0: 4 MI MFMAs; after every second one, one part of the
-            // next step's fetch and one operand read of sub-step 1.
-#pragma unroll
-            for (int x = 0; x < 4 * MI; ++x) {
-                const int i = x >> 2, j = x & 3;
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
-                if (x & 1) {
-                    const int y = x >> 1;   // 0 .. 2 MI - 1 >= NPART - 1
-                    if (y < NPART) issue_part(y, fetch);
-                    if (y < 4) b1[y] = *reinterpret_cast<const bf16x8_t*>(st + rdB[1] + y * 32 * ROWB);
-                    else if (y < 4 + MI) a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
-                }
-            }
-            if (KMASK) issue_part(NPART, fetch);
-            if (fetch) advance();
-            if (KMASK || tail) mask_frags(1, a1, b1);
-#pragma unroll
-            for (int x = 0; x < 4 * MI; ++x) {
-                const int i = x >> 2, j = x & 3;
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
-            }
-        }
-
-        // 32x32 accumulator layout: lane holds column (lane & 31) and, in
-        // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.  Either layout
-        // of C gets 32 consecutive floats (128 bytes) per half-wave store.
-        int ch, m0, n0;
-        decode(it, ch, m0, n0);
-        const int row0 = m0 + wm * (BM / 2) + 4 * hi, col0 = n0 + wn * 128 + rl;
-        const bool full = m0 + BM <= M && n0 + BN <= N;
-        const int64_t jblocks = (N + kResJ - 1) / kResJ;
-        float* Cb = BLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0)
-                            : C + ch * sC + (int64_t)row0 * ldc + col0;
-        const int64_t row_step = BLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
-                    // column block j*32 of a blocked C is (j * nchan * 32) floats further on
-                    float* p = Cb + (int64_t)dr * row_step + (BLOCKED ? (int64_t)j * nchan * kResJ : j * 32);
-                    if (full || (row0 + dr < M && col0 + j * 32 < N)) {
-                        float v = acc[i][j][r];
-                        if (accumulate) v += *p;
-                        *p = v;
-                    }
-                }
-    }
-    wait_vmcnt<0>();   // the zero-size loads of the last steps land before the work-group ends
-}
 
 // ------------------------------------------- bf16 MFMA, 8 + 4 specialised waves
 //
@@ -295,7 +56,7 @@ void k2_contract_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B
 // hold arbitrary data) -- are zeroed in LDS by the loader waves, in the rows
 // each loaded, before the barrier that publishes the stage: only steps that
 // hold such k pay, and the MFMA waves never mask.
-// LDS ring (5 stages), swizzle and tile order as in k2_contract_mfma.
+// LDS ring of 5 stages, swizzle and tile order as described above.
 template <bool BLOCKED, bool KMASK>
 __global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_per_eu(3, 3)))
 void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
@@ -621,21 +382,17 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
     const int grid = total < cus ? total : cus;
     const bf16_t* a = (const bf16_t*)A;
     const bf16_t* b = (const bf16_t*)B;
-#define K2_LAUNCH(KM, BL)                                                                                      \
-    hipLaunchKernelGGL((k2_contract_mfma<BM, KM, BL>), dim3(grid), dim3(256), 0, s, a, b, C, (int)M, (int)N, \
-                       (int)K, (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
 #define K2_WS(BL, KM)                                                                                           \
     hipLaunchKernelGGL((k2_contract_ws<BL, KM>), dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K,  \
                        (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
     if (kmask) {
-        if (blocked) K2_LAUNCH(true, true);
+        if (blocked) K2_WS(true, true);
         else K2_WS(false, true);
     } else {
         if (blocked) K2_WS(true, false);
         else K2_WS(false, false);
     }
 #undef K2_WS
-#undef K2_LAUNCH
     return hipGetLastError();
 }
 
