@@ -64,6 +64,33 @@ def test_block_accumulate_kmask_exact(dtype):
     np.testing.assert_array_equal(host(acc).transpose(1, 2, 0), ref)
 
 
+def test_block_accumulate_no_mask_ignores_padding():
+    """Without a token mask the contraction must still ignore the padding
+    columns past klen of row-major panels (NaN and huge values here), in the
+    last, ragged k-step that loads them; three panels, one shorter than a
+    k-step, exact on integer data (bf16)."""
+    say("block accumulate without mask, garbage padding")
+    layer, _ = make_layer("bf16")
+    rows, cols, n_total = 260, 33, 600
+    g = torch.Generator().manual_seed(11)
+    acc = torch.full((128, rows, cols), float("nan"), device="cuda")
+    ks = [(0, 61), (61, 20), (81, 100)]
+    aps, bps = [], []
+    for idx, (k0, klen) in enumerate(ks):
+        ld = (klen + 7) // 8 * 8 + 16
+        ap = torch.randint(-4, 5, (128, rows, ld), generator=g).to(torch.bfloat16)
+        bp = torch.randint(-4, 5, (128, cols, ld), generator=g).to(torch.bfloat16)
+        ap[:, :, klen:] = float("nan")
+        bp[:, :, klen:] = -3e38
+        aps.append(ap[:, :, :klen])
+        bps.append(bp[:, :, :klen])
+        v = T.BlockView(n_total, 100, 300, rows, cols, k0, klen, ld, ld, idx, len(ks) + 1)   # no epilogue
+        layer.block_accumulate(v, ap.cuda(), bp.cuda(), acc, None)
+    torch.cuda.synchronize()
+    ref = oracle.block_contract([host(a) for a in aps], [host(b) for b in bps], [np.ones(kl) for _, kl in ks])
+    np.testing.assert_array_equal(host(acc).transpose(1, 2, 0), ref)
+
+
 # ------------------------------------------------------------- projection
 
 @pytest.mark.parametrize("dtype,N", [("bf16", 72), ("bf16", 300), ("f32", 65)])
