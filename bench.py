@@ -348,11 +348,13 @@ def main():
         bz = synth.pair_tensor(0, dtype="bf16", device=dev, name="z_tile", shape=(bb, bb, 128))
         bacc = torch.empty((128, bb, bb), dtype=torch.float32, device=dev)
         bout = torch.empty((bb, bb, 128), dtype=torch.float32, device=dev)
+        tws = torch.empty(layer.block_workspace_size(T.BlockView(bn, brow, brow, bb, bb, 0, bb, bld, bld, 0, bg)),
+                          dtype=torch.uint8, device=dev)
 
         def ring_tile():
             for p in range(bg):
                 v = T.BlockView(bn, brow, brow, bb, bb, p * bb, bb, bld, bld, p, bg)
-                layer.block_accumulate(v, bpa[p & 1], bpb[p & 1], bacc, bmask, bz, bout, stream)
+                layer.block_accumulate(v, bpa[p & 1], bpb[p & 1], bacc, bmask, bz, bout, stream, ws=tws)
 
         ring_tile()
         t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -362,7 +364,7 @@ def main():
         t1e.record(stream)
         torch.cuda.synchronize()
         tile_ms = t0e.elapsed_time(t1e) / 2
-        del bpa, bpb, bz, bacc, bout
+        del bpa, bpb, bz, bacc, bout, tws
         torch.cuda.empty_cache()
         print(f"[bench] ring tile {tile_ms:.3f} ms", file=sys.stderr, flush=True)
 
@@ -428,7 +430,7 @@ def main():
         "ring_tile": None if tile_ms is None else {"ms": round(tile_ms, 4),
                       "TFLOP_per_s": round(tile_flops / (tile_ms * 1e-3) / 1e12, 2),
                       "roofline": mfma_roof(tile_flops, tile_ms),
-                      "what": "tile (7,7) of an 8x8 grid at N=30000: 8 block_accumulate ring steps (3750x3750 "
+                      "what": "tile (7,7) of an 8x8 grid at N=30000: 8 tri_mul_block_accumulate_ws ring steps (3750x3750 "
                               "outputs, 3750-token k-panels, 128 channels; 108.0 TFLOP contraction) with the "
                               "epilogue on the last step; fp32 accumulator and output; not part of ms_per_step"},
         "backward_layer": None if lbwd_ms is None else {"ms": round(lbwd_ms, 4),

@@ -162,6 +162,24 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v,
                              const uint8_t* mask, const void* z_tile, void* out_tile,
                              void* stream);
 
+/* Bytes of device workspace tri_mul_block_accumulate_ws needs for the view's
+ * sizes (rows, cols, klen): both panels repacked, masked, into the blocked
+ * operand layout (see tri_mul_project), 128 * ceil(rows/256) *
+ * ceil(klen/32) * 16 KB + the same for cols, each part 256-byte aligned; 0
+ * for the fp32 path.  *bytes is a HOST pointer. */
+int tri_mul_block_workspace_size(tri_mul_handle_t h, const tri_mul_block_view_t* v, size_t* bytes);
+
+/* The same ring step as tri_mul_block_accumulate (same arguments, results
+ * and errors) through a caller-owned workspace (256-byte aligned, at least
+ * tri_mul_block_workspace_size bytes, else TRI_MUL_ENOMEM): the two panels
+ * are first repacked, with the mask applied, into the blocked layout, so
+ * the contraction reads whole 16 KB blocks instead of 64-byte row pieces.
+ * The workspace is scratch for the duration of the call (stream-ordered). */
+int tri_mul_block_accumulate_ws(tri_mul_handle_t h, const tri_mul_block_view_t* v,
+                                const void* a_panel, const void* b_panel, float* acc,
+                                const uint8_t* mask, const void* z_tile, void* out_tile,
+                                void* ws, size_t ws_bytes, void* stream);
+
 /* The three stages of tri_mul_outgoing / tri_mul_incoming, exposed so that
  * callers can time or check them one by one.
  *

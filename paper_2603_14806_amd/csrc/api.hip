@@ -470,10 +470,13 @@ int tri_mul_contract_backward(tri_mul_handle_t h, const float* dC, const void* a
     return ok();
 }
 
-int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
-                             const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
-                             void* out_tile, void* stream) {
-    if (int rc = check_handle(h)) return rc;
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by the two block entry points.
+int check_block(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel, const void* b_panel,
+                const float* acc, const void* z_tile, const void* out_tile) {
     if (!v) return fail(TRI_MUL_EINVAL, "null view");
     if (!a_panel || !b_panel || !acc) return fail(TRI_MUL_EINVAL, "null panel or accumulator pointer");
     if (v->n_total < 1 || v->rows < 1 || v->cols < 1 || v->klen < 1) return fail(TRI_MUL_EINVAL, "empty or negative view sizes");
@@ -491,6 +494,29 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
         if (!z_tile || !out_tile) return fail(TRI_MUL_EINVAL, "the last k-panel needs z_tile and out_tile");
         if (!aligned16(z_tile) || !aligned16(out_tile)) return fail(TRI_MUL_EINVAL, "z_tile and out_tile must be 16-byte aligned");
     }
+    return TRI_MUL_OK;
+}
+
+// Bytes of the two repacked panels (blocked layout), each 256-byte aligned.
+size_t block_ws_a(const tri_mul_block_view_t* v) {
+    const size_t nk = (size_t)((v->klen + 31) / 32);
+    return round256((size_t)128 * (size_t)((v->rows + 255) / 256) * nk * 256 * 32 * 2);
+}
+size_t block_ws_b(const tri_mul_block_view_t* v) {
+    const size_t nk = (size_t)((v->klen + 31) / 32);
+    return round256((size_t)128 * (size_t)((v->cols + 255) / 256) * nk * 256 * 32 * 2);
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                             const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                             void* out_tile, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_block(h, v, a_panel, b_panel, acc, z_tile, out_tile)) return rc;
+    const bool last = v->k_index == v->k_count - 1;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int64_t sA = v->rows * v->ld_a, sB = v->cols * v->ld_b, sC = v->rows * v->cols;
     hipError_t e = hipSuccess;
@@ -511,6 +537,46 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v, 
     return ok();
 }
 
+
+int tri_mul_block_workspace_size(tri_mul_handle_t h, const tri_mul_block_view_t* v, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (!v || !bytes) return fail(TRI_MUL_EINVAL, "null view or bytes pointer");
+    if (v->rows < 1 || v->cols < 1 || v->klen < 1 || v->rows > kMaxN || v->cols > kMaxN ||
+        v->klen > trimul::kMaxKPanel)
+        return fail(TRI_MUL_EINVAL, "tile sides and k-panel length must lie in [1, %lld]", (long long)kMaxN);
+    *bytes = h->dtype == TRI_MUL_BF16 ? block_ws_a(v) + block_ws_b(v) : 0;
+    return ok();
+}
+
+int tri_mul_block_accumulate_ws(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                                const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                                void* out_tile, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_block(h, v, a_panel, b_panel, acc, z_tile, out_tile)) return rc;
+    if (h->dtype != TRI_MUL_BF16)   // the fp32 path has no blocked form: the plain call is the same op
+        return tri_mul_block_accumulate(h, v, a_panel, b_panel, acc, mask, z_tile, out_tile, stream);
+    const size_t need = block_ws_a(v) + block_ws_b(v);
+    if (!ws) return fail(TRI_MUL_EINVAL, "null workspace");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
+    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* wa = static_cast<char*>(ws);
+    char* wb = wa + block_ws_a(v);
+    const bool last = v->k_index == v->k_count - 1;
+    hipError_t e = trimul::launch_stage_kmask(mask ? mask + v->k0 : nullptr, v->klen, h->w.kmask_pad, s);
+    if (e == hipSuccess) e = trimul::launch_panel_block(a_panel, v->rows, v->ld_a, v->klen, h->c, h->w.kmask_pad, wa, s);
+    if (e == hipSuccess) e = trimul::launch_panel_block(b_panel, v->cols, v->ld_b, v->klen, h->c, h->w.kmask_pad, wb, s);
+    if (e != hipSuccess) return hip_fail(e, "panel repack kernel launch");
+    e = trimul::launch_contract_blocked_rowc(wa, wb, acc, v->rows, v->cols, v->klen, h->c, v->k_index > 0, h->w.cus, s);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    if (last) {
+        const int64_t sC = v->rows * v->cols;
+        trimul::EpilogueArgs ea{acc, 0, v->cols, sC, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
+        e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    }
+    return ok();
+}
 
 int tri_mul_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
     if (int rc = check_handle(h)) return rc;

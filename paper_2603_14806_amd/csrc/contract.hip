@@ -48,16 +48,17 @@ constexpr int kLdsBytes = 160 * 1024;           // gfx950 LDS per work-group
 // at barrier s steps s and s + 1 are complete, and the MFMA waves read step
 // s + 1's first operands behind step s's last MFMAs.
 //
-// Operands either blocked (the full update: one tile's k-step is a
-// contiguous 16 KB block, C in the pair-blocked result layout) or row-major
-// (a device tile's caller panels [ch][rows][ld] and accumulator
-// [ch][rows][ldc]).  k values that must not reach the sums -- masked by the
+// Operands either blocked (one tile's k-step is a contiguous 16 KB block:
+// the full update, the outer product mean, and a device tile's panels
+// repacked by k_panel_block) or row-major (a device tile's caller panels
+// [ch][rows][ld]); C either in the pair-blocked result layout (the full
+// update) or row-major [ch][rows][ldc] (a device tile's accumulator).  k values that must not reach the sums -- masked by the
 // optional k-mask, or past K in the last step (row-major padding columns
 // hold arbitrary data) -- are zeroed in LDS by the loader waves, in the rows
 // each loaded, before the barrier that publishes the stage: only steps that
 // hold such k pay, and the MFMA waves never mask.
 // LDS ring of 5 stages, swizzle and tile order as described above.
-template <bool BLOCKED, bool KMASK>
+template <bool BLOCKED, bool KMASK, bool CBLOCKED>
 __global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_per_eu(3, 3)))
 void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
                     int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB, int64_t sC, int tiles_m,
@@ -275,8 +276,8 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         const int row0 = m0 + wm * 64 + 4 * hi, col0 = n0 + wn * 128 + rl;
         const bool full = m0 + BM <= M && n0 + BN <= N;
         const int64_t jblocks = (N + kResJ - 1) / kResJ;
-        float* Cb = BLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0) : C + ch * sC + (int64_t)row0 * ldc + col0;
-        const int64_t row_step = BLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
+        float* Cb = CBLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0) : C + ch * sC + (int64_t)row0 * ldc + col0;
+        const int64_t row_step = CBLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -285,7 +286,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 for (int r = 0; r < 16; ++r) {
                     const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
                     // column block j*32 of a blocked C is (j * nchan * 32) floats further on
-                    float* p = Cb + (int64_t)dr * row_step + (BLOCKED ? (int64_t)j * nchan * kResJ : j * 32);
+                    float* p = Cb + (int64_t)dr * row_step + (CBLOCKED ? (int64_t)j * nchan * kResJ : j * 32);
                     if (full || (row0 + dr < M && col0 + j * 32 < N)) {
                         float v = acc[i][j][r];
                         if (accumulate) v += *p;
@@ -354,7 +355,68 @@ __global__ void k_stage_kmask(const uint8_t* __restrict__ mask, int klen, int pa
     if (k < padded) dst[k] = (k < klen && (!mask || mask[k] != 0)) ? 1 : 0;
 }
 
+// Repack a device tile's row-major panel [ch][rows][ld] (bf16) into the
+// blocked operand layout of the contraction, [ch][tiles][nk][256][32], with
+// the staged k-mask applied and zeros for rows >= rows and k >= klen (the
+// staged mask is 0 there).  One work-group per (two k-steps, 256-row tile,
+// channel); thread r moves the 128 bytes of its row: whole cache lines in,
+// two 64-byte rows of two 16 KB blocks out.
+__global__ __launch_bounds__(256) void k_panel_block(const bf16_t* __restrict__ P, int rows, int ld, int64_t sP,
+                                                     int tiles, int nk, const uint8_t* __restrict__ kst,
+                                                     bf16_t* __restrict__ dst) {
+    const int kp = blockIdx.x, tile = blockIdx.y, c = blockIdx.z, r = threadIdx.x;
+    const int r0 = tile * 256;
+    const int nrow = min(256, rows - r0);
+    // rows past the panel fall outside the descriptor and read as zero
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(P + c * sP + (int64_t)r0 * ld, (uint32_t)nrow * (uint32_t)ld * 2u);
+    uint4 v[2][4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            v[h][q] = buf_load16(rp, (uint32_t)(r * ld + (2 * kp + h) * 32 + 8 * q) * 2u);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int kt = 2 * kp + h;
+        if (kt >= nk) break;
+        bf16_t* out = dst + (((int64_t)c * tiles + tile) * nk + kt) * (256 * 32) + r * 32;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            // staged 0/1 bytes of k = 32 kt + 8 q .. + 7 (fresh for every k < 32 nk)
+            const uint2 m8 = *reinterpret_cast<const uint2*>(kst + kt * 32 + 8 * q);
+            const uint32_t mw[2] = {m8.x, m8.y};
+            uint32_t w[4] = {v[h][q].x, v[h][q].y, v[h][q].z, v[h][q].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t b2 = mw[e >> 1] >> (16 * (e & 1));
+                w[e] &= ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
+            }
+            *reinterpret_cast<uint4*>(out + 8 * q) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t klen, int nch, const uint8_t* kst,
+                              void* dst, hipStream_t s) {
+    const int tiles = (int)((rows + 255) / 256), nk = (int)((klen + 31) / 32);
+    hipLaunchKernelGGL(k_panel_block, dim3((unsigned)((nk + 1) / 2), (unsigned)tiles, (unsigned)nch), dim3(256), 0, s,
+                       (const bf16_t*)P, (int)rows, (int)ld, rows * ld, tiles, nk, kst, (bf16_t*)dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
+                                        int batch, int accumulate, int cus, hipStream_t s) {
+    constexpr int BM = 256;
+    const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
+    const int total = tm * tn * batch;
+    const int grid = total < cus ? total : cus;
+    hipLaunchKernelGGL((k2_contract_ws<true, false, false>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A,
+                       (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, N, (int64_t)0, (int64_t)0, M * N, tm, tn,
+                       total, accumulate, (const uint8_t*)nullptr);
+    return hipGetLastError();
+}
 
 hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s) {
     const int padded = (int)((klen + 31) / 32 * 32);
@@ -382,8 +444,8 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
     const int grid = total < cus ? total : cus;
     const bf16_t* a = (const bf16_t*)A;
     const bf16_t* b = (const bf16_t*)B;
-#define K2_WS(BL, KM)                                                                                           \
-    hipLaunchKernelGGL((k2_contract_ws<BL, KM>), dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K,  \
+#define K2_WS(BL, KM)                                                                                              \
+    hipLaunchKernelGGL((k2_contract_ws<BL, KM, BL>), dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K, \
                        (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
     if (kmask) {
         if (blocked) K2_WS(true, true);

@@ -34,6 +34,13 @@ constexpr int64_t kMaxKPanel = 65536;   // longest k-panel of one block call
 // Copies mask[0, klen) into dst as 0/1 bytes (mask NULL: all ones) and zero-fills dst up to the next
 // multiple of 32 (so the contraction can read whole 4-byte words of it).
 hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s);
+// Row-major bf16 panel [nch][rows][ld] -> blocked [nch][ceil(rows/256)][ceil(klen/32)][256][32],
+// staged k-mask applied, padding zero.
+hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t klen, int nch, const uint8_t* kst,
+                              void* dst, hipStream_t s);
+// bf16 contraction of blocked operands into a row-major fp32 C [batch][M][N].
+hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
+                                        int batch, int accumulate, int cus, hipStream_t s);
 
 struct EpilogueArgs {
     const float* C;      // fp32 contraction result: pair-blocked (cblocked) or [c][rows][ldc]

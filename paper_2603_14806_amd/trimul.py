@@ -71,6 +71,9 @@ SIGNATURES = {
     "tri_mul_outgoing": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
     "tri_mul_incoming": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
     "tri_mul_block_accumulate": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "tri_mul_block_workspace_size": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_block_accumulate_ws": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                    ctypes.c_size_t, _vp]),
     "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
@@ -182,6 +185,18 @@ def tri_mul_incoming(h, z, mask, N, out, ws, ws_bytes, stream=None):
 def tri_mul_block_accumulate(h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream=None):
     _check(lib().tri_mul_block_accumulate(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(acc),
                                           _ptr(mask), _ptr(z_tile), _ptr(out_tile), _stream(stream)))
+
+
+def tri_mul_block_workspace_size(h, view):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_block_workspace_size(h, ctypes.byref(view), ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_block_accumulate_ws(h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, ws, ws_bytes, stream=None):
+    _check(lib().tri_mul_block_accumulate_ws(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(acc),
+                                             _ptr(mask), _ptr(z_tile), _ptr(out_tile), _ptr(ws), ws_bytes,
+                                             _stream(stream)))
 
 
 def tri_mul_project(h, z, mask, N, direction, a_panels, b_panels, stream=None):
@@ -329,8 +344,18 @@ class TriMul:
         tri_mul_layer_backward(self.h, direction, z, mask, N, dout, dz, grads, ws, wsb, stream)
         return dz, grads
 
-    def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None):
-        tri_mul_block_accumulate(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream)
+    def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None,
+                         ws=None):
+        """One ring step; with `ws` (a uint8 device tensor of at least
+        block_workspace_size(view) bytes) through the repacking entry point."""
+        if ws is None:
+            tri_mul_block_accumulate(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream)
+        else:
+            tri_mul_block_accumulate_ws(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, ws,
+                                        ws.numel() * ws.element_size(), stream)
+
+    def block_workspace_size(self, view):
+        return tri_mul_block_workspace_size(self.h, view)
 
 
 # ------------------------------------------------------ panel layout views

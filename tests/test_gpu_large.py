@@ -104,13 +104,15 @@ def test_config5_tile_of_8x8_grid_n30000():
 
 
 @pytest.mark.parametrize("direction", DIRS)
-@pytest.mark.parametrize("N,g", [(1024, 2), (1024, 4), (1000, 4)])
-def test_block_decomposition_matches_full(direction, N, g):
+@pytest.mark.parametrize("N,g,use_ws", [(1024, 2, False), (1024, 4, False), (1000, 4, False), (1024, 2, True),
+                                        (1000, 4, True)])
+def test_block_decomposition_matches_full(direction, N, g, use_ws):
     """The one-GPU stand-in for the paper's ring: split the full problem into
     a g x g grid of tiles, run each tile as g block_accumulate calls (one per
-    k-panel, as in the Cannon ring) from the same projected panels, and compare
-    with the single-call contraction and update."""
-    say(f"block == full: N={N} g={g} {direction}")
+    k-panel, as in the Cannon ring; with use_ws through the repacking entry
+    point) from the same projected panels, and compare with the single-call
+    contraction and update."""
+    say(f"block == full: N={N} g={g} {direction} ws={use_ws}")
     layer, W = make_layer("bf16")
     z = synth.pair_tensor(N, dtype="bf16", device="cuda")
     mask = synth.random_mask(N, 0.9, sub=g).cuda()
@@ -125,6 +127,10 @@ def test_block_decomposition_matches_full(direction, N, g):
     bsz = N // g
     ld = (bsz + 7) // 8 * 8
     out_blk = torch.zeros_like(out_full)
+    ws = None
+    if use_ws:
+        n = layer.block_workspace_size(T.BlockView(N, 0, 0, bsz, bsz, 0, bsz, ld, ld, 0, g))
+        ws = torch.empty(n, dtype=torch.uint8, device="cuda")
     for r in range(g):
         for c in range(g):
             r0, c0 = r * bsz, c * bsz
@@ -138,7 +144,7 @@ def test_block_decomposition_matches_full(direction, N, g):
                 ap[:, :, :bsz] = A[:, r0:r0 + bsz, k0:k0 + bsz]
                 bp[:, :, :bsz] = B[:, c0:c0 + bsz, k0:k0 + bsz]
                 v = T.BlockView(N, r0, c0, bsz, bsz, k0, bsz, ld, ld, p, g)
-                layer.block_accumulate(v, ap, bp, acc, mask, z_tile, o_tile)
+                layer.block_accumulate(v, ap, bp, acc, mask, z_tile, o_tile, ws=ws)
             mx, rel = errors(host(acc), host(C_full[:, r0:r0 + bsz, c0:c0 + bsz]))
             assert rel <= 1e-5, (r, c, rel)
             out_blk[r0:r0 + bsz, c0:c0 + bsz] = o_tile

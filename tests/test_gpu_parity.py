@@ -33,12 +33,13 @@ def test_contract_exact_on_integers(dtype, N):
     np.testing.assert_array_equal(host(T.result_to_dense(C, N)).transpose(1, 2, 0), ref)
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_block_accumulate_kmask_exact(dtype):
+@pytest.mark.parametrize("dtype,use_ws", [("bf16", False), ("bf16", True), ("f32", False), ("f32", True)])
+def test_block_accumulate_kmask_exact(dtype, use_ws):
     """Two k-panels with a token mask over k, ragged tile (300 x 200) and
     panel lengths (130, 77) with padded row strides: overwrite on the first
-    panel, accumulate on the second, exact on integer data."""
-    say(f"block accumulate exact dtype={dtype}")
+    panel, accumulate on the second, exact on integer data; both entry
+    points (with use_ws the panels are repacked into the workspace)."""
+    say(f"block accumulate exact dtype={dtype} ws={use_ws}")
     layer, W = make_layer(dtype)
     rows, cols, n_total = 300, 200, 1000
     g = torch.Generator().manual_seed(7)
@@ -57,14 +58,38 @@ def test_block_accumulate_kmask_exact(dtype):
         aps.append(ap[:, :, :klen])
         bps.append(bp[:, :, :klen])
         v = T.BlockView(n_total, 700, 10, rows, cols, k0, klen, ld, ld, idx, 3)
-        layer.block_accumulate(v, ap.cuda(), bp.cuda(), acc, mask_d)
+        ws = None
+        if use_ws:   # a fresh workspace full of garbage for every panel
+            ws = torch.full((max(layer.block_workspace_size(v), 1),), 0xff, dtype=torch.uint8, device="cuda")
+        layer.block_accumulate(v, ap.cuda(), bp.cuda(), acc, mask_d, ws=ws)
     torch.cuda.synchronize()
     ref = oracle.block_contract([host(a) for a in aps], [host(b) for b in bps],
                                 [host(mask[k0:k0 + kl]) for k0, kl in ks])
     np.testing.assert_array_equal(host(acc).transpose(1, 2, 0), ref)
 
 
-def test_block_accumulate_no_mask_ignores_padding():
+def test_block_accumulate_ws_errors():
+    """The workspace entry point rejects a short or misaligned workspace
+    before launching anything."""
+    layer, _ = make_layer("bf16")
+    rows, cols, klen, ld = 64, 40, 50, 56
+    ap = torch.zeros((128, rows, ld), dtype=torch.bfloat16, device="cuda")
+    bp = torch.zeros((128, cols, ld), dtype=torch.bfloat16, device="cuda")
+    acc = torch.zeros((128, rows, cols), device="cuda")
+    v = T.BlockView(200, 0, 0, rows, cols, 0, klen, ld, ld, 0, 2)
+    need = layer.block_workspace_size(v)
+    assert need == 128 * 1 * 2 * 16384 * 2        # one 256-row tile and two k-steps per operand
+    ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(T.TriMulError) as e:
+        T.tri_mul_block_accumulate_ws(layer.h, v, ap, bp, acc, None, None, None, ws, need - 1)
+    assert e.value.code == T.TRI_MUL_ENOMEM
+    with pytest.raises(T.TriMulError) as e:
+        T.tri_mul_block_accumulate_ws(layer.h, v, ap, bp, acc, None, None, None, ws[16:], need)
+    assert e.value.code == T.TRI_MUL_EINVAL
+
+
+@pytest.mark.parametrize("use_ws", [False, True])
+def test_block_accumulate_no_mask_ignores_padding(use_ws):
     """Without a token mask the contraction must still ignore the padding
     columns past klen of row-major panels (NaN and huge values here), in the
     last, ragged k-step that loads them; three panels, one shorter than a
@@ -85,7 +110,10 @@ def test_block_accumulate_no_mask_ignores_padding():
         aps.append(ap[:, :, :klen])
         bps.append(bp[:, :, :klen])
         v = T.BlockView(n_total, 100, 300, rows, cols, k0, klen, ld, ld, idx, len(ks) + 1)   # no epilogue
-        layer.block_accumulate(v, ap.cuda(), bp.cuda(), acc, None)
+        ws = None
+        if use_ws:
+            ws = torch.full((layer.block_workspace_size(v),), 0xff, dtype=torch.uint8, device="cuda")
+        layer.block_accumulate(v, ap.cuda(), bp.cuda(), acc, None, ws=ws)
     torch.cuda.synchronize()
     ref = oracle.block_contract([host(a) for a in aps], [host(b) for b in bps], [np.ones(kl) for _, kl in ks])
     np.testing.assert_array_equal(host(acc).transpose(1, 2, 0), ref)
