@@ -278,21 +278,36 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         const int64_t jblocks = (N + kResJ - 1) / kResJ;
         float* Cb = CBLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0) : C + ch * sC + (int64_t)row0 * ldc + col0;
         const int64_t row_step = CBLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
+        // One 32 x 32 block at a time.  Accumulating, the block's 16 loads
+        // go out together (a lane outside C reads C[0] instead) and are
+        // waited for once, before its 16 guarded stores; element by element
+        // the compiler would wait for every load.
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < 4; ++j) {
+                float* pb = Cb + (CBLOCKED ? (int64_t)j * nchan * kResJ : j * 32);   // column block j
+                const bool colok = full || col0 + j * 32 < N;
+                float v[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) v[r] = acc[i][j][r];
+                if (accumulate) {
+                    float old[16];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
+                        const bool ok = colok && (full || row0 + dr < M);
+                        old[r] = *(ok ? pb + (int64_t)dr * row_step : C);
+                    }
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) v[r] += old[r];
+                }
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int dr = i * 32 + 8 * (r >> 2) + (r & 3);
-                    // column block j*32 of a blocked C is (j * nchan * 32) floats further on
-                    float* p = Cb + (int64_t)dr * row_step + (CBLOCKED ? (int64_t)j * nchan * kResJ : j * 32);
-                    if (full || (row0 + dr < M && col0 + j * 32 < N)) {
-                        float v = acc[i][j][r];
-                        if (accumulate) v += *p;
-                        *p = v;
-                    }
+                    if (colok && (full || row0 + dr < M)) pb[(int64_t)dr * row_step] = v[r];
                 }
+            }
     }
 }
 
