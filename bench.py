@@ -79,15 +79,25 @@ def cpu_baseline(N, sample):
 
 
 def gpu_state():
-    """Current clocks and socket power of GPU 0 as rocm-smi reports them (a
-    child process; None if the tool is missing or fails)."""
-    import subprocess
+    """Current graphics and memory clocks (and socket power, where exposed) of
+    the first GPU, read from the amdgpu sysfs files -- plain file reads, no
+    child process.  None where the files are missing or unreadable."""
+    import glob
+
+    def current(path):   # the DPM level marked '*', e.g. '1: 2100Mhz *'
+        for line in open(path):
+            if line.rstrip().endswith("*"):
+                return line.split(":", 1)[1].replace("*", "").strip()
+        return None
+
     try:
-        r = subprocess.run(["rocm-smi", "-d", "0", "-c", "-P", "--json"], capture_output=True, text=True, timeout=30)
-        card = next(iter(json.loads(r.stdout).values()))
-        keep = ("sclk", "mclk", "fclk", "socclk", "power")
-        return {k: v for k, v in card.items() if any(w in k.lower() for w in keep)}
-    except Exception:
+        dev = sorted(d for d in glob.glob("/sys/class/drm/card*/device") if os.path.exists(d + "/pp_dpm_sclk"))[0]
+        out = {"sclk": current(dev + "/pp_dpm_sclk"), "mclk": current(dev + "/pp_dpm_mclk")}
+        pw = glob.glob(dev + "/hwmon/hwmon*/power1_average") + glob.glob(dev + "/hwmon/hwmon*/power1_input")
+        if pw:
+            out["power_W"] = round(int(open(pw[0]).read()) / 1e6, 1)
+        return out
+    except (IndexError, OSError, ValueError):
         return None
 
 
