@@ -262,7 +262,7 @@ def main():
     torch.cuda.synchronize()
     full_ms = f0.elapsed_time(f1) / 2
 
-    bwd_ms = lbwd_ms = opm_ms = ta_ms = tile_ms = None
+    bwd_ms = lbwd_ms = sbwd_ms = opm_ms = ta_ms = tile_ms = None
     ta_scores = 2048 * 4 * 2048 * 2048
     opm_flops = 2 * 4096 * (1024 * 32) ** 2
     if not args.no_extras:
@@ -297,8 +297,19 @@ def main():
         l1.record(stream)
         torch.cuda.synchronize()
         lbwd_ms = l0.elapsed_time(l1) / 2
-        del dout, dz, grads, lws
         print(f"[bench] layer backward {lbwd_ms:.3f} ms", file=sys.stderr, flush=True)
+        # the same backward from the forward's saved A, B, C (training keeps them)
+        T.tri_mul_project(h, z, mask, N, T.TRI_MUL_OUTGOING, A, B, stream)
+        T.tri_mul_contract(h, A, B, N, C, stream)
+        T.tri_mul_layer_backward_saved(h, "outgoing", z, mask, N, A, B, C, dout, dz, grads, lws, lws_n, stream)
+        l0.record(stream)
+        for _ in range(2):
+            T.tri_mul_layer_backward_saved(h, "outgoing", z, mask, N, A, B, C, dout, dz, grads, lws, lws_n, stream)
+        l1.record(stream)
+        torch.cuda.synchronize()
+        sbwd_ms = l0.elapsed_time(l1) / 2
+        del dout, dz, grads, lws
+        print(f"[bench] layer backward from saved forward {sbwd_ms:.3f} ms", file=sys.stderr, flush=True)
 
         # the outer product mean (a second op of the same ring archetype), outside
         # the timed region: S = 4096 sequences, N = 1024 tokens, D = 32, c_z = 128
@@ -381,6 +392,7 @@ def main():
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
     bw = perf.backward_layer_work(N)
+    bws_ = perf.backward_layer_work(N, recompute=False)
     opm_proj_flops = 2 * 1024 * 1024 * 1024 * 128
     tile_flops = 2.0 * 3750 * 3750 * 30000 * 128
 
@@ -443,6 +455,13 @@ def main():
                       "what": "tile (7,7) of an 8x8 grid at N=30000: 8 tri_mul_block_accumulate_ws ring steps (3750x3750 "
                               "outputs, 3750-token k-panels, 128 channels; 108.0 TFLOP contraction) with the "
                               "epilogue on the last step; fp32 accumulator and output; not part of ms_per_step"},
+        "backward_layer_saved": None if sbwd_ms is None else {"ms": round(sbwd_ms, 4),
+                           "roofline": {"bound": "mfma + hbm", "floor_ms": round(bws_["floor_ms"], 3),
+                                        "frac": round(bws_["floor_ms"] / sbwd_ms, 4),
+                                        "basis": "floor = two N^3 bf16 products at MFMA peak + the per-pair "
+                                                 "kernels' algorithmic bytes at HBM peak; frac = floor / ms"},
+                           "what": "tri_mul_outgoing_backward_saved: the layer backward from the forward's saved "
+                                   "A, B panels and C (no recomputation); not part of ms_per_step"},
         "backward_layer": None if lbwd_ms is None else {"ms": round(lbwd_ms, 4),
                            "roofline": {"bound": "mfma + hbm", "floor_ms": round(bw["floor_ms"], 3),
                                         "frac": round(bw["floor_ms"] / lbwd_ms, 4),

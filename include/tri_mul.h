@@ -278,6 +278,25 @@ int tri_mul_outgoing_backward(tri_mul_handle_t h, const void* z, const uint8_t* 
 int tri_mul_incoming_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
                               void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream);
 
+/* The same backward from the forward's saved state instead of recomputing
+ * it: a_panels, b_panels (panel layout, as tri_mul_project wrote them for
+ * this z, mask and direction) and c_result (result layout, as
+ * tri_mul_contract wrote it from them) replace the recomputed projections
+ * and contraction; the full calls tri_mul_outgoing / tri_mul_incoming leave
+ * exactly these in their workspace, at byte offsets 0, P and 2 P with
+ * P = tri_mul_panel_size rounded up to a multiple of 256.  Results are
+ * identical to tri_mul_outgoing_backward / tri_mul_incoming_backward on the
+ * same inputs; the saved tensors are only read and must not alias ws.  Same
+ * workspace size, alignment and errors (16-byte aligned saved pointers). */
+int tri_mul_outgoing_backward_saved(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                                    const void* a_panels, const void* b_panels, const float* c_result,
+                                    const void* dout, void* dz, const tri_mul_grads_t* grads, void* ws,
+                                    size_t ws_bytes, void* stream);
+int tri_mul_incoming_backward_saved(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                                    const void* a_panels, const void* b_panels, const float* c_result,
+                                    const void* dout, void* dz, const tri_mul_grads_t* grads, void* ws,
+                                    size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -171,8 +171,13 @@ BwdLayout bwd_layout(tri_mul_handle_t h, int64_t N) {
 }
 
 int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout, void* dz,
-                 const tri_mul_grads_t* g, void* ws, size_t ws_bytes, void* stream, int incoming) {
+                 const tri_mul_grads_t* g, void* ws, size_t ws_bytes, void* stream, int incoming,
+                 const void* sA = nullptr, const void* sB = nullptr, const float* sC = nullptr) {
     if (int rc = check_handle(h)) return rc;
+    const bool saved = sA || sB || sC;
+    if (saved && (!sA || !sB || !sC)) return fail(TRI_MUL_EINVAL, "null saved forward tensor");
+    if (saved && (!aligned16(sA) || !aligned16(sB) || !aligned16(sC)))
+        return fail(TRI_MUL_EINVAL, "saved forward tensors must be 16-byte aligned");
     if (int rc = check_n(N)) return rc;
     if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "the layer backward supports the bf16 storage path only");
     if (!z || !dout || !dz || !g || !ws) return fail(TRI_MUL_EINVAL, "null pointer argument");
@@ -185,8 +190,14 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     if (ws_bytes < L.total) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes < %zu needed for N = %lld", ws_bytes, L.total, (long long)N);
     char* p = static_cast<char*>(ws);
     auto take = [&](size_t n) { char* q = p; p += n; return q; };
-    void *A = take(L.panel), *B = take(L.panel), *dCp = take(L.panel), *dCt = take(L.panel), *At = take(L.panel), *Bt = take(L.panel);
-    float* C = reinterpret_cast<float*>(take(L.result));
+    const void *A = take(L.panel), *B = take(L.panel);
+    void *dCp = take(L.panel), *dCt = take(L.panel), *At = take(L.panel), *Bt = take(L.panel);
+    const float* C = reinterpret_cast<float*>(take(L.result));
+    if (saved) {   // the forward's own A, B, C (their workspace regions go unused)
+        A = sA;
+        B = sB;
+        C = sC;
+    }
     float* dA = reinterpret_cast<float*>(take(L.result));
     float* dB = reinterpret_cast<float*>(take(L.result));
     float* dxg = reinterpret_cast<float*>(take(L.dxg));
@@ -200,8 +211,13 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int cus = h->w.cus, G = L.grid_pair, GW = L.grid_w;
 
-    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, A, B, s);
-    if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    hipError_t e = hipSuccess;
+    if (!saved) {   // recompute the forward's operands and contraction
+        e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, const_cast<void*>(A), const_cast<void*>(B), s);
+        if (e == hipSuccess)
+            e = trimul::launch_contract(h->dtype, 1, A, B, const_cast<float*>(C), N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0,
+                                        nullptr, cus, s);
+    }
     if (e == hipSuccess) e = trimul::launch_epilogue_backward(h->out_dtype, h->w, C, z, mask, dout, N, dCp, dxg, bb, peb, G, s);
     if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, dCp, dCt, N, cus, s);
     if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, A, At, N, cus, s);
@@ -594,6 +610,22 @@ int tri_mul_outgoing_backward(tri_mul_handle_t h, const void* z, const uint8_t* 
 int tri_mul_incoming_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, const void* dout,
                               void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream) {
     return run_backward(h, z, mask, N, dout, dz, grads, ws, ws_bytes, stream, 1);
+}
+
+int tri_mul_outgoing_backward_saved(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                                    const void* a_panels, const void* b_panels, const float* c_result,
+                                    const void* dout, void* dz, const tri_mul_grads_t* grads, void* ws,
+                                    size_t ws_bytes, void* stream) {
+    if (!a_panels || !b_panels || !c_result) return fail(TRI_MUL_EINVAL, "null saved forward tensor");
+    return run_backward(h, z, mask, N, dout, dz, grads, ws, ws_bytes, stream, 0, a_panels, b_panels, c_result);
+}
+
+int tri_mul_incoming_backward_saved(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                                    const void* a_panels, const void* b_panels, const float* c_result,
+                                    const void* dout, void* dz, const tri_mul_grads_t* grads, void* ws,
+                                    size_t ws_bytes, void* stream) {
+    if (!a_panels || !b_panels || !c_result) return fail(TRI_MUL_EINVAL, "null saved forward tensor");
+    return run_backward(h, z, mask, N, dout, dz, grads, ws, ws_bytes, stream, 1, a_panels, b_panels, c_result);
 }
 
 }  // extern "C"

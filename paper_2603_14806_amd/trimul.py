@@ -84,6 +84,10 @@ SIGNATURES = {
                                                  ctypes.c_size_t, _vp]),
     "tri_mul_incoming_backward": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.POINTER(Grads), _vp,
                                                  ctypes.c_size_t, _vp]),
+    "tri_mul_outgoing_backward_saved": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                                        ctypes.POINTER(Grads), _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_incoming_backward_saved": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                                        ctypes.POINTER(Grads), _vp, ctypes.c_size_t, _vp]),
     "opm_init": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.POINTER(OpmParams), _vp]),
     "opm_destroy": (ctypes.c_int, [_vp]),
     "opm_accumulator_size": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
@@ -236,6 +240,16 @@ def tri_mul_layer_backward(h, direction, z, mask, N, dout, dz, grads, ws, ws_byt
     _check(f(h, _ptr(z), _ptr(mask), N, _ptr(dout), _ptr(dz), ctypes.byref(g), _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def tri_mul_layer_backward_saved(h, direction, z, mask, N, a_panels, b_panels, c_result, dout, dz, grads, ws,
+                                 ws_bytes, stream=None):
+    """The layer backward from the forward's saved A, B panels and C result."""
+    g = Grads(*[_ptr(grads[n]) for n in WEIGHT_FIELDS])
+    f = (lib().tri_mul_incoming_backward_saved if direction in (TRI_MUL_INCOMING, "incoming")
+         else lib().tri_mul_outgoing_backward_saved)
+    _check(f(h, _ptr(z), _ptr(mask), N, _ptr(a_panels), _ptr(b_panels), _ptr(c_result), _ptr(dout), _ptr(dz),
+             ctypes.byref(g), _ptr(ws), ws_bytes, _stream(stream)))
+
+
 # ---------------------------------------------------------------- wrapper
 
 class TriMul:
@@ -326,9 +340,11 @@ class TriMul:
         tri_mul_contract_backward(self.h, dC, A, B, N, dA, dB, ws, wsb, stream)
         return dA, dB
 
-    def backward(self, z, dout, mask=None, direction="outgoing", stream=None):
+    def backward(self, z, dout, mask=None, direction="outgoing", stream=None, saved=None):
         """Gradients of sum(out * dout) for the update of z: returns (dz,
-        grads) with grads a dict of float32 tensors shaped like the weights."""
+        grads) with grads a dict of float32 tensors shaped like the weights.
+        saved = (A, B, C) from project / contract of the same z, mask and
+        direction skips the recomputation of the forward."""
         N = z.shape[0]
         cz = 128
         if tuple(z.shape) != (N, N, cz) or tuple(dout.shape) != (N, N, cz):
@@ -341,7 +357,10 @@ class TriMul:
         dz = torch.empty_like(z)
         wsb = tri_mul_backward_workspace_size(self.h, N)
         ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
-        tri_mul_layer_backward(self.h, direction, z, mask, N, dout, dz, grads, ws, wsb, stream)
+        if saved is None:
+            tri_mul_layer_backward(self.h, direction, z, mask, N, dout, dz, grads, ws, wsb, stream)
+        else:
+            tri_mul_layer_backward_saved(self.h, direction, z, mask, N, *saved, dout, dz, grads, ws, wsb, stream)
         return dz, grads
 
     def block_accumulate(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None, stream=None,

@@ -14,6 +14,7 @@ import torch
 
 import oracle
 from paper_2603_14806_amd import synth
+from paper_2603_14806_amd import trimul as T
 from tests.gpu_util import errors, host, make_layer, say
 
 pytestmark = pytest.mark.gpu
@@ -73,3 +74,35 @@ def test_layer_backward_n4096_runs_deterministic():
         assert torch.equal(g1[k], g2[k]), k
     assert (dz1[-40:] == 0).all() and (dz1[:, -40:] == 0).all()
     assert torch.isfinite(dz1.float()).all()
+
+
+@pytest.mark.parametrize("direction", ["outgoing", "incoming"])
+def test_layer_backward_from_saved_forward_is_identical(direction):
+    """The saved-state entry points skip the recomputation of the forward:
+    from the stage calls' A, B, C, and from the regions the full call leaves
+    in its workspace (offsets 0, P, 2 P), the results equal the recomputing
+    backward bit for bit."""
+    N = 300
+    say(f"layer backward from saved forward {direction} N={N}")
+    layer, _ = make_layer("bf16", "f32", affine=True, seed=3)
+    z = synth.pair_tensor(N, dtype="bf16", seed=3, device="cuda")
+    mask = torch.ones(N, dtype=torch.uint8, device="cuda")
+    mask[[5, 77, 299]] = 0
+    g = torch.Generator(device="cuda").manual_seed(9)
+    dout = torch.randn((N, N, 128), generator=g, device="cuda")
+    dz0, g0 = layer.backward(z, dout, mask, direction)
+    A, B = layer.project(z, mask, direction)
+    C = layer.contract(A, B, N)
+    dz1, g1 = layer.backward(z, dout, mask, direction, saved=(A, B, C))
+    layer(z, mask, direction)                                   # the full call, workspace kept by the wrapper
+    ws, _ = layer.workspace(N)
+    P = -(-T.tri_mul_panel_size(layer.h, N) // 256) * 256
+    nA = T.tri_mul_panel_size(layer.h, N)
+    wA, wB = ws[:nA].view(torch.bfloat16), ws[P:P + nA].view(torch.bfloat16)
+    wC = ws[2 * P:2 * P + C.numel() * 4].view(torch.float32)
+    dz2, g2 = layer.backward(z, dout, mask, direction, saved=(wA, wB, wC))
+    torch.cuda.synchronize()
+    assert torch.equal(dz0, dz1) and torch.equal(dz0, dz2)
+    for k in g0:
+        assert torch.equal(g0[k], g1[k]), k
+        assert torch.equal(g0[k], g2[k]), k
