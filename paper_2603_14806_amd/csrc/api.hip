@@ -150,9 +150,10 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
 // layout), dx_g [N*N][c_z] fp32, nine unit-block tensors, and the partial
 // sums of the weight-gradient reductions.
 struct BwdLayout {
-    size_t panel, result, dxg, block, part_eb, part_pb, part_w, total;
+    size_t panel, result, dxg, block, part_eb, part_pb, part_w, part_w4, total;
     int grid_pair;   // per-pair stages: one 512-thread work-group per compute unit
     int grid_w;      // weight-gradient sums: two 256-thread work-groups per compute unit
+    int grid_w4;     // the four sums over the x blocks: one 512-thread work-group per compute unit
 };
 BwdLayout bwd_layout(tri_mul_handle_t h, int64_t N) {
     BwdLayout L;
@@ -166,7 +167,9 @@ BwdLayout bwd_layout(tri_mul_handle_t h, int64_t N) {
     L.part_eb = round256((size_t)L.grid_pair * 2 * 128 * 4);
     L.part_pb = round256((size_t)L.grid_pair * 2 * 128 * 4);
     L.part_w = round256((size_t)L.grid_w * 128 * 128 * 4);
-    L.total = 6 * L.panel + 3 * L.result + L.dxg + 9 * L.block + L.part_eb + L.part_pb + L.part_w;
+    L.grid_w4 = trimul::backward_grid(units, h->w.cus, 1);
+    L.part_w4 = round256((size_t)4 * L.grid_w4 * 128 * 128 * 4);
+    L.total = 6 * L.panel + 3 * L.result + L.dxg + 9 * L.block + L.part_eb + L.part_pb + L.part_w + L.part_w4;
     return L;
 }
 
@@ -208,8 +211,9 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     float* peb = reinterpret_cast<float*>(take(L.part_eb));
     float* ppb = reinterpret_cast<float*>(take(L.part_pb));
     float* pw = reinterpret_cast<float*>(take(L.part_w));
+    float* pw4 = reinterpret_cast<float*>(take(L.part_w4));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int cus = h->w.cus, G = L.grid_pair, GW = L.grid_w;
+    const int cus = h->w.cus, G = L.grid_pair, GW = L.grid_w, GW4 = L.grid_w4;
 
     hipError_t e = hipSuccess;
     if (!saved) {   // recompute the forward's operands and contraction
@@ -225,13 +229,18 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, dCp, Bt, dA, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
     if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, dCt, At, dB, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
     if (e == hipSuccess) e = trimul::launch_projection_backward(h->w, z, mask, N, incoming, dA, dB, dxg, dz, bb, ppb, G, s);
-    const struct { const bf16_t* u; const bf16_t* v; float* out; } wg[] = {
-        {bb.du, bb.y, g->w_o}, {bb.dgg, bb.xe, g->w_g}, {bb.dpa, bb.xp, g->w_a},
-        {bb.dga, bb.xp, g->w_ga}, {bb.dpb, bb.xp, g->w_b}, {bb.dgb, bb.xp, g->w_gb}};
+    const struct { const bf16_t* u; const bf16_t* v; float* out; } wg[] = {{bb.du, bb.y, g->w_o}, {bb.dgg, bb.xe, g->w_g}};
     for (const auto& q : wg) {
         if (e == hipSuccess) e = trimul::launch_wgrad(q.u, q.v, N, pw, GW, s);
         if (e == hipSuccess) e = trimul::launch_sum_parts(pw, GW, 128 * 128, 128 * 128, q.out, s);
     }
+    // the four projection weights share the x blocks: one pass over them
+    const bf16_t* const u4[4] = {bb.dpa, bb.dga, bb.dpb, bb.dgb};
+    float* const out4[4] = {g->w_a, g->w_ga, g->w_b, g->w_gb};
+    if (e == hipSuccess) e = trimul::launch_wgrad4(u4, bb.xp, N, pw4, GW4, s);
+    for (int o = 0; o < 4; ++o)
+        if (e == hipSuccess)
+            e = trimul::launch_sum_parts(pw4 + (size_t)o * GW4 * 128 * 128, GW4, 128 * 128, 128 * 128, out4[o], s);
     if (e == hipSuccess) e = trimul::launch_sum_parts(peb, G, 256, 128, g->ln_out_w, s);
     if (e == hipSuccess) e = trimul::launch_sum_parts(peb + 128, G, 256, 128, g->ln_out_b, s);
     if (e == hipSuccess) e = trimul::launch_sum_parts(ppb, G, 256, 128, g->ln_in_w, s);

@@ -823,6 +823,68 @@ __global__ __launch_bounds__(256) void k_wgrad(const bf16_t* __restrict__ U, con
 }
 
 // out[i] = sum over g < parts of in[g * stride + i], in that order.
+// Four weight gradients that share their second operand (W_a, W_ga, W_b,
+// W_gb all multiply the x blocks): sum over units of U_o V^T for o = 0..3,
+// reading each unit's V block once instead of four times.  8 waves: wave w
+// owns rows 32 (w % 4) .. + 31 of outputs 2 (w / 4) and 2 (w / 4) + 1
+// (two 32 x 128 accumulators); the next unit's operands are loaded while
+// the current one is multiplied.  Partials: [o][grid][128][128].
+struct Wgrad4Args {
+    const bf16_t* u[4];
+};
+
+__global__ __launch_bounds__(512) void k_wgrad4(Wgrad4Args a, const bf16_t* __restrict__ V, int64_t units,
+                                                float* __restrict__ partial) {
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int rl = lane & 31, hi = lane >> 5;
+    const int rb = 32 * (w & 3), o0 = 2 * (w >> 2);
+    const bf16_t* U0 = a.u[o0];
+    const bf16_t* U1 = a.u[o0 + 1];
+    f32x16_t acc[2][4];
+#pragma unroll
+    for (int o = 0; o < 2; ++o)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[o][j][r] = 0.f;
+    struct Ops { bf16x8_t a[2][2], b[4][2]; };
+    auto load = [&](int64_t u, Ops& p) {
+        const int64_t uu = u < units ? u : units - 1;   // past the end: a repeat, never multiplied
+        const int64_t base = uu * (kCh * kQ);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int64_t ra = base + (rb + rl) * kQ + 16 * ks + 8 * hi;
+            p.a[0][ks] = *reinterpret_cast<const bf16x8_t*>(U0 + ra);
+            p.a[1][ks] = *reinterpret_cast<const bf16x8_t*>(U1 + ra);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                p.b[j][ks] = *reinterpret_cast<const bf16x8_t*>(V + base + (32 * j + rl) * kQ + 16 * ks + 8 * hi);
+        }
+    };
+    Ops cur, nxt;
+    load(blockIdx.x, cur);
+    for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
+        load(u + gridDim.x, nxt);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int o = 0; o < 2; ++o)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[o][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[o][ks], cur.b[j][ks], acc[o][j], 0, 0, 0);
+        cur = nxt;
+    }
+    // lane holds column 32 j + rl; register r holds row rb + 8 (r / 4) + 4 hi + r % 4
+#pragma unroll
+    for (int o = 0; o < 2; ++o) {
+        float* pw = partial + ((int64_t)(o0 + o) * gridDim.x + blockIdx.x) * (kCh * kCh);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) pw[(rb + 8 * (r >> 2) + 4 * hi + (r & 3)) * kCh + 32 * j + rl] = acc[o][j][r];
+    }
+}
+
 __global__ __launch_bounds__(256) void k_sum_parts(const float* __restrict__ in, int parts, int64_t stride, int n,
                                                     float* __restrict__ out) {
     const int i = blockIdx.x * 256 + threadIdx.x;
@@ -899,6 +961,14 @@ hipError_t launch_projection_backward(const DeviceWeights& w, const void* z, con
 hipError_t launch_wgrad(const bf16_t* U, const bf16_t* V, int64_t N, float* partial, int grid, hipStream_t s) {
     const int64_t units = N * ((N + 31) / 32);
     hipLaunchKernelGGL(k_wgrad, dim3(grid), dim3(256), 0, s, U, V, units, partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_wgrad4(const bf16_t* const U[4], const bf16_t* V, int64_t N, float* partial, int grid,
+                         hipStream_t s) {
+    const int64_t units = N * ((N + 31) / 32);
+    Wgrad4Args a{{U[0], U[1], U[2], U[3]}};
+    hipLaunchKernelGGL(k_wgrad4, dim3(grid), dim3(512), 0, s, a, V, units, partial);
     return hipGetLastError();
 }
 

@@ -93,6 +93,9 @@ hipError_t launch_projection_backward(const DeviceWeights& w, const void* z, con
                                       int incoming, const float* dA, const float* dB, const float* dxg, void* dz,
                                       const BackwardBlocks& bb, float* partial, int grid, hipStream_t s);
 hipError_t launch_wgrad(const bf16_t* U, const bf16_t* V, int64_t N, float* partial, int grid, hipStream_t s);
+// Four weight gradients sharing V: partial[o][grid][128][128] for U[o] V^T, o = 0..3.
+hipError_t launch_wgrad4(const bf16_t* const U[4], const bf16_t* V, int64_t N, float* partial, int grid,
+                         hipStream_t s);
 hipError_t launch_sum_parts(const float* in, int parts, int64_t stride, int n, float* out, hipStream_t s);
 
 // Outer product mean (opm.hip).  Pack: tokens [tok0, tok0 + ntok) and
