@@ -229,7 +229,9 @@ int tri_mul_epilogue(tri_mul_handle_t h, const float* c_in, const void* z,
  * caller maps dA back to a by the same transposition.
  *
  * tri_mul_contract_backward_workspace_size: bytes of device workspace for N
- * tokens (four operands in the panel layout, 256-byte aligned each).
+ * tokens: one operand in the panel layout (dC) in the bf16 path, which reads
+ * the other operands transposed in place; four (dC and the transposes of dC,
+ * A and B) in the fp32 path; 256-byte aligned each.
  * *bytes is a HOST pointer. */
 int tri_mul_contract_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
 

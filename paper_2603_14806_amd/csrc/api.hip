@@ -169,7 +169,7 @@ BwdLayout bwd_layout(tri_mul_handle_t h, int64_t N) {
     L.part_w = round256((size_t)L.grid_w * 128 * 128 * 4);
     L.grid_w4 = trimul::backward_grid(units, h->w.cus, 1);
     L.part_w4 = round256((size_t)4 * L.grid_w4 * 128 * 128 * 4);
-    L.total = 6 * L.panel + 3 * L.result + L.dxg + 9 * L.block + L.part_eb + L.part_pb + L.part_w + L.part_w4;
+    L.total = 3 * L.panel + 3 * L.result + L.dxg + 9 * L.block + L.part_eb + L.part_pb + L.part_w + L.part_w4;
     return L;
 }
 
@@ -194,7 +194,7 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     char* p = static_cast<char*>(ws);
     auto take = [&](size_t n) { char* q = p; p += n; return q; };
     const void *A = take(L.panel), *B = take(L.panel);
-    void *dCp = take(L.panel), *dCt = take(L.panel), *At = take(L.panel), *Bt = take(L.panel);
+    void* dCp = take(L.panel);
     const float* C = reinterpret_cast<float*>(take(L.result));
     if (saved) {   // the forward's own A, B, C (their workspace regions go unused)
         A = sA;
@@ -223,11 +223,9 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
                                         nullptr, cus, s);
     }
     if (e == hipSuccess) e = trimul::launch_epilogue_backward(h->out_dtype, h->w, C, z, mask, dout, N, dCp, dxg, bb, peb, G, s);
-    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, dCp, dCt, N, cus, s);
-    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, A, At, N, cus, s);
-    if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, B, Bt, N, cus, s);
-    if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, dCp, Bt, dA, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
-    if (e == hipSuccess) e = trimul::launch_contract(h->dtype, 1, dCt, At, dB, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    // dA = dC B and dB = dC^T A, reading B, dC and A transposed straight from their panels
+    if (e == hipSuccess) e = trimul::launch_contract_transposed(0, 1, dCp, B, dA, N, N, N, h->c, cus, s);
+    if (e == hipSuccess) e = trimul::launch_contract_transposed(1, 1, dCp, A, dB, N, N, N, h->c, cus, s);
     if (e == hipSuccess) e = trimul::launch_projection_backward(h->w, z, mask, N, incoming, dA, dB, dxg, dz, bb, ppb, G, s);
     const struct { const bf16_t* u; const bf16_t* v; float* out; } wg[] = {{bb.du, bb.y, g->w_o}, {bb.dgg, bb.xe, g->w_g}};
     for (const auto& q : wg) {
@@ -459,7 +457,8 @@ int tri_mul_contract_backward_workspace_size(tri_mul_handle_t h, int64_t N, size
     if (int rc = check_handle(h)) return rc;
     if (int rc = check_n(N)) return rc;
     if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
-    *bytes = 4 * round256(panel_bytes(N, h->c, h->dtype));
+    // bf16: dC as a panel; fp32 also the transposes of dC, A and B
+    *bytes = (h->dtype == TRI_MUL_BF16 ? 1 : 4) * round256(panel_bytes(N, h->c, h->dtype));
     return ok();
 }
 
@@ -477,12 +476,20 @@ int tri_mul_contract_backward(tri_mul_handle_t h, const float* dC, const void* a
     const size_t panel = round256(panel_bytes(N, h->c, h->dtype));
     char* base = static_cast<char*>(ws);
     void* dCp = base;               // dC as operand rows i, k = j
-    void* dCt = base + panel;       // dC^T: rows j, k = i
-    void* At = base + 2 * panel;    // A^T
-    void* Bt = base + 3 * panel;    // B^T
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int cus = h->w.cus;
     hipError_t e = trimul::launch_result_to_panel(h->dtype, dC, dCp, N, cus, s);
+    if (h->dtype == TRI_MUL_BF16) {
+        // dA[i][k] = sum_j dC[i][j] B[j][k];  dB[j][k] = sum_i dC[i][j] A[i][k]: the matrix
+        // cores read B, dC and A transposed from their panels
+        if (e == hipSuccess) e = trimul::launch_contract_transposed(0, 1, dCp, b_panels, dA, N, N, N, h->c, cus, s);
+        if (e == hipSuccess) e = trimul::launch_contract_transposed(1, 1, dCp, a_panels, dB, N, N, N, h->c, cus, s);
+        if (e != hipSuccess) return hip_fail(e, "backward contraction kernel launch");
+        return ok();
+    }
+    void* dCt = base + panel;       // dC^T: rows j, k = i
+    void* At = base + 2 * panel;    // A^T
+    void* Bt = base + 3 * panel;    // B^T
     if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, dCp, dCt, N, cus, s);
     if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, a_panels, At, N, cus, s);
     if (e == hipSuccess) e = trimul::launch_panel_transpose(h->dtype, b_panels, Bt, N, cus, s);

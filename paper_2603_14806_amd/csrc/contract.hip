@@ -36,6 +36,18 @@ constexpr int ROWB = BK * 2;                    // 64 bytes per row per stage
 constexpr int B_ST = BN * ROWB;                 // 16 KB
 constexpr int kLdsBytes = 160 * 1024;           // gfx950 LDS per work-group
 
+// Eight bf16 of an MFMA operand from a row-major [k][32] LDS block through
+// two ds_read_b64_tr_b16 (k values 0-3, then 4-7 from four rows further on).
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef short v8i16_t __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ bf16x8_t lds_read_tr8(const char* p) {
+    typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+    const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(p));
+    const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(p + 4 * ROWB));
+    const v8i16_t v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+
 // ------------------------------------------- bf16 MFMA, 8 + 4 specialised waves
 //
 // The contraction with the loads taken off the MFMA waves: 12 waves per
@@ -58,7 +70,21 @@ constexpr int kLdsBytes = 160 * 1024;           // gfx950 LDS per work-group
 // each loaded, before the barrier that publishes the stage: only steps that
 // hold such k pay, and the MFMA waves never mask.
 // LDS ring of 5 stages, swizzle and tile order as described above.
-template <bool BLOCKED, bool KMASK, bool CBLOCKED>
+//
+// Transposed operands (TA / TB, blocked only, no k-mask): the operand is
+// given as its transpose X in the panel layout, A[c][i][k] = X[c][k][i], so
+// the products of the backward, dC B and dC^T A, run without transposing
+// panels in memory.  A k-step of a 256-wide tile is then the 32 rows k of
+// eight 32-column blocks of X: eight contiguous 2 KB pieces, copied to LDS
+// as they are (block b of the tile at 2 KB b, 64 bytes per row k, no
+// swizzle).  The MFMA waves read such an operand with ds_read_b64_tr_b16:
+// lanes 16 g + 4 i + a (g < 4, i < 4, a < 4) address row 8 (g >> 1) + i,
+// columns 16 (g & 1) + 4 a .. + 3 of a block, and lane 16 g + 4 a + b receives
+// element b of the four chunks lanes 16 g + a, + 4, + 8, + 12 address, i.e.
+// column 16 (g & 1) + 4 a + b of rows 8 (g >> 1) .. + 3 -- the MFMA operand
+// layout, 4 of its 8 k values; a second read 4 rows further gives the rest.
+// A half-wave reads 256 contiguous bytes: no bank conflicts.
+template <bool BLOCKED, bool KMASK, bool CBLOCKED, bool TA = false, bool TB = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_per_eu(3, 3)))
 void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
                     int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB, int64_t sC, int tiles_m,
@@ -67,6 +93,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
     constexpr int A_ST = BM * ROWB, ST_BYTES = A_ST + B_ST;
     constexpr int STAGES = kLdsBytes / ST_BYTES;  // 5
     constexpr int LOADS = 8;                     // direct-to-LDS loads per loader wave per step
+    static_assert(!(TA || TB) || (BLOCKED && !KMASK), "transposed operands are blocked and unmasked");
     __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
 
     const int G = gridDim.x, wg = blockIdx.x;
@@ -101,17 +128,23 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         const int lw = wave - 8;
         const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
         const int rsa = BLOCKED ? BK : lda, rsb = BLOCKED ? BK : ldb;   // elements between rows
-        const uint32_t va = (uint32_t)(((lw * 64 + (lane >> 2)) * rsa + lkc * 8) * 2);
-        const uint32_t vb = (uint32_t)(((lw * 64 + (lane >> 2)) * rsb + lkc * 8) * 2);
+        const uint32_t va = TA ? (uint32_t)(lane * 16) : (uint32_t)(((lw * 64 + (lane >> 2)) * rsa + lkc * 8) * 2);
+        const uint32_t vb = TB ? (uint32_t)(lane * 16) : (uint32_t)(((lw * 64 + (lane >> 2)) * rsb + lkc * 8) * 2);
+        // transposed operand X: 32-column blocks per 256-row tile of X, and
+        // those tiles per channel (X has K rows)
+        const int xs_a = (M + 31) / 32, xs_b = (N + 31) / 32, xt = (K + 255) / 256;
         const uint32_t a_j = (uint32_t)(16 * rsa * 2), b_j = (uint32_t)(16 * rsb * 2);   // bytes per 16 rows
         const uint32_t a_k = BLOCKED ? (uint32_t)(BM * BK * 2) : (uint32_t)ROWB;       // bytes per k-step
         const uint32_t b_k = BLOCKED ? (uint32_t)(BN * BK * 2) : (uint32_t)ROWB;
-        int l_it = 0, l_kt = 0, l_stage = 0;
+        int l_it = 0, l_kt = 0, l_stage = 0, l_ch = 0, l_m0 = 0, l_n0 = 0;
         v4i_t ra = buffer_desc(A, 0u), rb = buffer_desc(B, 0u);
         const v4i_t rnone = buffer_desc(A, 0u);
         auto load_tile = [&]() {
             int ch, m0, n0;
             decode(l_it, ch, m0, n0);
+            l_ch = ch;
+            l_m0 = m0;
+            l_n0 = n0;
             if (BLOCKED) {
                 ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK),
                                  (uint32_t)(nk * BM * BK * 2));
@@ -122,14 +155,28 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
             }
         };
+        // Transposed operand: the descriptor covers the 256-row tile of X
+        // that holds step kt (rows past it, or blocks past the last column
+        // block, read as zero).
+        auto tr_desc = [&](const bf16_t* X, int xs, int kt) {
+            return buffer_desc(X + ((int64_t)l_ch * xt + (kt >> 3)) * xs * (256 * 32), (uint32_t)(xs * 256 * 32 * 2));
+        };
         auto issue_step = [&](bool live) {
             const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
+            const v4i_t rta = TA ? tr_desc(A, xs_a, l_kt) : ra, rtb = TB ? tr_desc(B, xs_b, l_kt) : rb;
 #pragma unroll
             for (int j = 0; j < LOADS; ++j) {   // j < 4: A groups, j >= 4: B groups
                 const bool isb = j >= 4;
-                const uint32_t soff = (uint32_t)(j & 3) * (isb ? b_j : a_j) + (uint32_t)l_kt * (isb ? b_k : a_k);
+                uint32_t soff;
+                if (isb ? TB : TA) {   // piece (j & 1) of column block 2 lw + ((j & 3) >> 1) of the tile
+                    const int cb = ((isb ? l_n0 : l_m0) >> 5) + 2 * lw + ((j & 3) >> 1);
+                    soff = (uint32_t)cb * (uint32_t)(256 * 32 * 2) + (uint32_t)((l_kt & 7) * 32 + 16 * (j & 1)) * ROWB;
+                } else {
+                    soff = (uint32_t)(j & 3) * (isb ? b_j : a_j) + (uint32_t)l_kt * (isb ? b_k : a_k);
+                }
+                // (the same LDS offset in both layouts: 1 KB piece lw * 4 + (j & 3))
                 const uint32_t dst = st + (isb ? A_ST : 0) + (uint32_t)(lw * 64 + 16 * (j & 3)) * ROWB;
-                lds_load16(live ? (isb ? rb : ra) : rnone, isb ? vb : va, soff, dst);
+                lds_load16(live ? (isb ? rtb : rta) : rnone, isb ? vb : va, soff, dst);
             }
         };
         auto advance = [&]() {
@@ -177,13 +224,24 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             if (bits == 0) return;
             char* st = smem + (u % STAGES) * ST_BYTES;
             const int r = lw * 64 + lane;                 // this lane's row of the A and of the B block
+            if (TA || TB) {   // in a transposed operand the row is k = lane % 32 of a column block
+                if ((bits >> (lane & 31)) & 1u) {
+                    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (TA) *reinterpret_cast<uint4*>(st + r * ROWB + 16 * q) = zero;
+                        if (TB) *reinterpret_cast<uint4*>(st + A_ST + r * ROWB + 16 * q) = zero;
+                    }
+                }
+                if (TA && TB) return;
+            }
             const int sw = (r >> 2) & 3;
             while (bits) {
                 const int k = __builtin_ctz(bits);
                 bits &= bits - 1;
                 const uint32_t o = (uint32_t)(r * ROWB + ((((k >> 3) ^ sw)) << 4) + (k & 7) * 2);
-                *reinterpret_cast<bf16_t*>(st + o) = 0;
-                *reinterpret_cast<bf16_t*>(st + A_ST + o) = 0;
+                if (!TA) *reinterpret_cast<bf16_t*>(st + o) = 0;
+                if (!TB) *reinterpret_cast<bf16_t*>(st + A_ST + o) = 0;
             }
         };
         if (my_tiles > 0) load_tile();
@@ -219,6 +277,18 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         rdA[sub] = (wm * 64 + rl) * ROWB + x;
         rdB[sub] = A_ST + (wn * 128 + rl) * ROWB + x;
     }
+    // transposed operands: this lane's address in a column block
+    const int tg = lane >> 4;
+    const uint32_t trb = (uint32_t)((8 * (tg >> 1) + ((lane >> 2) & 3)) * ROWB + (16 * (tg & 1) + 4 * (lane & 3)) * 2);
+    // operand i (A) / j (B) of sub-step sub from the stage at st
+    auto opA = [&](const char* st, int sub, int i) -> bf16x8_t {
+        if constexpr (TA) return lds_read_tr8(st + trb + (2 * wm + i) * 2048 + sub * 16 * ROWB);
+        else return *reinterpret_cast<const bf16x8_t*>(st + rdA[sub] + i * 32 * ROWB);
+    };
+    auto opB = [&](const char* st, int sub, int j) -> bf16x8_t {
+        if constexpr (TB) return lds_read_tr8(st + A_ST + trb + (4 * wn + j) * 2048 + sub * 16 * ROWB);
+        else return *reinterpret_cast<const bf16x8_t*>(st + rdB[sub] + j * 32 * ROWB);
+    };
     int c_stage = 0;
     for (int it = 0; it < my_tiles; ++it) {
         bf16x8_t a0[MI], b0[4];  // sub-step 0 operands, read one step ahead within a tile
@@ -235,10 +305,10 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            b0[j] = *reinterpret_cast<const bf16x8_t*>(smem + c_stage * ST_BYTES + rdB[0] + j * 32 * ROWB);
+            b0[j] = opB(smem + c_stage * ST_BYTES, 0, j);
 #pragma unroll
         for (int i = 0; i < MI; ++i)
-            a0[i] = *reinterpret_cast<const bf16x8_t*>(smem + c_stage * ST_BYTES + rdA[0] + i * 32 * ROWB);
+            a0[i] = opA(smem + c_stage * ST_BYTES, 0, i);
         for (int kt = 0; kt < nk; ++kt) {
             if (kt > 0) __syncthreads();
             const char* st = smem + c_stage * ST_BYTES;
@@ -250,9 +320,8 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 const int i = x >> 2, j = x & 3;
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
                 const int y = x - 2;   // reads of sub-step 1 start after the first two MFMAs
-                if (y >= 0 && y < 4) b1[y] = *reinterpret_cast<const bf16x8_t*>(st + rdB[1] + y * 32 * ROWB);
-                else if (y >= 4 && y < 4 + MI)
-                    a1[y - 4] = *reinterpret_cast<const bf16x8_t*>(st + rdA[1] + (y - 4) * 32 * ROWB);
+                if (y >= 0 && y < 4) b1[y] = opB(st, 1, y);
+                else if (y >= 4 && y < 4 + MI) a1[y - 4] = opA(st, 1, y - 4);
             }
             // sub-step 1; after MFMA x, the operand read x - 2 of the next
             // step's sub-step 0 (its stage is complete since this step's
@@ -262,10 +331,8 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
                 const int i = x >> 2, j = x & 3;
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
                 const int y = x - 2;
-                if (y >= 0 && y < 4)
-                    b0[y] = *reinterpret_cast<const bf16x8_t*>(stn + rdB[0] + y * 32 * ROWB);
-                else if (y >= 4 && y < 4 + MI)
-                    a0[y - 4] = *reinterpret_cast<const bf16x8_t*>(stn + rdA[0] + (y - 4) * 32 * ROWB);
+                if (y >= 0 && y < 4) b0[y] = opB(stn, 0, y);
+                else if (y >= 4 && y < 4 + MI) a0[y - 4] = opA(stn, 0, y - 4);
             }
         }
 
@@ -430,6 +497,23 @@ hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, 
     hipLaunchKernelGGL((k2_contract_ws<true, false, false>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A,
                        (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, N, (int64_t)0, (int64_t)0, M * N, tm, tn,
                        total, accumulate, (const uint8_t*)nullptr);
+    return hipGetLastError();
+}
+
+hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void* B, float* C, int64_t M, int64_t N,
+                                      int64_t K, int batch, int cus, hipStream_t s) {
+    constexpr int BM = 256;
+    const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
+    const int total = tm * tn * batch;
+    const int grid = total < cus ? total : cus;
+#define K2_TR(TA_, TB_)                                                                                             \
+    hipLaunchKernelGGL((k2_contract_ws<true, false, true, TA_, TB_>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A, \
+                       (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, (int64_t)0, (int64_t)0, (int64_t)0,     \
+                       (int64_t)0, tm, tn, total, 0, (const uint8_t*)nullptr)
+    if (!ta && tb) K2_TR(false, true);
+    else if (ta && tb) K2_TR(true, true);
+    else return hipErrorInvalidValue;
+#undef K2_TR
     return hipGetLastError();
 }
 

@@ -41,6 +41,12 @@ hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t k
 // bf16 contraction of blocked operands into a row-major fp32 C [batch][M][N].
 hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
                                         int batch, int accumulate, int cus, hipStream_t s);
+// bf16 contraction of blocked operands, either given as its transpose in the
+// panel layout (ta: A[c][i][k] = X[c][k][i], X with K rows and M columns; tb
+// likewise with N columns), into the pair-blocked fp32 result layout.
+// Supported: (ta, tb) = (0, 1) and (1, 1).
+hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void* B, float* C, int64_t M, int64_t N,
+                                      int64_t K, int batch, int cus, hipStream_t s);
 
 struct EpilogueArgs {
     const float* C;      // fp32 contraction result: pair-blocked (cblocked) or [c][rows][ldc]

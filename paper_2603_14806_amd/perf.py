@@ -40,12 +40,12 @@ def backward_layer_work(N, c_z=128, c=128, recompute=True):
     forward's state is passed in, dA and dB) and the algorithmic HBM bytes of
     its per-pair kernels (per pair: projection recompute 768 B (recompute
     only), epilogue backward 3072 B, projection backward 3328 B, six
-    weight-gradient sums 6 x 512 B, three panel transposes 3 x 512 B =
-    11776 B at c_z = c = 128 with the recompute)."""
+    weight-gradient sums 6 x 512 B = 10240 B at c_z = c = 128 with the
+    recompute; the products read their transposed operands in place)."""
     mfma = (3 if recompute else 2) * 2.0 * N ** 3 * c
     per_pair = (c_z * 2 + 2 * c * 2 if recompute else 0) \
         + (c * 4 + c_z * 2 + c_z * 4 + c * 2 + c_z * 4 + 4 * 2 * c) \
-        + (2 * c * 4 + c_z * 2 + c_z * 4 + c_z * 2 + 5 * 2 * c) + 6 * 4 * c + 3 * 2 * 2 * c
+        + (2 * c * 4 + c_z * 2 + c_z * 4 + c_z * 2 + 5 * 2 * c) + 6 * 4 * c
     return {"mfma_flops": mfma, "hbm_bytes": float(per_pair) * N * N,
             "floor_ms": 1e3 * (mfma / (PEAK_BF16_TFLOPS * 1e12) + per_pair * N * N / (PEAK_HBM_GBS * 1e9))}
 

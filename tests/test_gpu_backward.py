@@ -68,6 +68,44 @@ def test_contract_backward_gaussian(dtype, N):
     check(host(dB), rB, dtype, "dB")
 
 
+def poisoned_panel(X):
+    """dense_to_panel with NaN in every padding element."""
+    c, N = X.shape[0], X.shape[1]
+    _, tr, S = T._panel_dims(N, c)
+    Y = torch.full((c, tr * 256, S * 32), float("nan"), dtype=X.dtype, device=X.device)
+    Y[:, :N, :N] = X
+    return Y.reshape(c, tr, 256, S, 32).permute(0, 1, 3, 2, 4).contiguous().reshape(-1)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("N", [100, 300])
+def test_contract_backward_ignores_padding(dtype, N):
+    """NaN in the padding rows and columns of the A and B panels, in the
+    padding columns of dC's result layout and in the whole workspace: the
+    products reach no padding element (k past N is zeroed in LDS, output
+    rows and columns past N are not stored), so integer data stay exact."""
+    say(f"contract backward poisoned padding dtype={dtype} N={N}")
+    layer, _ = make_layer(dtype)
+    g = torch.Generator().manual_seed(300 + N)
+    A = torch.randint(-4, 5, (128, N, N), generator=g).to(synth.DTYPES[dtype]).cuda()
+    B = torch.randint(-4, 5, (128, N, N), generator=g).to(synth.DTYPES[dtype]).cuda()
+    dC = torch.randint(-4, 5, (128, N, N), generator=g).float().cuda()
+    J = -(-N // 32)
+    dCr = torch.full((128, N, J * 32), float("nan"), device="cuda")
+    dCr[:, :, :N] = dC
+    dCr = dCr.reshape(128, N, J, 32).permute(1, 2, 0, 3).contiguous().reshape(-1)
+    n = N * J * 32 * 128
+    dA = torch.empty(n, device="cuda")
+    dB = torch.empty(n, device="cuda")
+    wsb = T.tri_mul_contract_backward_workspace_size(layer.h, N)
+    ws = torch.full((wsb,), 0xff, dtype=torch.uint8, device="cuda")       # NaN in both dtypes
+    T.tri_mul_contract_backward(layer.h, dCr, poisoned_panel(A), poisoned_panel(B), N, dA, dB, ws, wsb)
+    torch.cuda.synchronize()
+    rA, rB = oracle.contract_backward(host(A), host(B), host(dC))
+    np.testing.assert_array_equal(host(T.result_to_dense(dA, N)), rA)
+    np.testing.assert_array_equal(host(T.result_to_dense(dB, N)), rB)
+
+
 def test_contract_backward_n4096_sampled():
     """The benchmark size (N = 4096, bf16) in the launch configuration the
     benchmark times; sampled rows of dA and dB against the oracle, one channel
