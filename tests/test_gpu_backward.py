@@ -39,7 +39,7 @@ def run(layer, A, B, dC_dense, N):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("N", [64, 100, 300])
+@pytest.mark.parametrize("N", [1, 33, 64, 100, 300])
 def test_contract_backward_exact_on_integers(dtype, N):
     say(f"contract backward exact dtype={dtype} N={N}")
     layer, _ = make_layer(dtype)

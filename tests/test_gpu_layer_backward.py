@@ -37,7 +37,7 @@ def grads_vs_oracle(N, direction, masked, seed):
 
 
 @pytest.mark.parametrize("direction", ["outgoing", "incoming"])
-@pytest.mark.parametrize("N,masked", [(64, False), (100, True), (257, True)])
+@pytest.mark.parametrize("N,masked", [(1, False), (2, True), (33, True), (64, False), (100, True), (257, True)])
 def test_layer_backward_matches_oracle(direction, N, masked):
     say(f"layer backward {direction} N={N} masked={masked}")
     dz, g, ref, mask = grads_vs_oracle(N, direction, masked, seed=N + (7 if direction == "incoming" else 0))
