@@ -251,11 +251,13 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             advance();
         }
         for (int s = 0; s < steps; ++s) {
-            // steps s and s + 1 complete at barrier s; later ones in flight
+            // steps s and s + 1 complete at barrier s; later ones in flight.
+            // (Waits with a memory clobber: the LDS zeroing below must not
+            // be moved above them.)
             const int ahead = min(STAGES - 3, steps - 2 - s);
-            if (ahead >= 2) wait_vmcnt<2 * LOADS>();
-            else if (ahead == 1) wait_vmcnt<LOADS>();
-            else wait_vmcnt<0>();
+            if (ahead >= 2) wait_vmcnt_pinned<2 * LOADS>();
+            else if (ahead == 1) wait_vmcnt_pinned<LOADS>();
+            else wait_vmcnt_pinned<0>();
             if (s == 0) zero_dead(0);
             if (s + 1 < steps) zero_dead(s + 1);
             __syncthreads();
@@ -263,7 +265,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             issue_step(fetch);
             if (fetch) advance();
         }
-        wait_vmcnt<0>();
+        wait_vmcnt_pinned<0>();
         return;
     }
 
