@@ -17,7 +17,6 @@ namespace {
 constexpr int kHd = 32;          // head dimension
 constexpr int kKc = 64;          // keys per chunk
 constexpr int kQt = 128;         // queries per work-group (4 waves x 32)
-constexpr int kVtRow = 68;       // LDS row stride (bf16) of V^T [32 d][64 keys]: rows 34 banks apart
 constexpr int kBRow = 68;        // LDS row stride (bf16) of the bias tile [128 q][64 keys]
 
 // K chunk [64 keys][32 d] bf16: 16-byte piece c4 (d = 8 c4 ..) of key kk,
@@ -25,6 +24,14 @@ constexpr int kBRow = 68;        // LDS row stride (bf16) of the bias tile [128 
 __device__ __forceinline__ uint32_t koff(int kk, int c4) { return (uint32_t)(kk * 64 + ((c4 ^ ((kk >> 2) & 3)) << 4)); }
 
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32); }
+
+// ds_read_b64_tr_b16: in each 16-lane group g, lane 16 g + 4 a + b receives
+// element b of the 8-byte chunks addressed by lanes 16 g + a, + 4, + 8, + 12.
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr4(const void* p) {
+    typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(p)));
+}
 
 struct TaChunk {                 // one chunk's global loads (registers)
     uint4 kv, vv;                // key t / 4, piece t % 4 of K and V
@@ -41,7 +48,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
                                                  float* __restrict__ stL, int load_state, int finish,
                                                  TO* __restrict__ out) {
     __shared__ __align__(16) char ks[2][kKc * 64];            // K chunks
-    __shared__ __align__(16) bf16_t vt[2][kHd * kVtRow];      // V^T chunks
+    __shared__ __align__(16) char vs[2][kKc * 64];            // V chunks [64 keys][32 d], row-major
     __shared__ __align__(16) bf16_t bt[2][kQt * kBRow];       // bias tiles
     __shared__ float mb[2][kKc];                              // 0 or -inf per key
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -92,12 +99,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
         const int kb = k0 + c * kKc;
         const int kk = t >> 2, c4 = t & 3;
         *reinterpret_cast<uint4*>(ks[buf] + koff(kk, c4)) = p.kv;
-        const uint32_t vw[4] = {p.vv.x, p.vv.y, p.vv.z, p.vv.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            vt[buf][(8 * c4 + 2 * e) * kVtRow + kk] = (bf16_t)(vw[e] & 0xffffu);
-            vt[buf][(8 * c4 + 2 * e + 1) * kVtRow + kk] = (bf16_t)(vw[e] >> 16);
-        }
+        *reinterpret_cast<uint4*>(vs[buf] + kk * 64 + c4 * 16) = p.vv;   // a wave: 1 KB contiguous
         const int br = t >> 1;
 #pragma unroll
         for (int s2 = 0; s2 < 4; ++s2) {
@@ -128,6 +130,8 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
     }
 
     const float scale = 0.17677669529663688f;                 // 1 / sqrt(32)
+    const int vkey = 4 * (lane >> 5) + ((lane >> 2) & 3);     // transposing reads of V: this lane's key
+    const int vdim = 2 * (16 * ((lane >> 4) & 1) + 4 * (lane & 3));   // and byte offset of its 4 dims
     TaChunk cur;
     load(0, cur);
     for (int c = 0; c < nchunks; ++c) {
@@ -194,14 +198,18 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
         for (int r = 0; r < 16; ++r) o[r] *= alpha;
         M = Mn;
         // O^T += V^T P^T: k-step (b, t2) covers keys 32 b + 16 t2 .. + 15; half hi supplies keys
-        // {16 t2 + 4 hi + 0..3, 16 t2 + 8 + 4 hi + 0..3} = registers 8 t2 .. 8 t2 + 7
+        // {16 t2 + 4 hi + 0..3, 16 t2 + 8 + 4 hi + 0..3} = registers 8 t2 .. 8 t2 + 7.  The V^T
+        // fragment (lane: output dim ql, those 8 keys) comes from the row-major V chunk through two
+        // transposing reads: addressing lane 16 g + 4 i + a points at key 4 (g >> 1) + i (+ 8 for
+        // the second read) and dims 16 (g & 1) + 4 a .. + 3, so lane l receives dim l % 32 of four
+        // consecutive keys.
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2) {
-                const bf16_t* vr = &vt[buf][ql * kVtRow + 32 * b + 16 * t2 + 4 * hi];
-                const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
-                const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 8);
+                const char* vr = vs[buf] + (32 * b + 16 * t2 + vkey) * 64 + vdim;
+                const uint2 v0 = lds_read_tr4(vr);
+                const uint2 v1 = lds_read_tr4(vr + 8 * 64);
                 const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
                 uint32_t ph[4], pl[4];
 #pragma unroll
