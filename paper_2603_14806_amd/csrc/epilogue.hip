@@ -355,7 +355,9 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
     constexpr bool kDirect = sizeof(TO) == 4;
     constexpr int kStages = kDirect ? 3 : 2;
     __shared__ __attribute__((aligned(16))) char ring[kStages * kRSt];
-    __shared__ __attribute__((aligned(16))) float prm[4][128];               // LN gains and biases
+    // LN gains and biases; channel c at (c / 16) * 20 + c % 16, so that the 8
+    // broadcast addresses of a read (c = 16 lq + 2 k) fall in distinct banks
+    __shared__ __attribute__((aligned(16))) float prm[4][8 * 20];
     __shared__ __attribute__((aligned(16))) float os[kDirect ? 4 : kP3 * kOsRow];   // outputs as [p][d]
     const int t = threadIdx.x, lane = t & 63;
     const int w = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -411,10 +413,11 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         wg[ks] = *reinterpret_cast<const bf16x8_t*>(wepi + (size_t)(128 + w * 32 + (lane & 31)) * 128 + col);
     }
     if (t < 128) {
-        prm[0][t] = lnout_w[t];
-        prm[1][t] = lnout_b[t];
-        prm[2][t] = lnin_w[t];
-        prm[3][t] = lnin_b[t];
+        const int tp = (t >> 4) * 20 + (t & 15);
+        prm[0][tp] = lnout_w[t];
+        prm[1][tp] = lnout_b[t];
+        prm[2][tp] = lnin_w[t];
+        prm[3][tp] = lnin_b[t];
     }
 
     int stage = 0;
@@ -483,7 +486,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
             uint32_t yh[8], yl[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
-                const int c = 16 * lq + 2 * k;
+                const int c = 20 * lq + 2 * k;   // channel 16 lq + 2 k in prm
                 const float y0 = v[2 * k] * rs * prm[0][c] + prm[1][c];
                 const float y1 = v[2 * k + 1] * rs * prm[0][c + 1] + prm[1][c + 1];
                 const uint32_t h = pack_bf16x2(y0, y1);
@@ -512,7 +515,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
             uint32_t hx[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
-                const int c = 16 * lq + 2 * k;
+                const int c = 20 * lq + 2 * k;   // channel 16 lq + 2 k in prm
                 hx[k] = pack_bf16x2(zv[2 * k] * rs * prm[2][c] + prm[3][c], zv[2 * k + 1] * rs * prm[2][c + 1] + prm[3][c + 1]);
             }
             *reinterpret_cast<uint4*>(st + kRC + yoff(lp, 2 * lq)) = make_uint4(hx[0], hx[1], hx[2], hx[3]);

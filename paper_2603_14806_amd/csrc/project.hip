@@ -127,7 +127,9 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
     __shared__ __attribute__((aligned(16))) char ring[kRing * kSt];     // z rows [p][256 B], mask
     __shared__ __attribute__((aligned(16))) char xs[2][kP1 * kXRow];   // x_hi, x_lo
     __shared__ __attribute__((aligned(16))) float os[2][kCh][kP1];      // a, b as [c][p]
-    __shared__ __attribute__((aligned(16))) float gb[2][kCz];           // LayerNorm gain, bias
+    // LayerNorm gain, bias; channel c at (c / 16) * 20 + c % 16, so that the
+    // 8 broadcast addresses of a read (c = 16 lq + 4 i) fall in distinct banks
+    __shared__ __attribute__((aligned(16))) float gb[2][8 * 20];
     const int t = threadIdx.x, lane = t & 63;
     const int g = __builtin_amdgcn_readfirstlane(t >> 6);
     const int lp = t >> 3, lq = t & 7;     // LayerNorm: pair lp, channels 16 lq .. 16 lq + 15
@@ -179,8 +181,8 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
             w[ob][ks] = *reinterpret_cast<const bf16x8_t*>(
                 wproj + (size_t)(g * 128 + ob * 32 + (lane & 31)) * kCz + ks * 16 + 8 * (lane >> 5));
     if (t < kCz) {
-        gb[0][t] = lnw[t];
-        gb[1][t] = lnb[t];
+        gb[0][(t >> 4) * 20 + (t & 15)] = lnw[t];
+        gb[1][(t >> 4) * 20 + (t & 15)] = lnb[t];
     }
     const PanelGeom pg = panel_geom(N, N);
     // Store mapping: thread t writes pairs 8 (t & 3) .. 8 (t & 3) + 7 of
@@ -229,8 +231,8 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         float gam[16], bet[16];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float4 a4 = *reinterpret_cast<const float4*>(&gb[0][16 * lq + 4 * i]);
-            const float4 b4 = *reinterpret_cast<const float4*>(&gb[1][16 * lq + 4 * i]);
+            const float4 a4 = *reinterpret_cast<const float4*>(&gb[0][20 * lq + 4 * i]);
+            const float4 b4 = *reinterpret_cast<const float4*>(&gb[1][20 * lq + 4 * i]);
             gam[4 * i] = a4.x; gam[4 * i + 1] = a4.y; gam[4 * i + 2] = a4.z; gam[4 * i + 3] = a4.w;
             bet[4 * i] = b4.x; bet[4 * i + 1] = b4.y; bet[4 * i + 2] = b4.z; bet[4 * i + 3] = b4.w;
         }
