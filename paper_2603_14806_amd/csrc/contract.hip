@@ -443,41 +443,38 @@ __global__ void k_stage_kmask(const uint8_t* __restrict__ mask, int klen, int pa
 // blocked operand layout of the contraction, [ch][tiles][nk][256][32], with
 // the staged k-mask applied and zeros for rows >= rows and k >= klen (the
 // staged mask is 0 there).  One work-group per (two k-steps, 256-row tile,
-// channel); thread r moves the 128 bytes of its row: whole cache lines in,
-// two 64-byte rows of two 16 KB blocks out.
+// channel).  Thread t moves 16-byte piece e = t % 8 of the 128 bytes (two
+// k-steps) of rows t / 8 + 32 j, j < 8: a load instruction reads eight whole
+// 128-byte row segments, a store writes two runs of eight consecutive
+// 64-byte block rows (one per k-step).
 __global__ __launch_bounds__(256) void k_panel_block(const bf16_t* __restrict__ P, int rows, int ld, int64_t sP,
                                                      int tiles, int nk, const uint8_t* __restrict__ kst,
                                                      bf16_t* __restrict__ dst) {
-    const int kp = blockIdx.x, tile = blockIdx.y, c = blockIdx.z, r = threadIdx.x;
+    const int kp = blockIdx.x, tile = blockIdx.y, c = blockIdx.z, t = threadIdx.x;
     const int r0 = tile * 256;
     const int nrow = min(256, rows - r0);
+    const int e = t & 7, h = e >> 2, q = e & 3;   // k-step 2 kp + h, k = 8 q .. + 7 within it
+    const int kt = 2 * kp + h;
     // rows past the panel fall outside the descriptor and read as zero
     const __amdgpu_buffer_rsrc_t rp = make_rsrc(P + c * sP + (int64_t)r0 * ld, (uint32_t)nrow * (uint32_t)ld * 2u);
-    uint4 v[2][4];
+    uint4 v[8];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int j = 0; j < 8; ++j) v[j] = buf_load16(rp, (uint32_t)(((t >> 3) + 32 * j) * ld + kp * 64 + 8 * e) * 2u);
+    if (kt >= nk) return;   // the odd last k-step of the panel has no second half
+    // staged 0/1 bytes of k = 32 kt + 8 q .. + 7 (fresh for every k < 32 nk)
+    const uint2 m8 = *reinterpret_cast<const uint2*>(kst + kt * 32 + 8 * q);
+    const uint32_t mw[2] = {m8.x, m8.y};
+    uint32_t keep[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            v[h][q] = buf_load16(rp, (uint32_t)(r * ld + (2 * kp + h) * 32 + 8 * q) * 2u);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int kt = 2 * kp + h;
-        if (kt >= nk) break;
-        bf16_t* out = dst + (((int64_t)c * tiles + tile) * nk + kt) * (256 * 32) + r * 32;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            // staged 0/1 bytes of k = 32 kt + 8 q .. + 7 (fresh for every k < 32 nk)
-            const uint2 m8 = *reinterpret_cast<const uint2*>(kst + kt * 32 + 8 * q);
-            const uint32_t mw[2] = {m8.x, m8.y};
-            uint32_t w[4] = {v[h][q].x, v[h][q].y, v[h][q].z, v[h][q].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t b2 = mw[e >> 1] >> (16 * (e & 1));
-                w[e] &= ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
-            }
-            *reinterpret_cast<uint4*>(out + 8 * q) = make_uint4(w[0], w[1], w[2], w[3]);
-        }
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t b2 = mw[i >> 1] >> (16 * (i & 1));
+        keep[i] = ((b2 & 0xffu) ? 0xffffu : 0u) | ((b2 & 0xff00u) ? 0xffff0000u : 0u);
     }
+    bf16_t* out = dst + (((int64_t)c * tiles + tile) * nk + kt) * (256 * 32) + 8 * q;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        *reinterpret_cast<uint4*>(out + ((t >> 3) + 32 * j) * 32) =
+            make_uint4(v[j].x & keep[0], v[j].y & keep[1], v[j].z & keep[2], v[j].w & keep[3]);
 }
 
 }  // namespace
