@@ -16,11 +16,13 @@ namespace trimul {
 namespace {
 
 // dC in the pair-blocked result layout (fp32) -> the panel layout, element
-// (c, i, j) -> X_c[i][k = j], converted to T.  One unit = one row i and one
-// 32-column block: 128 channels x 32 floats, contiguous in both layouts per
-// channel.  Thread t moves channel t / 2, columns 16 (t % 2) .. + 15.
-// Columns past N carry whatever the result layout holds there into the k
-// padding of the panel, which the contraction never uses.
+// (c, i, j) -> X_c[i][k = j], converted to T.  One unit = two rows i, i + 1
+// (i even) and one 32-column block: 2 x 128 channels x 32 floats, contiguous
+// per channel in the result layout; in the panel the two rows of a channel
+// are adjacent (one 128-byte line in bf16), so no store writes a partial
+// line.  Thread t moves channel t / 2, columns 16 (t % 2) .. + 15 of both
+// rows.  Columns past N carry whatever the result layout holds there into
+// the k padding of the panel, which the contraction never uses.
 template <typename T>
 __global__ __launch_bounds__(256) void k_result_to_panel(const float* __restrict__ R, T* __restrict__ P, int N,
                                                         int64_t units) {
@@ -28,23 +30,34 @@ __global__ __launch_bounds__(256) void k_result_to_panel(const float* __restrict
     const int J = (N + kResJ - 1) / kResJ;
     const PanelGeom pg = panel_geom(N, N);
     for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
-        const int64_t i = u / J, jb = u - (u / J) * J;
-        const float4* src = reinterpret_cast<const float4*>(R + result_off(J, kCh, ch, i, jb * kResJ) + 16 * h);
-        float4 v[4];
+        const int64_t ip = u / J, jb = u - (u / J) * J;
+        const int64_t i0 = 2 * ip;
+        const int nr = i0 + 1 < N ? 2 : 1;                 // an odd N's last unit holds one row
+        float4 v[2][4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = src[q];
-        T* dst = P + panel_off(pg, ch, i, jb * kResJ + 16 * h);
-        if constexpr (sizeof(T) == 2) {
-            uint4 o[2];
-            o[0] = make_uint4(pack_bf16x2(v[0].x, v[0].y), pack_bf16x2(v[0].z, v[0].w),
-                              pack_bf16x2(v[1].x, v[1].y), pack_bf16x2(v[1].z, v[1].w));
-            o[1] = make_uint4(pack_bf16x2(v[2].x, v[2].y), pack_bf16x2(v[2].z, v[2].w),
-                              pack_bf16x2(v[3].x, v[3].y), pack_bf16x2(v[3].z, v[3].w));
-            reinterpret_cast<uint4*>(dst)[0] = o[0];
-            reinterpret_cast<uint4*>(dst)[1] = o[1];
-        } else {
+        for (int rr = 0; rr < 2; ++rr) {
+            if (rr < nr) {
+                const float4* src = reinterpret_cast<const float4*>(R + result_off(J, kCh, ch, i0 + rr, jb * kResJ) + 16 * h);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) reinterpret_cast<float4*>(dst)[q] = v[q];
+                for (int q = 0; q < 4; ++q) v[rr][q] = src[q];
+            }
+        }
+#pragma unroll
+        for (int rr = 0; rr < 2; ++rr) {
+            if (rr >= nr) break;
+            T* dst = P + panel_off(pg, ch, i0 + rr, jb * kResJ + 16 * h);
+            if constexpr (sizeof(T) == 2) {
+                uint4 o[2];
+                o[0] = make_uint4(pack_bf16x2(v[rr][0].x, v[rr][0].y), pack_bf16x2(v[rr][0].z, v[rr][0].w),
+                                  pack_bf16x2(v[rr][1].x, v[rr][1].y), pack_bf16x2(v[rr][1].z, v[rr][1].w));
+                o[1] = make_uint4(pack_bf16x2(v[rr][2].x, v[rr][2].y), pack_bf16x2(v[rr][2].z, v[rr][2].w),
+                                  pack_bf16x2(v[rr][3].x, v[rr][3].y), pack_bf16x2(v[rr][3].z, v[rr][3].w));
+                reinterpret_cast<uint4*>(dst)[0] = o[0];
+                reinterpret_cast<uint4*>(dst)[1] = o[1];
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) reinterpret_cast<float4*>(dst)[q] = v[rr][q];
+            }
         }
     }
 }
@@ -897,7 +910,7 @@ __global__ __launch_bounds__(256) void k_sum_parts(const float* __restrict__ in,
 }  // namespace
 
 hipError_t launch_result_to_panel(int dtype, const float* R, void* P, int64_t N, int cus, hipStream_t s) {
-    const int64_t units = N * ((N + kResJ - 1) / kResJ);
+    const int64_t units = (N + 1) / 2 * ((N + kResJ - 1) / kResJ);   // row pairs x column blocks
     const unsigned g = (unsigned)(units < 8 * (int64_t)cus ? units : 8 * (int64_t)cus);
     if (dtype == 0)
         hipLaunchKernelGGL(k_result_to_panel<float>, dim3(g), dim3(256), 0, s, R, (float*)P, (int)N, units);
