@@ -148,7 +148,8 @@ __global__ __launch_bounds__(256) void k_panel_transpose(const T* __restrict__ X
 constexpr int kQ = 32;        // pairs per unit
 constexpr int kBT = 512;      // threads of the per-pair backward kernels
 constexpr int kCs = 36;       // row stride (floats) of [channel][pair] tiles
-constexpr int kPq = 132;      // row stride (floats) of [pair][channel] tiles
+constexpr int kPq = 148;      // row stride (floats) of [pair][channel] tiles (the fewest bank conflicts
+                              // over their four access patterns)
 constexpr int kArow = 256;    // bytes of one bf16 activation row [128]
 
 // Byte offset of 16-byte chunk ch of row p in a bf16 [q][128] tile; chunks
@@ -245,7 +246,10 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
     __shared__ __align__(16) float dct[kCh * kCs];       // dC [c][q]
     __shared__ __align__(16) char act[4][kQ * kArow];    // y hi, y lo, x hi, x lo  [q][128]
     __shared__ __align__(16) char act2[4][kQ * kArow];   // du hi, du lo, dgg hi, dgg lo  [q][128]
-    __shared__ float prm[4][128];                        // gamma_out, beta_out, gamma_in, beta_in
+    // gamma_out, beta_out, gamma_in, beta_in; rows 2 and 3 put channel d at
+    // d + 4 (d / 64), so that the 16 addresses 8 l + 2 i of a LayerNorm-input
+    // read fall in distinct banks
+    __shared__ float prm[4][136];
     __shared__ float mq[kQ];                             // pair mask of the unit
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const int lp = t >> 4, lq = t & 15;                  // LayerNorms: pair lp, 16 lanes per pair
@@ -307,8 +311,8 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
     if (t < 128) {
         prm[0][t] = lnow[t];
         prm[1][t] = lnob[t];
-        prm[2][t] = lniw[t];
-        prm[3][t] = lnib[t];
+        prm[2][t + 4 * (t >> 6)] = lniw[t];
+        prm[3][t + 4 * (t >> 6)] = lnib[t];
     }
 
     // Everything issued so far completes here, in a wait the compiler sees
@@ -351,8 +355,9 @@ __global__ __launch_bounds__(kBT) void k_epilogue_backward(
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int d = 8 * lq + 2 * i;
-                const float x0 = x[2 * i] * rz * prm[2][d] + prm[3][d];
-                const float x1 = x[2 * i + 1] * rz * prm[2][d + 1] + prm[3][d + 1];
+                const int dp = d + 4 * (d >> 6);             // padded position of d, d + 1
+                const float x0 = x[2 * i] * rz * prm[2][dp] + prm[3][dp];
+                const float x1 = x[2 * i + 1] * rz * prm[2][dp + 1] + prm[3][dp + 1];
                 hw[i] = pack_bf16x2(x0, x1);
                 lw[i] = pack_bf16x2(x0 - __uint_as_float(hw[i] << 16), x1 - __uint_as_float(hw[i] & 0xffff0000u));
             }
