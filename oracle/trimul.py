@@ -238,7 +238,9 @@ def contract_backward(A, B, dC):
     both directions take on the channel-major operands): given dL/dC return
         dA[c] = dC[c] @ B[c],   dB[c] = dC[c]^T @ A[c].
     A: [c][n][K], B: [c][m][K], dC: [c][n][m]."""
-    A, B, dC = f64(A), f64(B), f64(dC)
+    # contiguous copies, as in the forward contraction, so that numpy hands
+    # each channel's product to BLAS instead of its strided fallback loop
+    A, B, dC = (np.ascontiguousarray(f64(x)) for x in (A, B, dC))
     return dC @ B, dC.transpose(0, 2, 1) @ A
 
 
