@@ -70,12 +70,71 @@ def cpu_baseline(N, sample):
     t_dir = per_pair_proj * N * N + per_pair_token * N ** 3 + per_pair_epi * N * N
     f = perf.flops(N)["total"]
     return {"value": round(2 * f / (2 * t_dir) / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores),
-            "kind": "oracle",
+            "kind": "oracle", "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+            "implementation": "the fp64 numpy oracle (oracle/trimul.py) as it stands; its matrix products run "
+                              "in the BLAS library numpy links, on `cores` threads",
             "sample": (f"outgoing update of a {sample}x{sample} block of output pairs at N={N} (c_z=c=128, fp64): "
                        f"projections of {2 * sample}x{N} pairs, contraction over {N} tokens, epilogue; "
                        f"measured {t3 - t0:.1f} s, per-stage cost extrapolated to both directions of the layer "
                        f"({2 * t_dir:.0f} s per layer)"),
             "sample_seconds": round(t3 - t0, 2)}
+
+
+def cpu_model():
+    """The host CPU's model name from /proc/cpuinfo (None if unreadable)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+class ClockSampler:
+    """Samples the GPU's current graphics clock (the DPM level the amdgpu
+    sysfs file marks as current) every `period` seconds on a host thread, for
+    the clock-adjusted MFMA fraction.  Plain file reads, no GPU calls."""
+
+    def __init__(self, period=0.02):
+        import glob
+        import threading
+        self.period, self.samples, self._stop = period, [], threading.Event()
+        devs = sorted(d for d in glob.glob("/sys/class/drm/card*/device") if os.path.exists(d + "/pp_dpm_sclk"))
+        self.path = devs[0] + "/pp_dpm_sclk" if devs else None
+        self._th = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        for line in open(self.path):
+            if line.rstrip().endswith("*"):
+                return float(line.split(":", 1)[1].replace("*", "").strip().lower().replace("mhz", ""))
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                v = self._read()
+                if v:
+                    self.samples.append(v)
+            except (OSError, ValueError):
+                return
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.path:
+            self._th.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self.path:
+            self._th.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        v = sorted(self.samples)
+        return {"mean_MHz": round(sum(v) / len(v), 1), "min_MHz": v[0], "max_MHz": v[-1], "samples": len(v)}
 
 
 def gpu_state():
@@ -238,11 +297,12 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t0.record(stream)
-    for _ in range(args.steps):
-        step(evs)
-    t1.record(stream)
-    torch.cuda.synchronize()
+    with ClockSampler() as clocks:
+        t0.record(stream)
+        for _ in range(args.steps):
+            step(evs)
+        t1.record(stream)
+        torch.cuda.synchronize()
     ms_step = t0.elapsed_time(t1) / args.steps
     k_ms = {name: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / len(evs)
             for i, name in enumerate(("project", "contract", "epilogue"))}
@@ -261,6 +321,50 @@ def main():
     f1.record(stream)
     torch.cuda.synchronize()
     full_ms = f0.elapsed_time(f1) / 2
+
+    # the N = 2048 workload with channel-scaled z (s_c ~ U(0.5, 2)), both
+    # directions through the three kernels, outside the timed region
+    c3 = None
+    if N != 2048:
+        N3 = 2048
+        z3 = synth.pair_tensor(N3, dtype="bf16", scale=synth.channel_scale(), device=dev)
+        np3 = T.tri_mul_panel_size(h, N3) // 2
+        A3, B3 = A[:np3], B[:np3]
+        C3 = C[:N3 * (-(-N3 // 32) * 32) * 128]
+        o3 = outs[0].view(-1)[:N3 * N3 * 128].view(N3, N3, 128)
+        ev3 = {}
+        for direction, code in (("outgoing", T.TRI_MUL_OUTGOING), ("incoming", T.TRI_MUL_INCOMING)):
+            for _ in range(2):   # warm-up
+                T.tri_mul_project(h, z3, None, N3, code, A3, B3, stream)
+                T.tri_mul_contract(h, A3, B3, N3, C3, stream)
+                T.tri_mul_epilogue(h, C3, z3, None, N3, o3, stream)
+            es = []
+            for _ in range(5):
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                e[0].record(stream)
+                T.tri_mul_project(h, z3, None, N3, code, A3, B3, stream)
+                e[1].record(stream)
+                T.tri_mul_contract(h, A3, B3, N3, C3, stream)
+                e[2].record(stream)
+                T.tri_mul_epilogue(h, C3, z3, None, N3, o3, stream)
+                e[3].record(stream)
+                es.append(e)
+            ev3[direction] = es
+        torch.cuda.synchronize()
+        fl3 = perf.flops(N3)
+        c3 = {"what": "N=2048, z_ijc = s_c n_ijc with s_c ~ U(0.5, 2) per pair channel, n ~ N(0,1), all-ones mask, "
+                      "bf16 storage, fp32 output; each direction through K1 -> K2 -> K3, 2 warm-up + 5 timed "
+                      "calls; not part of ms_per_step"}
+        for direction, es in ev3.items():
+            k = [sum(e[i].elapsed_time(e[i + 1]) for e in es) / len(es) for i in range(3)]
+            tot = sum(e[0].elapsed_time(e[3]) for e in es) / len(es)
+            c3[direction] = {"ms": round(tot, 4), "TFLOP_per_s": round(fl3["total"] / (tot * 1e-3) / 1e12, 2),
+                             "project_ms": round(k[0], 4), "contract_ms": round(k[1], 4),
+                             "epilogue_ms": round(k[2], 4),
+                             "contract_TFLOP_per_s": round(fl3["contract"] / (k[1] * 1e-3) / 1e12, 2)}
+        c3["ms_per_layer"] = round(c3["outgoing"]["ms"] + c3["incoming"]["ms"], 4)
+        del z3
+        print(f"[bench] N=2048 channel-scaled layer {c3['ms_per_layer']:.3f} ms", file=sys.stderr, flush=True)
 
     bwd_ms = lbwd_ms = sbwd_ms = opm_ms = ta_ms = tile_ms = None
     ta_scores = 2048 * 4 * 2048 * 2048
@@ -405,6 +509,12 @@ def main():
                 "frac": round(a / perf.PEAK_BF16_TFLOPS, 4)}
     layer_flops = 2 * fl["total"]
     contract_tflops = fl["contract"] / (k_ms["contract"] * 1e-3) / 1e12
+    clk = clocks.summary()
+
+    def hbm_roof(nbytes, ms):
+        a = nbytes / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": perf.PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(a / perf.PEAK_HBM_GBS, 4), "bytes_per_launch": nbytes}
     result = {
         "metric": "triangle-mult ms/layer + TFLOP/s at N=4096 bf16; % of MFMA bf16 peak",
         "value": round(layer_flops / (ms_step * 1e-3) / 1e12, 3),
@@ -421,14 +531,20 @@ def main():
         "ms_per_layer_median": round(step_median, 4), "ms_per_layer_min": round(per_step[0], 4),
         "gpu_state": {"before": state_before, "after": gpu_state()},
         "contract_pct_of_bf16_peak": round(100 * contract_tflops / perf.PEAK_BF16_TFLOPS, 2),
+        "contract_pct_of_bf16_peak_clock_adjusted": None if clk is None else
+            round(100 * contract_tflops / perf.bf16_peak_at(clk["mean_MHz"]), 2),
+        "sclk_during_timed_steps": clk,
         "kernels": {
             "project": {"ms": round(k_ms["project"], 4),
                         "GB_per_s": round(by["project"] / (k_ms["project"] * 1e-3) / 1e9, 1),
-                        "TFLOP_per_s": round(fl["project"] / (k_ms["project"] * 1e-3) / 1e12, 2)},
+                        "TFLOP_per_s": round(fl["project"] / (k_ms["project"] * 1e-3) / 1e12, 2),
+                        "roofline": hbm_roof(by["project"], k_ms["project"])},
             "contract": {"ms": round(k_ms["contract"], 4), "TFLOP_per_s": round(contract_tflops, 2)},
             "epilogue": {"ms": round(k_ms["epilogue"], 4),
-                         "GB_per_s": round(by["epilogue"] / (k_ms["epilogue"] * 1e-3) / 1e9, 1)},
+                         "GB_per_s": round(by["epilogue"] / (k_ms["epilogue"] * 1e-3) / 1e9, 1),
+                         "roofline": hbm_roof(by["epilogue"], k_ms["epilogue"])},
         },
+        "n2048_channel_scaled": c3,
         "backward_contract": None if bwd_ms is None else {"ms": round(bwd_ms, 4),
                               "TFLOP_per_s": round(2 * fl["contract"] / (bwd_ms * 1e-3) / 1e12, 2),
                               "roofline": mfma_roof(2 * fl["contract"], bwd_ms),
@@ -475,6 +591,8 @@ def main():
                                    "contraction, dz and all ten weight gradients; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
+                     "frac_clock_adjusted": None if clk is None else
+                         round(contract_tflops / perf.bf16_peak_at(clk["mean_MHz"]), 4),
                      "traffic": measured_traffic(), "kernel": "k2_contract_ws",
                      "per_launch": f"2*N^3*c = {fl['contract']:.4e} flop (128 channels of one {N}^3 product)"},
         "cpu_baseline": None,

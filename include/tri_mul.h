@@ -102,7 +102,8 @@ typedef struct {
  *   output rows  i in [row0, row0 + rows),  columns j in [col0, col0 + cols),
  *   k-panel      k in [k0, k0 + klen) of n_total tokens.
  * ld_a / ld_b are the row strides (elements) of the a / b panels, >= klen,
- * multiples of 8.  k_index / k_count number the panels of one tile: the call
+ * multiples of 8, at most 65536 (larger strides return TRI_MUL_EUNSUPPORTED:
+ * the kernels address a panel tile with 32-bit byte offsets).  k_index / k_count number the panels of one tile: the call
  * with k_index == 0 overwrites the accumulator, later calls add to it, and
  * the call with k_index == k_count - 1 also runs the epilogue. */
 typedef struct {

@@ -11,6 +11,7 @@
 #include "tri_mul.h"
 #include "opm.h"
 #include "triattn.h"
+#include "tri_mul_check.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -519,6 +520,9 @@ int check_block(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a
         return fail(TRI_MUL_EUNSUPPORTED, "tile sides and k-panel length are limited to %lld", (long long)kMaxN);
     if (v->ld_a < v->klen || v->ld_b < v->klen || (v->ld_a % 8) || (v->ld_b % 8))
         return fail(TRI_MUL_EINVAL, "ld_a / ld_b must be >= klen and multiples of 8");
+    // the kernels address a 256-row panel tile with 32-bit byte offsets
+    if (v->ld_a > kMaxN || v->ld_b > kMaxN)
+        return fail(TRI_MUL_EUNSUPPORTED, "ld_a / ld_b are limited to %lld elements", (long long)kMaxN);
     if (v->k_count < 1 || v->k_index < 0 || v->k_index >= v->k_count) return fail(TRI_MUL_EINVAL, "bad k_index %d / k_count %d", v->k_index, v->k_count);
     if (!aligned16(a_panel) || !aligned16(b_panel) || !aligned16(acc)) return fail(TRI_MUL_EINVAL, "panels and accumulator must be 16-byte aligned");
     const bool last = v->k_index == v->k_count - 1;
@@ -878,6 +882,24 @@ int tri_attn_forward(const void* q, const void* k, const void* v, const void* bi
                      void* stream) {
     const tri_attn_view_t view{rows, n, heads, out_dtype, ld_bias, 0, n, 0, 1};
     return tri_attn_chunk(&view, q, k, v, bias, mask, nullptr, out, stream);
+}
+
+int tri_mul_check_contract_loads(int a_mode, int b_mode, int64_t M, int64_t N, int64_t K, int64_t lda,
+                                 int64_t ldb, int64_t a_stride, int64_t b_stride, int batch, uint64_t a_bytes,
+                                 uint64_t b_bytes, int grid, int all_channels, tri_mul_load_check_t* out) {
+    if (!out) return fail(TRI_MUL_EINVAL, "null out");
+    if (M < 1 || N < 1 || K < 1 || batch < 1 || grid < 1 || M > kMaxN || N > kMaxN || K > kMaxN)
+        return fail(TRI_MUL_EINVAL, "sizes must lie in [1, %lld]", (long long)kMaxN);
+    for (int m : {a_mode, b_mode})
+        if (m < TRI_MUL_OPERAND_BLOCKED || m > TRI_MUL_OPERAND_TRANSPOSED) return fail(TRI_MUL_EINVAL, "bad operand mode %d", m);
+    if ((a_mode == TRI_MUL_OPERAND_ROW_MAJOR && (lda < K || lda % 8 || lda > kMaxN)) ||
+        (b_mode == TRI_MUL_OPERAND_ROW_MAJOR && (ldb < K || ldb % 8 || ldb > kMaxN)))
+        return fail(TRI_MUL_EINVAL, "row-major ld must be >= K, <= %lld and a multiple of 8", (long long)kMaxN);
+    trimul::K2CheckCounts n;
+    trimul::k2_check_loads(a_mode, b_mode, M, N, K, lda, ldb, a_stride, b_stride, batch, a_bytes, b_bytes, grid,
+                           all_channels, n);
+    *out = tri_mul_load_check_t{n.tiles, n.loads, n.elems, n.bad_tiles, n.bad_desc, n.bad_elem};
+    return ok();
 }
 
 }  // extern "C"

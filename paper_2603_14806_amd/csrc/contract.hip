@@ -8,7 +8,10 @@
 // panels arrive unmasked).  The bf16 path runs on gfx950 matrix cores
 // (v_mfma_f32_32x32x16_bf16, fp32 accumulation); the fp32 path is a plain
 // LDS-tiled VALU kernel.
+#include <vector>
+
 #include "common.h"
+#include "k2_addr.h"
 #include "kernels.h"
 
 namespace trimul {
@@ -89,16 +92,19 @@ __global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_pe
 void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
                     int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB, int64_t sC, int tiles_m,
                     int tiles_n, int total, int accumulate, const uint8_t* __restrict__ kmask) {
-    constexpr int BM = 256, MI = 2;
+    constexpr int BM = kK2Tile, MI = 2;
     constexpr int A_ST = BM * ROWB, ST_BYTES = A_ST + B_ST;
     constexpr int STAGES = kLdsBytes / ST_BYTES;  // 5
-    constexpr int LOADS = 8;                     // direct-to-LDS loads per loader wave per step
+    constexpr int LOADS = 2 * kK2LoadsPerOperand;  // direct-to-LDS loads per loader wave per step
     static_assert(!(TA || TB) || (BLOCKED && !KMASK), "transposed operands are blocked and unmasked");
+    // a blocked operand's k-step must be exactly one panel block (256 rows x 32 k)
+    static_assert(!BLOCKED || (BM == kBlkRows && BN == kBlkRows && BK == kBlkK), "blocked tiles are panel blocks");
+    static_assert(BN == kK2Tile && BK == kK2BK && ROWB == kK2Row, "loader addressing assumes this tile");
     __shared__ __attribute__((aligned(16))) char smem[STAGES * ST_BYTES];
 
     const int G = gridDim.x, wg = blockIdx.x;
-    const int perm = (G & 7) == 0 ? (wg & 7) * (G >> 3) + (wg >> 3) : wg;
-    const int my_tiles = perm < total ? (total - 1 - perm) / G + 1 : 0;
+    const int perm = k2_perm(wg, G);
+    const int my_tiles = k2_my_tiles(perm, G, total);
     const int nk = (K + BK - 1) / BK;
     const int steps = my_tiles * nk;
     const int tiles = tiles_m * tiles_n;
@@ -106,77 +112,42 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
 
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // 0 .. 11
-
-    auto decode = [&](int it, int& ch, int& m0, int& n0) {
-        const int L = it * G + perm;
-        ch = L / tiles;
-        const int rem = L - ch * tiles;
-        constexpr int GR = 4;
-        const int gid = rem / (GR * tiles_n);
-        const int first_m = gid * GR;
-        const int gsz = min(tiles_m - first_m, GR);
-        const int in_g = rem - gid * GR * tiles_n;
-        m0 = (first_m + in_g % gsz) * BM;
-        n0 = (in_g / gsz) * BN;
-    };
     const uint32_t lds_base = lds_addr(smem);
 
     if (wave >= 8) {
-        // Loader wave lw: rows 64 lw .. 64 lw + 63 of the A and B blocks as four
-        // 16-row loads each; lane i -> row (i >> 2) of a group, slot (i & 3),
-        // chunk (i & 3) ^ ((row >> 2) & 3).
+        // Loader wave lw: rows 64 lw .. 64 lw + 63 of the A and B halves of a
+        // stage as four 16-row loads each (k2_addr.h).  Every offset is in the
+        // lane offset; the scalar offset is 0.
         const int lw = wave - 8;
-        const int lkc = (lane & 3) ^ ((lane >> 4) & 3);
-        const int rsa = BLOCKED ? BK : lda, rsb = BLOCKED ? BK : ldb;   // elements between rows
-        const uint32_t va = TA ? (uint32_t)(lane * 16) : (uint32_t)(((lw * 64 + (lane >> 2)) * rsa + lkc * 8) * 2);
-        const uint32_t vb = TB ? (uint32_t)(lane * 16) : (uint32_t)(((lw * 64 + (lane >> 2)) * rsb + lkc * 8) * 2);
-        // transposed operand X: 32-column blocks per 256-row tile of X, and
-        // those tiles per channel (X has K rows)
-        const int xs_a = (M + 31) / 32, xs_b = (N + 31) / 32, xt = (K + 255) / 256;
-        const uint32_t a_j = (uint32_t)(16 * rsa * 2), b_j = (uint32_t)(16 * rsb * 2);   // bytes per 16 rows
-        const uint32_t a_k = BLOCKED ? (uint32_t)(BM * BK * 2) : (uint32_t)ROWB;       // bytes per k-step
-        const uint32_t b_k = BLOCKED ? (uint32_t)(BN * BK * 2) : (uint32_t)ROWB;
+        const K2Operand opa{TA ? kK2Transposed : BLOCKED ? kK2Blocked : kK2RowMajor, M, K, lda, sA};
+        const K2Operand opb{TB ? kK2Transposed : BLOCKED ? kK2Blocked : kK2RowMajor, N, K, ldb, sB};
+        const uint32_t la = k2_lane_off(opa, lw, lane), lb = k2_lane_off(opb, lw, lane);
         int l_it = 0, l_kt = 0, l_stage = 0, l_ch = 0, l_m0 = 0, l_n0 = 0;
-        v4i_t ra = buffer_desc(A, 0u), rb = buffer_desc(B, 0u);
         const v4i_t rnone = buffer_desc(A, 0u);
-        auto load_tile = [&]() {
-            int ch, m0, n0;
-            decode(l_it, ch, m0, n0);
-            l_ch = ch;
-            l_m0 = m0;
-            l_n0 = n0;
-            if (BLOCKED) {
-                ra = buffer_desc(A + ((int64_t)ch * tiles_m + m0 / BM) * nk * (BM * BK),
-                                 (uint32_t)(nk * BM * BK * 2));
-                rb = buffer_desc(B + ((int64_t)ch * tiles_n + n0 / BN) * nk * (BN * BK),
-                                 (uint32_t)(nk * BN * BK * 2));
-            } else {   // rows past M (N) fall outside the descriptor and load as zero
-                ra = buffer_desc(A + ch * sA + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 2));
-                rb = buffer_desc(B + ch * sB + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 2));
-            }
+        v4i_t ra = rnone, rb = rnone;
+        auto desc = [&](const bf16_t* X, const K2Operand& op, int t0, int kt) {
+            const K2Desc d = k2_desc(op, l_ch, t0, kt);
+            return buffer_desc(X + d.base, d.range);
         };
-        // Transposed operand: the descriptor covers the 256-row tile of X
-        // that holds step kt (rows past it, or blocks past the last column
-        // block, read as zero).
-        auto tr_desc = [&](const bf16_t* X, int xs, int kt) {
-            return buffer_desc(X + ((int64_t)l_ch * xt + (kt >> 3)) * xs * (256 * 32), (uint32_t)(xs * 256 * 32 * 2));
+        auto load_tile = [&]() {
+            const K2Tile tl = k2_decode(l_it * G + perm, tiles_m, tiles_n);
+            l_ch = tl.ch;
+            l_m0 = tl.m0;
+            l_n0 = tl.n0;
+            if (!TA) ra = desc(A, opa, l_m0, 0);
+            if (!TB) rb = desc(B, opb, l_n0, 0);
         };
         auto issue_step = [&](bool live) {
             const uint32_t st = lds_base + (uint32_t)(l_stage * ST_BYTES);
-            const v4i_t rta = TA ? tr_desc(A, xs_a, l_kt) : ra, rtb = TB ? tr_desc(B, xs_b, l_kt) : rb;
+            const v4i_t rta = TA ? desc(A, opa, l_m0, l_kt) : ra, rtb = TB ? desc(B, opb, l_n0, l_kt) : rb;
 #pragma unroll
-            for (int j = 0; j < LOADS; ++j) {   // j < 4: A groups, j >= 4: B groups
-                const bool isb = j >= 4;
-                uint32_t soff;
-                if (isb ? TB : TA) {   // piece (j & 1) of column block 2 lw + ((j & 3) >> 1) of the tile
-                    const int cb = ((isb ? l_n0 : l_m0) >> 5) + 2 * lw + ((j & 3) >> 1);
-                    soff = (uint32_t)cb * (uint32_t)(256 * 32 * 2) + (uint32_t)((l_kt & 7) * 32 + 16 * (j & 1)) * ROWB;
-                } else {
-                    soff = (uint32_t)(j & 3) * (isb ? b_j : a_j) + (uint32_t)l_kt * (isb ? b_k : a_k);
-                }
-                // (the same LDS offset in both layouts: 1 KB piece lw * 4 + (j & 3))
-                const uint32_t dst = st + (isb ? A_ST : 0) + (uint32_t)(lw * 64 + 16 * (j & 3)) * ROWB;
-                lds_load16(live ? (isb ? rtb : rta) : rnone, isb ? vb : va, soff, dst);
+            for (int j = 0; j < LOADS; ++j) {   // j < 4: A loads, j >= 4: B loads
+                const bool isb = j >= kK2LoadsPerOperand;
+                const int jj = j % kK2LoadsPerOperand;
+                uint32_t off;
+                const bool in = k2_load_off(isb ? opb : opa, isb ? l_n0 : l_m0, l_kt, lw, jj, off);
+                const uint32_t dst = st + (isb ? A_ST : 0) + k2_lds_off(lw, jj);
+                lds_load16((live && in) ? (isb ? rtb : rta) : rnone, (isb ? lb : la) + off, 0u, dst);
             }
         };
         auto advance = [&]() {
@@ -340,8 +311,8 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
 
         // 32x32 accumulator layout: lane holds column (lane & 31) and, in
         // register r, row 8 (r / 4) + 4 (lane / 32) + r % 4.
-        int ch, m0, n0;
-        decode(it, ch, m0, n0);
+        const K2Tile tl = k2_decode(it * G + perm, tiles_m, tiles_n);
+        const int ch = tl.ch, m0 = tl.m0, n0 = tl.n0;
         const int row0 = m0 + wm * 64 + 4 * hi, col0 = n0 + wn * 128 + rl;
         const bool full = m0 + BM <= M && n0 + BN <= N;
         const int64_t jblocks = (N + kResJ - 1) / kResJ;
@@ -554,6 +525,102 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
     }
 #undef K2_WS
     return hipGetLastError();
+}
+
+// Host-side walk over the direct-to-LDS loads of one k2_contract_ws launch,
+// computed with the kernel's own addressing functions (k2_addr.h).
+//
+// Tile order: every (channel, row tile, column tile) must be taken by exactly
+// one (work-group, round) of the persistent grid.  Loads: for the channels in
+// `chans` (the kernel's addressing is the same in every channel apart from
+// the channel offset, so the first and last channel bound it), every row tile
+// of A and every column tile of B, every step, loader wave, load, lane and
+// element: the descriptor must lie inside the operand's allocation (base >= 0,
+// base + range <= bytes, range a multiple of 16), and every element the tile
+// needs (row < rows, k < K) must be inside the range at the byte address the
+// operand's layout gives it.  Elements the tile does not need (rows past the
+// operand, k past K) may read anything inside the range, or zeros.
+namespace {
+int64_t k2_layout_off(const K2Operand& op, int ch, int64_t row, int64_t k) {
+    if (op.mode == kK2Blocked) return panel_off(panel_geom(op.rows, op.K), ch, row, k);
+    if (op.mode == kK2RowMajor) return (int64_t)ch * op.stride + row * op.ld + k;
+    return panel_off(panel_geom(op.K, op.rows), ch, k, row);   // X[k][row] in the panel layout of X
+}
+
+void k2_check_operand(const K2Operand& op, uint64_t bytes, int ch, K2CheckCounts& n) {
+    const int nk = (op.K + kK2BK - 1) / kK2BK;
+    const int tiles = (op.rows + kK2Tile - 1) / kK2Tile;
+    for (int tt = 0; tt < tiles; ++tt) {
+        const int t0 = tt * kK2Tile;
+        for (int kt = 0; kt < nk; ++kt) {
+            const K2Desc d = k2_desc(op, ch, t0, kt);
+            const bool desc_ok = d.base >= 0 && (d.range % 16) == 0 && (uint64_t)d.base * 2 + d.range <= bytes;
+            for (int lw = 0; lw < kK2Loaders; ++lw)
+                for (int jj = 0; jj < kK2LoadsPerOperand; ++jj) {
+                    uint32_t off = 0;
+                    const bool in = k2_load_off(op, t0, kt, lw, jj, off);
+                    ++n.loads;
+                    if (in && !desc_ok) ++n.bad_desc;
+                    const uint32_t lds = k2_lds_off(lw, jj);
+                    for (int lane = 0; lane < 64; ++lane) {
+                        const uint64_t voff = (uint64_t)k2_lane_off(op, lw, lane) + off;
+                        if (voff + 16 > 0xffffffffull) ++n.bad_elem;   // the lane offset is 32-bit
+                        const uint32_t lb = lds + 16u * (uint32_t)lane;   // LDS byte the lane's 16 bytes go to
+                        for (int e = 0; e < 8; ++e) {
+                            int64_t row, k;
+                            if (op.mode == kK2Transposed) {   // 2 KB per 32-column block, 64 bytes per k row
+                                const int blk = (int)(lb / 2048), kr = (int)(lb % 2048) / kK2Row;
+                                row = t0 + 32 * blk + ((lb % kK2Row) / 2 + e);
+                                k = (int64_t)kt * kK2BK + kr;
+                            } else {   // row r, slot s holds chunk s ^ ((r >> 2) & 3)
+                                const int r = (int)(lb / kK2Row), slot = (int)(lb % kK2Row) / 16;
+                                row = t0 + r;
+                                k = (int64_t)kt * kK2BK + 8 * (slot ^ ((r >> 2) & 3)) + e;
+                            }
+                            if (row >= op.rows || k >= op.K) continue;   // not needed by the tile
+                            ++n.elems;
+                            const uint64_t byte = voff + 2u * (uint32_t)e;
+                            const bool hit = in && byte + 2 <= d.range &&
+                                             d.base * 2 + (int64_t)byte == 2 * k2_layout_off(op, ch, row, k);
+                            if (!hit) ++n.bad_elem;
+                        }
+                    }
+                }
+        }
+    }
+}
+}  // namespace
+
+void k2_check_loads(int a_mode, int b_mode, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t sA,
+                    int64_t sB, int batch, uint64_t a_bytes, uint64_t b_bytes, int grid, int all_channels,
+                    K2CheckCounts& n) {
+    n = K2CheckCounts{};
+    const int tm = (int)((M + kK2Tile - 1) / kK2Tile), tn = (int)((N + kK2Tile - 1) / kK2Tile);
+    const int64_t total = (int64_t)tm * tn * batch;
+    std::vector<uint8_t> seen((size_t)total, 0);
+    for (int wg = 0; wg < grid; ++wg) {
+        const int perm = k2_perm(wg, grid), mine = k2_my_tiles(perm, grid, (int)total);
+        for (int it = 0; it < mine; ++it) {
+            const K2Tile t = k2_decode(it * grid + perm, tm, tn);
+            const bool ok = t.ch >= 0 && t.ch < batch && t.m0 >= 0 && t.m0 < M && t.n0 >= 0 && t.n0 < N &&
+                            t.m0 % kK2Tile == 0 && t.n0 % kK2Tile == 0;
+            if (!ok) {
+                ++n.bad_tiles;
+                continue;
+            }
+            uint8_t& v = seen[((size_t)t.ch * tm + t.m0 / kK2Tile) * tn + t.n0 / kK2Tile];
+            if (v) ++n.bad_tiles;
+            v = 1;
+        }
+    }
+    for (uint8_t v : seen) n.bad_tiles += v ? 0 : 1;
+    n.tiles = total;
+    const K2Operand opa{a_mode, (int)M, (int)K, (int)lda, sA}, opb{b_mode, (int)N, (int)K, (int)ldb, sB};
+    for (int ch = 0; ch < batch; ++ch) {
+        if (!all_channels && ch != 0 && ch != batch - 1) continue;
+        k2_check_operand(opa, a_bytes, ch, n);
+        k2_check_operand(opb, b_bytes, ch, n);
+    }
 }
 
 }  // namespace trimul

@@ -48,6 +48,20 @@ hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, 
 hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void* B, float* C, int64_t M, int64_t N,
                                       int64_t K, int batch, int cus, hipStream_t s);
 
+// Host-side check of the contraction kernel's loads (contract.hip): counts of
+// tiles, loads and needed elements visited, and of violations.
+struct K2CheckCounts {
+    int64_t tiles = 0, loads = 0, elems = 0;
+    int64_t bad_tiles = 0;   // tiles taken by no or several (work-group, round) pairs
+    int64_t bad_desc = 0;    // loads whose descriptor reaches outside the operand
+    int64_t bad_elem = 0;    // needed elements read from the wrong address or not at all
+};
+// a_mode / b_mode: 0 blocked panel, 1 row-major [batch][rows][ld] (channel stride sA / sB), 2 transposed
+// (the operand given as X[k][row] in the panel layout of K rows).  a_bytes / b_bytes: allocation sizes.
+void k2_check_loads(int a_mode, int b_mode, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t sA,
+                    int64_t sB, int batch, uint64_t a_bytes, uint64_t b_bytes, int grid, int all_channels,
+                    K2CheckCounts& n);
+
 struct EpilogueArgs {
     const float* C;      // fp32 contraction result: pair-blocked (cblocked) or [c][rows][ldc]
     int cblocked;        // C in the pair-blocked result layout (common.h)

@@ -5,6 +5,12 @@ figures).  A multiply-add counts as 2 flops."""
 PEAK_BF16_TFLOPS = 2516.6      # dense bf16 MFMA: 256 CUs x 4096 flop/clk x 2.4 GHz
 PEAK_FP32_VALU_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+CUS, BF16_FLOP_PER_CLK_CU = 256, 4096
+
+
+def bf16_peak_at(mhz):
+    """Dense bf16 MFMA peak (TFLOP/s) at a graphics clock of `mhz`."""
+    return CUS * BF16_FLOP_PER_CLK_CU * mhz * 1e6 / 1e12
 
 
 def flops(N, c_z=128, c=128):

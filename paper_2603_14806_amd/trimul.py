@@ -56,6 +56,15 @@ class TriAttnView(ctypes.Structure):
                 ("k0", _i64), ("klen", _i64), ("k_index", _i32), ("k_count", _i32)]
 
 
+class LoadCheck(ctypes.Structure):
+    """tri_mul_load_check_t (include/tri_mul_check.h)."""
+    _fields_ = [("tiles", _i64), ("loads", _i64), ("elems", _i64), ("bad_tiles", _i64), ("bad_desc", _i64),
+                ("bad_elem", _i64)]
+
+
+TRI_MUL_OPERAND_BLOCKED, TRI_MUL_OPERAND_ROW_MAJOR, TRI_MUL_OPERAND_TRANSPOSED = 0, 1, 2
+
+
 class Grads(ctypes.Structure):
     """tri_mul_grads_t: device pointers of the float32 weight gradients."""
     _fields_ = [(name, _vp) for name in WEIGHT_FIELDS]
@@ -96,6 +105,9 @@ SIGNATURES = {
                                             ctypes.c_size_t, _vp]),
     "opm_forward_workspace_size": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
     "opm_forward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_check_contract_loads": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64,
+                                                    _i64, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int,
+                                                    ctypes.c_int, ctypes.POINTER(LoadCheck)]),
     "tri_attn_state_size": (ctypes.c_int, [ctypes.POINTER(TriAttnView), ctypes.POINTER(ctypes.c_size_t)]),
     "tri_attn_chunk": (ctypes.c_int, [ctypes.POINTER(TriAttnView), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "tri_attn_forward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, ctypes.c_int32, _i64, ctypes.c_int32,
@@ -535,3 +547,13 @@ def triangle_attention(q, k, v, bias, mask=None, out_dtype="f32", stream=None):
     out = torch.empty((rows, n, heads, 32), dtype=TORCH_DTYPE[DTYPE_CODE[out_dtype]], device=q.device)
     tri_attn_forward(q, k, v, bias, mask, rows, n, heads, bias.stride(1), out_dtype, out, stream)
     return out
+
+
+def check_contract_loads(a_mode, b_mode, M, N, K, lda=0, ldb=0, a_stride=0, b_stride=0, batch=128, a_bytes=0,
+                         b_bytes=0, grid=256, all_channels=False):
+    """Host-side walk over the contraction kernel's loads for one launch shape
+    (tri_mul_check_contract_loads); returns the counts as a dict."""
+    out = LoadCheck()
+    _check(lib().tri_mul_check_contract_loads(a_mode, b_mode, M, N, K, lda, ldb, a_stride, b_stride, batch, a_bytes,
+                                              b_bytes, grid, int(all_channels), ctypes.byref(out)))
+    return {name: getattr(out, name) for name, _ in LoadCheck._fields_}

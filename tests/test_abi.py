@@ -9,7 +9,7 @@ import pytest
 from paper_2603_14806_amd import trimul as T
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADERS = [os.path.join(ROOT, "include", h) for h in ("tri_mul.h", "opm.h", "triattn.h")]
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("tri_mul.h", "opm.h", "triattn.h", "tri_mul_check.h")]
 
 
 def declared_functions():
@@ -103,3 +103,20 @@ def test_last_error_is_thread_local(lib):
     th.join()
     assert seen == [""]
     assert T.last_error() != ""
+
+
+def test_block_view_leading_dimension_bounds(lib):
+    # validation runs before the handle's contents are used, so a dummy
+    # (non-null, never dereferenced) handle reaches the view checks
+    dummy = ctypes.c_void_p(16)
+    base = dict(n_total=4096, row0=0, col0=0, rows=256, cols=256, k0=0, klen=256, k_index=0, k_count=2)
+    v = T.BlockView(**base, ld_a=65536 + 8, ld_b=256)
+    assert lib.tri_mul_block_accumulate(dummy, ctypes.byref(v), 16, 16, 16, None, None, None, None) == \
+        T.TRI_MUL_EUNSUPPORTED
+    assert "65536" in T.last_error()
+    v = T.BlockView(**base, ld_a=256, ld_b=1 << 24)
+    assert lib.tri_mul_block_accumulate(dummy, ctypes.byref(v), 16, 16, 16, None, None, None, None) == \
+        T.TRI_MUL_EUNSUPPORTED
+    v = T.BlockView(**base, ld_a=252, ld_b=256)   # below klen
+    assert lib.tri_mul_block_accumulate(dummy, ctypes.byref(v), 16, 16, 16, None, None, None, None) == \
+        T.TRI_MUL_EINVAL

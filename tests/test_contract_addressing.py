@@ -1,0 +1,131 @@
+"""Host-side walk over the contraction kernel's loads (CPU, no GPU).
+
+The bf16 contraction (Section 3.3, Eq. 2 / Eq. 3) streams both operands into
+LDS with buffer loads; tri_mul_check_contract_loads runs the kernel's own
+addressing functions on the host for one launch shape and counts:
+- tiles taken by no (work-group, round) of the persistent grid, or by several;
+- loads whose buffer descriptor reaches outside the operand's allocation;
+- needed elements (row < rows, k < K) read from a wrong address or not at all.
+Every offset is in the lane offset (the scalar offset is 0), so "inside the
+descriptor" means inside the allocation whichever offsets the hardware's range
+check covers.  The allocation sizes below are written from the layouts'
+definitions, not taken from the library.
+"""
+import pytest
+
+from paper_2603_14806_amd import trimul as T
+
+BLK, ROW, TR = T.TRI_MUL_OPERAND_BLOCKED, T.TRI_MUL_OPERAND_ROW_MAJOR, T.TRI_MUL_OPERAND_TRANSPOSED
+SIZES = [1, 33, 300, 3750, 4096]
+
+
+def ceil(a, b):
+    return -(-a // b)
+
+
+def blocked_bytes(rows, K, nch=128):
+    """[nch][ceil(rows/256)][ceil(K/32)][256][32] bf16."""
+    return nch * ceil(rows, 256) * ceil(K, 32) * 256 * 32 * 2
+
+
+def transposed_bytes(rows, K, nch=128):
+    """The operand given as X[k][row]: the blocked panel of K rows and `rows` columns."""
+    return blocked_bytes(K, rows, nch)
+
+
+def assert_clean(r, expect_tiles):
+    assert r["tiles"] == expect_tiles
+    assert r["bad_tiles"] == 0, r
+    assert r["bad_desc"] == 0, r
+    assert r["bad_elem"] == 0, r
+    assert r["elems"] > 0 and r["loads"] > 0
+
+
+def tiles(M, N, batch=128):
+    return ceil(M, 256) * ceil(N, 256) * batch
+
+
+@pytest.mark.parametrize("n", SIZES)
+def test_full_update_blocked_operands(n):
+    # outgoing and incoming run the same launch: both panels blocked, M = N = K = n
+    b = blocked_bytes(n, n)
+    r = T.check_contract_loads(BLK, BLK, n, n, n, a_bytes=b, b_bytes=b, grid=min(256, tiles(n, n)),
+                               all_channels=n <= 300)
+    assert_clean(r, tiles(n, n))
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("ta", [0, 1])
+def test_backward_products_transposed_operands(n, ta):
+    # dA = dC B (B read transposed from its panel), dB = dC^T A (both transposed)
+    a_mode = TR if ta else BLK
+    a_bytes = transposed_bytes(n, n) if ta else blocked_bytes(n, n)
+    r = T.check_contract_loads(a_mode, TR, n, n, n, a_bytes=a_bytes, b_bytes=transposed_bytes(n, n),
+                               grid=min(256, tiles(n, n)), all_channels=n <= 300)
+    assert_clean(r, tiles(n, n))
+
+
+# device-tile views: (rows, cols, klen, ld); the first is one tile of an 8 x 8
+# grid at N = 30000 (3750-token panels, ld rounded up to 8)
+VIEWS = [(3750, 3750, 3750, 3752), (300, 200, 100, 104), (33, 1, 7, 8), (1, 1, 1, 8), (257, 513, 4096, 4104),
+         (256, 256, 32, 32)]
+
+
+@pytest.mark.parametrize("view", VIEWS)
+def test_block_call_row_major_panels(view):
+    rows, cols, klen, ld = view
+    a_bytes, b_bytes = 128 * rows * ld * 2, 128 * cols * ld * 2
+    r = T.check_contract_loads(ROW, ROW, rows, cols, klen, ld, ld, rows * ld, cols * ld, a_bytes=a_bytes,
+                               b_bytes=b_bytes, grid=min(256, tiles(rows, cols)), all_channels=rows * cols < 1e5)
+    assert_clean(r, tiles(rows, cols))
+
+
+@pytest.mark.parametrize("view", VIEWS)
+def test_block_call_repacked_panels(view):
+    rows, cols, klen, _ = view
+    r = T.check_contract_loads(BLK, BLK, rows, cols, klen, a_bytes=blocked_bytes(rows, klen),
+                               b_bytes=blocked_bytes(cols, klen), grid=min(256, tiles(rows, cols)),
+                               all_channels=rows * cols < 1e5)
+    assert_clean(r, tiles(rows, cols))
+
+
+@pytest.mark.parametrize("shape", [(1024, 1024, 4096), (100, 257, 37), (3, 5, 1)])
+def test_outer_product_mean_launches(shape):
+    # sums: rows (token, c) = ntok * 32, K = sequences; counts: rows = tokens
+    rows, cols, S = shape
+    r = T.check_contract_loads(BLK, BLK, 32 * rows, 32 * cols, S, batch=1, a_bytes=blocked_bytes(32 * rows, S, 1),
+                               b_bytes=blocked_bytes(32 * cols, S, 1), grid=min(256, tiles(32 * rows, 32 * cols, 1)))
+    assert_clean(r, tiles(32 * rows, 32 * cols, 1))
+    r = T.check_contract_loads(BLK, BLK, rows, cols, S, batch=1, a_bytes=blocked_bytes(rows, S, 1),
+                               b_bytes=blocked_bytes(cols, S, 1), grid=min(256, tiles(rows, cols, 1)))
+    assert_clean(r, tiles(rows, cols, 1))
+
+
+@pytest.mark.parametrize("grid", [1, 7, 80, 256, 304, 1000])
+def test_tile_census_any_grid(grid):
+    n = 1000   # 4 x 4 tiles per channel, 2048 tiles
+    b = blocked_bytes(n, n)
+    r = T.check_contract_loads(BLK, BLK, n, n, n, a_bytes=b, b_bytes=b, grid=min(grid, tiles(n, n)))
+    assert_clean(r, tiles(n, n))
+
+
+def test_short_allocation_is_reported():
+    # one 16 KB block short: the last channel's last row tile reaches past the end
+    n = 300
+    b = blocked_bytes(n, n)
+    r = T.check_contract_loads(BLK, BLK, n, n, n, a_bytes=b - 16384, b_bytes=b, grid=tiles(n, n))
+    assert r["bad_desc"] > 0
+    rows, cols, klen, ld = 300, 200, 100, 104
+    r = T.check_contract_loads(ROW, ROW, rows, cols, klen, ld, ld, rows * ld, cols * ld,
+                               a_bytes=128 * rows * ld * 2, b_bytes=128 * cols * ld * 2 - 2, grid=4)
+    assert r["bad_desc"] > 0
+
+
+def test_bad_arguments_rejected():
+    with pytest.raises(T.TriMulError):
+        T.check_contract_loads(ROW, ROW, 10, 10, 100, 96, 104, 960, 1040, a_bytes=1 << 20, b_bytes=1 << 20)
+    with pytest.raises(T.TriMulError):
+        T.check_contract_loads(ROW, ROW, 10, 10, 100, 1 << 20, 104, 10 << 20, 1040, a_bytes=1 << 30,
+                               b_bytes=1 << 20)
+    with pytest.raises(T.TriMulError):
+        T.check_contract_loads(3, BLK, 10, 10, 10, a_bytes=1 << 20, b_bytes=1 << 20)

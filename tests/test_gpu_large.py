@@ -1,9 +1,9 @@
 """GPU parity at the benchmark table's full sizes (N = 2048, N = 4096, and one
 3750 x 3750 tile of an 8 x 8 grid at N = 30000), checked on sampled outputs
-the oracle computes one by one (at N = 2048 also four full output rows; at
-N = 4096 a full row would need the CPU projection of all 16.7M pairs), plus
-the block decomposition of the full
-update (each tile accumulated over k-panels equals the full result)."""
+the oracle computes one by one and on four full output rows (at N = 4096 the
+oracle projects all 16.7M pairs for them, in column chunks on worker
+processes), plus the block decomposition of the full update (each tile
+accumulated over k-panels equals the full result)."""
 import numpy as np
 import pytest
 import torch
@@ -61,10 +61,38 @@ def test_config4_bf16_n4096(direction):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.timeout(900)
+def test_config4_full_rows_n4096():
+    """Four full output rows of each direction at N = 4096 (all 4096 columns,
+    all 128 channels), against oracle.tri_mul over 64-column chunks."""
+    from tests.oracle_pool import tri_mul_rows
+    N = 4096
+    say(f"config 4: bf16 N={N}, four full output rows per direction")
+    layer, W = make_layer("bf16")
+    z = synth.pair_tensor(N, dtype="bf16", device="cuda")
+    R = np.array([0, 1537, 2890, N - 1])
+    Rt = torch.as_tensor(R, device="cuda")
+    got = {}
+    for direction in DIRS:
+        got[direction] = host(layer(z, None, direction)[Rt])
+    torch.cuda.synchronize()
+    say("  device runs done")
+    pieces = ((r0, z[r0:r0 + 256].float().cpu().numpy()) for r0 in range(0, N, 256))
+    ref = tri_mul_rows(pieces, N, np.ones(N), W, DIRS, R, say=say)
+    for direction in DIRS:
+        assert_close(got[direction], ref[direction], "bf16", f"c4 {direction} rows {R.tolist()}")
+    layer.close()
+    del z
+    torch.cuda.empty_cache()
+
+
 def test_config5_tile_of_8x8_grid_n30000():
     """Tile (7, 7) of an 8 x 8 grid at N = 30000: 3750 x 3750 outputs, 8
     k-panels of 3750 tokens, the last 300 tokens padded (rows, columns and the
-    last k-panel).  Panels ~ N(0,1) bf16 generated on the device."""
+    last k-panel).  Panels ~ N(0,1) bf16 generated on the device.  Both
+    entry points run on the same panels: tri_mul_block_accumulate (row-major
+    panels read in place) and tri_mul_block_accumulate_ws (panels repacked
+    through the workspace, the one the benchmark times)."""
     n_total, g = 30000, 8
     b = n_total // g
     row0 = col0 = 7 * b
@@ -81,26 +109,32 @@ def test_config5_tile_of_8x8_grid_n30000():
     z_tile = synth.pair_tensor(0, dtype="bf16", device="cuda", name="z_tile", shape=(b, b, 128))
     acc = torch.empty((128, b, b), dtype=torch.float32, device="cuda")
     out = torch.empty((b, b, 128), dtype=torch.float32, device="cuda")
-    for p in range(g):
-        v = T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g)
-        layer.block_accumulate(v, aps[p], bps[p], acc, mask, z_tile, out)
-    torch.cuda.synchronize()
-    say("  device run done")
     I = sample_index(b, 114, 5, extra=(3449, 3450, 3451, 3700, 3748))
     J = sample_index(b, 114, 6, extra=(3449, 3450, 3451, 3700, 3748))
     It, Jt = torch.as_tensor(I, device="cuda"), torch.as_tensor(J, device="cuda")
     mask_h = host(mask)
     ref_C = oracle.block_contract([host(a[:, It, :b]) for a in aps], [host(bb[:, Jt, :b]) for bb in bps],
                                   [mask_h[p * b:(p + 1) * b] for p in range(g)])
-    got_C = host(acc[:, It][:, :, Jt]).transpose(1, 2, 0)
-    mx, rel = errors(got_C, ref_C)
-    say(f"  accumulator: max_abs={mx:.3e} rel_fro={rel:.3e}")
-    assert rel <= 1e-5
     ref = oracle.block_epilogue(ref_C, oracle.take_pairs(z_tile, I, J), mask_h[row0 + I], mask_h[col0 + J], W)
-    got = host(out[It][:, Jt])
     valid = (mask_h[row0 + I] != 0)[:, None] & (mask_h[col0 + J] != 0)[None, :]
-    assert_close(got[valid], ref[valid], "bf16", "c5 sampled valid pairs")
-    assert np.all(got[~valid] == 0)
+    ws = torch.empty(layer.block_workspace_size(T.BlockView(n_total, row0, col0, b, b, 0, b, ld, ld, 0, g)),
+                     dtype=torch.uint8, device="cuda")
+    for use_ws in (False, True):
+        acc.fill_(float("nan"))   # the first ring step must overwrite every element
+        out.fill_(float("nan"))
+        for p in range(g):
+            v = T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g)
+            layer.block_accumulate(v, aps[p], bps[p], acc, mask, z_tile, out, ws=ws if use_ws else None)
+        torch.cuda.synchronize()
+        say(f"  device run done ({'tri_mul_block_accumulate_ws' if use_ws else 'tri_mul_block_accumulate'})")
+        got_C = host(acc[:, It][:, :, Jt]).transpose(1, 2, 0)
+        mx, rel = errors(got_C, ref_C)
+        say(f"  accumulator: max_abs={mx:.3e} rel_fro={rel:.3e}")
+        assert rel <= 1e-5
+        got = host(out[It][:, Jt])
+        assert_close(got[valid], ref[valid], "bf16", "c5 sampled valid pairs")
+        assert np.all(got[~valid] == 0)
+        assert torch.isfinite(out).all() and torch.isfinite(acc).all()
 
 
 @pytest.mark.parametrize("direction", DIRS)

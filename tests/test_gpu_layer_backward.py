@@ -2,11 +2,14 @@
 tri_mul_incoming_backward, bf16 storage) against the fp64 oracle
 (oracle.tri_mul_backward): dz and all ten weight gradients.
 
-Tolerance (bf16 path): relative Frobenius error <= 1e-2 for every gradient.
-Derivation: beyond fp32 arithmetic, a gradient passes through at most four
-bf16 roundings of independent values (the recomputed a/b operands, dC, and
-the two operands of a weight-gradient sum), each <= 2^-9 relative per element
-(about 1.1e-3 RMS), i.e. <= ~4.5e-3 RMS in total; the bar leaves a factor ~2.
+Tolerance (bf16 path): relative Frobenius error <= 5e-3 for every gradient
+(the forward's bar).  Derivation: beyond fp32 arithmetic, a gradient passes
+through at most four bf16 roundings of independent values (the recomputed a/b
+operands, dC, and the two operands of a weight-gradient sum; for dz the a/b
+operands, dC and its own bf16 storage), each with a relative error uniform in
++-2^-9 per element, i.e. 2^-9 / sqrt(3) = 1.1e-3 RMS; independent roundings
+add in quadrature to 2.3e-3, and the LayerNorm backward's centring can raise
+that by a small factor.  Measured: at most 3.5e-3 (N = 1 ... 1024).
 Pairs with a masked token must get exactly zero dz."""
 import numpy as np
 import pytest
@@ -18,7 +21,7 @@ from paper_2603_14806_amd import trimul as T
 from tests.gpu_util import errors, host, make_layer, say
 
 pytestmark = pytest.mark.gpu
-REL = 1e-2
+REL = 5e-3
 
 
 def grads_vs_oracle(N, direction, masked, seed):
@@ -52,6 +55,48 @@ def test_layer_backward_matches_oracle(direction, N, masked):
     dead = (mask[:, None] == 0) | (mask[None, :] == 0)
     assert np.all(dz[dead] == 0.0)
     say(f"  worst rel_fro {worst:.3e}")
+
+
+@pytest.mark.timeout(900)
+def test_layer_backward_n1024_both_directions():
+    """The layer backward at N = 1024 (32 768 units of 32 pairs: more than
+    100 units per work-group of every per-pair kernel), masked, both
+    directions, against the fp64 oracle computed in two worker processes
+    while the GPU runs."""
+    from tests.oracle_pool import backward_pair
+    N = 1024
+    say(f"layer backward N={N}, both directions, masked")
+    layer, W = make_layer("bf16", "f32", affine=True, seed=11)
+    z = synth.pair_tensor(N, dtype="bf16", seed=11)
+    rng = np.random.default_rng(11)
+    mask = np.ones(N, dtype=np.uint8)
+    mask[rng.choice(N, size=N // 10, replace=False)] = 0
+    dout = rng.standard_normal((N, N, 128)).astype(np.float32)
+    ex, futs = backward_pair(z.float().numpy(), mask, W, dout)
+    try:
+        zd, md, dd = z.cuda(), torch.tensor(mask, device="cuda"), torch.tensor(dout, device="cuda")
+        got = {}
+        for direction in ("outgoing", "incoming"):
+            dz, g = layer.backward(zd, dd, md, direction)
+            got[direction] = (host(dz), {k: host(v) for k, v in g.items()})
+        torch.cuda.synchronize()
+        say("  device runs done")
+        dead = (mask[:, None] == 0) | (mask[None, :] == 0)
+        for direction in ("outgoing", "incoming"):
+            ref = futs[direction].result()
+            dz, g = got[direction]
+            worst = 0.0
+            for k in ["dz"] + list(oracle.WEIGHT_NAMES):
+                v = dz if k == "dz" else g[k]
+                mx, rel = errors(v, ref[k])
+                assert np.all(np.isfinite(v)), k
+                worst = max(worst, rel)
+                assert rel <= REL, f"{direction} {k}: relative Frobenius error {rel:.3e} > {REL}"
+            assert np.all(dz[dead] == 0.0)
+            say(f"  {direction}: worst rel_fro {worst:.3e}")
+    finally:
+        ex.shutdown(wait=True, cancel_futures=True)
+    layer.close()
 
 
 def test_layer_backward_n4096_runs_deterministic():
