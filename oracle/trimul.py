@@ -58,14 +58,11 @@ def layer_norm(v, gamma, beta, eps=EPS):
 
 
 def sigmoid(t):
-    """Logistic function 1 / (1 + exp(-t)), evaluated without overflow."""
+    """Logistic function 1 / (1 + exp(-t)), evaluated without overflow:
+    with e = exp(-|t|), 1 / (1 + e) for t >= 0 and e / (1 + e) for t < 0."""
     t = f64(t)
-    out = np.empty_like(t)
-    pos = t >= 0
-    out[pos] = 1.0 / (1.0 + np.exp(-t[pos]))
-    e = np.exp(t[~pos])
-    out[~pos] = e / (1.0 + e)
-    return out
+    e = np.exp(-np.abs(t))
+    return np.where(t >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
 
 
 def pair_mask(mask_rows, mask_cols=None):
@@ -80,6 +77,11 @@ def linear(x, w):
     return f64(x) @ f64(w).T
 
 
+def gated(x, m_pairs, w_gate, w_val):
+    """One gated projection of normalised pairs x: m * sigmoid(W_gate x) * (W_val x)."""
+    return f64(m_pairs)[..., None] * sigmoid(linear(x, w_gate)) * linear(x, w_val)
+
+
 def project(z_pairs, m_pairs, W, eps=EPS):
     """Input LayerNorm and the two gated projections plus the output gate for a
     block of pairs (Section 3.3: a, b are gated projections of z).
@@ -87,9 +89,8 @@ def project(z_pairs, m_pairs, W, eps=EPS):
     z_pairs: [..., c_z]; m_pairs: [...] pair mask.  Returns (a, b, g) with
     a, b: [..., c] and g: [..., c_z]."""
     x = layer_norm(z_pairs, W["ln_in_w"], W["ln_in_b"], eps)
-    m = f64(m_pairs)[..., None]
-    a = m * sigmoid(linear(x, W["w_ga"])) * linear(x, W["w_a"])
-    b = m * sigmoid(linear(x, W["w_gb"])) * linear(x, W["w_b"])
+    a = gated(x, m_pairs, W["w_ga"], W["w_a"])
+    b = gated(x, m_pairs, W["w_gb"], W["w_b"])
     g = sigmoid(linear(x, W["w_g"]))
     return a, b, g
 
@@ -147,20 +148,24 @@ def tri_mul(z, mask, W, direction, rows=None, cols=None, eps=EPS):
     N = z.shape[0]
     rows = np.arange(N) if rows is None else np.asarray(rows)
     cols = np.arange(N) if cols is None else np.asarray(cols)
+    def ln(pairs):
+        return layer_norm(pairs, W["ln_in_w"], W["ln_in_b"], eps)
+
+    # each block of pairs gets only the projection the update reads from it
     if direction == "outgoing":
         # a[i, k] for i in rows, all k; b[j, k] for j in cols, all k.
-        a, _, _ = project(take_pairs(z, rows), pair_mask(mask[rows], mask), W, eps)
-        _, b, _ = project(take_pairs(z, cols), pair_mask(mask[cols], mask), W, eps)
+        a = gated(ln(take_pairs(z, rows)), pair_mask(mask[rows], mask), W["w_ga"], W["w_a"])
+        b = gated(ln(take_pairs(z, cols)), pair_mask(mask[cols], mask), W["w_gb"], W["w_b"])
         C = contract_outgoing(a, b)
     elif direction == "incoming":
         # a[k, i] for i in rows, all k; b[k, j] for j in cols, all k.
-        a, _, _ = project(take_pairs(z, None, rows), pair_mask(mask, mask[rows]), W, eps)
-        _, b, _ = project(take_pairs(z, None, cols), pair_mask(mask, mask[cols]), W, eps)
+        a = gated(ln(take_pairs(z, None, rows)), pair_mask(mask, mask[rows]), W["w_ga"], W["w_a"])
+        b = gated(ln(take_pairs(z, None, cols)), pair_mask(mask, mask[cols]), W["w_gb"], W["w_b"])
         C = contract_incoming(a, b)
     else:
         raise ValueError(f"direction must be 'outgoing' or 'incoming', got {direction!r}")
     m_out = pair_mask(mask[rows], mask[cols])
-    _, _, g = project(take_pairs(z, rows, cols), m_out, W, eps)
+    g = sigmoid(linear(ln(take_pairs(z, rows, cols)), W["w_g"]))
     return epilogue(C, g, m_out, W, eps)
 
 
