@@ -11,15 +11,13 @@ import torch
 import oracle
 from paper_2603_14806_amd import synth
 from paper_2603_14806_amd.trimul import TriMul
+from tests.progress import say  # noqa: F401  (re-exported for the tests)
 
 TOL = {"f32": dict(max_abs=None, rel_fro=1e-5), "bf16": dict(max_abs=2e-2, rel_fro=5e-3)}
 
 needs_gpu = pytest.mark.skipif(not torch.cuda.is_available(), reason="no GPU visible")
 
 
-def say(*a):
-    print(*a, flush=True)
-    sys.stdout.flush()
 
 
 def errors(got, ref):

@@ -5,13 +5,13 @@ never torch or the GPU library).
 - full output rows of the N = 4096 update: oracle.tri_mul over column chunks,
   each worker reading the pair tensor from a float32 memory-mapped .npy file
   (exact: every bf16 value is a float32 value);
-- the layer backward at N = 1024: one oracle.tri_mul_backward per direction,
+- the layer backward at N = 512: one oracle.tri_mul_backward per direction,
   the two in parallel.
 """
 import os
 import shutil
 import tempfile
-from concurrent.futures import ProcessPoolExecutor
+from concurrent.futures import ProcessPoolExecutor, as_completed
 import multiprocessing as mp
 
 import numpy as np
@@ -56,7 +56,7 @@ def scratch_dir(nbytes):
     raise RuntimeError(f"no scratch directory with {nbytes / 1e9:.1f} GB free")
 
 
-def tri_mul_rows(z_rows_f32, N, mask, W, directions, rows, chunk=64, workers=12, say=print):
+def tri_mul_rows(z_rows_f32, N, mask, W, directions, rows, chunk=64, workers=15, say=print):
     """oracle.tri_mul(z, mask, W, direction, rows, all columns) for each
     direction, with z given as an iterator of (r0, float32 rows) pieces.
     Returns {direction: [len(rows)][N][c_z] float64}."""
@@ -70,17 +70,16 @@ def tri_mul_rows(z_rows_f32, N, mask, W, directions, rows, chunk=64, workers=12,
         zm.flush()
         del zm
         say(f"  pair tensor written to {path}")
-        out = {}
+        out = {d: np.empty((len(rows), N, 128)) for d in directions}
         with _pool(workers, 1) as ex:
-            for direction in directions:
-                futs = [(c0, ex.submit(_rows_chunk, path, mask, W, direction, rows, np.arange(c0, min(N, c0 + chunk))))
-                        for c0 in range(0, N, chunk)]
-                res = np.empty((len(rows), N, 128))
-                for c0, f in futs:
-                    r = f.result()
-                    res[:, c0:c0 + r.shape[1]] = r
-                out[direction] = res
-                say(f"  oracle rows done: {direction}")
+            futs = {ex.submit(_rows_chunk, path, mask, W, d, rows, np.arange(c0, min(N, c0 + chunk))): (d, c0)
+                    for d in directions for c0 in range(0, N, chunk)}
+            for n, f in enumerate(as_completed(futs), 1):
+                d, c0 = futs[f]
+                r = f.result()
+                out[d][:, c0:c0 + r.shape[1]] = r
+                if n % 8 == 0 or n == len(futs):
+                    say(f"  oracle column chunks done: {n} of {len(futs)}")
         return out
     finally:
         shutil.rmtree(d, ignore_errors=True)
