@@ -14,8 +14,8 @@ a small factor.  With one to four valid pairs (N = 1, 2) nothing averages
 over pairs: each of the 128 or 16384 entries of a weight gradient is then one
 or a few products, and the relative error of the whole gradient is that of a
 single pair's rounding pattern, which fluctuates around the same RMS with a
-wider spread; the bar there is 1e-2.  Measured: 2.5e-3 to 3.5e-3 for
-N = 33 ... 512, 3.9e-3 to 5.9e-3 for N = 1, 2.
+wider spread; the bar there is 1e-2.  Measured (worst gradient per case):
+3.3e-3 to 3.4e-3 for N = 33 ... 512, 3.9e-3 to 6.9e-3 for N = 1, 2.
 Pairs with a masked token must get exactly zero dz."""
 import numpy as np
 import pytest
