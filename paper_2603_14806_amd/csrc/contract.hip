@@ -87,11 +87,28 @@ __device__ __forceinline__ bf16x8_t lds_read_tr8(const char* p) {
 // column 16 (g & 1) + 4 a + b of rows 8 (g >> 1) .. + 3 -- the MFMA operand
 // layout, 4 of its 8 k values; a second read 4 rows further gives the rest.
 // A half-wave reads 256 contiguous bytes: no bank conflicts.
+// Round pacing.  The work-groups of one XCD share their round's A row
+// panels and B column panels through that XCD's L2 only while they stream
+// the same k range; left alone they drift apart (measured: up to ~100 us,
+// about 100 k-steps, within a few rounds, far beyond the ~20 k-steps of
+// operand traffic the L2 holds), and every lagging tile then refetches its
+// panels from memory.  So at the start of every full round each work-group
+// counts in on its XCD's counter and waits until all G / 8 of them have (a
+// bounded wait: 20 us, after which it goes on anyway -- pacing changes only
+// where the data comes from, never the results).  One 128-byte line per XCD;
+// reset by k_pace_reset before every paced launch.  Concurrent contraction
+// launches on one device share the counters and then mostly wait the bound.
+constexpr int kPaceLine = 32;   // counters per 128-byte line
+__device__ unsigned int g_k2_pace[8 * kPaceLine];
+__global__ void k_pace_reset() {
+    if (threadIdx.x < 8 * kPaceLine) g_k2_pace[threadIdx.x] = 0u;
+}
+
 template <bool BLOCKED, bool KMASK, bool CBLOCKED, bool TA = false, bool TB = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(768, 768), amdgpu_waves_per_eu(3, 3)))
 void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, float* __restrict__ C, int M,
                     int N, int K, int lda, int ldb, int64_t ldc, int64_t sA, int64_t sB, int64_t sC, int tiles_m,
-                    int tiles_n, int total, int accumulate, const uint8_t* __restrict__ kmask) {
+                    int tiles_n, int total, int accumulate, const uint8_t* __restrict__ kmask, int pace) {
     constexpr int BM = kK2Tile, MI = 2;
     constexpr int A_ST = BM * ROWB, ST_BYTES = A_ST + B_ST;
     constexpr int STAGES = kLdsBytes / ST_BYTES;  // 5
@@ -130,6 +147,18 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
             return buffer_desc(X + d.base, d.range);
         };
         auto load_tile = [&]() {
+            if (pace && lw == 0 && l_it > 0 && (l_it + 1) * G <= total) {   // every full round but the first
+                unsigned int* cnt = &g_k2_pace[(wg & 7) * kPaceLine];
+                const unsigned int target = (unsigned int)l_it * (unsigned int)(G >> 3);
+                if (lane == 0) atomicAdd(cnt, 1u);
+                const uint64_t t0 = __builtin_amdgcn_s_memrealtime();   // 100 MHz
+                while (true) {
+                    const unsigned int v = __builtin_amdgcn_readfirstlane(
+                        __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                    if (v >= target || __builtin_amdgcn_s_memrealtime() - t0 > 2000u) break;
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
             const K2Tile tl = k2_decode(l_it * G + perm, tiles_m, tiles_n);
             l_ch = tl.ch;
             l_m0 = tl.m0;
@@ -458,15 +487,27 @@ hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t k
     return hipGetLastError();
 }
 
+// Pacing needs whole XCD groups (G a multiple of 8, all resident) and at
+// least two full rounds; it resets the counters first (a kernel, not a
+// memset, so that the sequence can be captured in a graph).
+namespace {
+int pace_launch(int grid, int total, hipStream_t s) {
+    if ((grid & 7) != 0 || total < 2 * grid) return 0;
+    hipLaunchKernelGGL(k_pace_reset, dim3(1), dim3(8 * kPaceLine), 0, s);
+    return 1;
+}
+}  // namespace
+
 hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
                                         int batch, int accumulate, int cus, hipStream_t s) {
     constexpr int BM = 256;
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
     const int grid = total < cus ? total : cus;
+    const int pace = pace_launch(grid, total, s);
     hipLaunchKernelGGL((k2_contract_ws<true, false, false>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A,
                        (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, N, (int64_t)0, (int64_t)0, M * N, tm, tn,
-                       total, accumulate, (const uint8_t*)nullptr);
+                       total, accumulate, (const uint8_t*)nullptr, pace);
     return hipGetLastError();
 }
 
@@ -476,10 +517,12 @@ hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void*
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
     const int grid = total < cus ? total : cus;
+    if (!tb) return hipErrorInvalidValue;
+    const int pace = pace_launch(grid, total, s);
 #define K2_TR(TA_, TB_)                                                                                             \
     hipLaunchKernelGGL((k2_contract_ws<true, false, true, TA_, TB_>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A, \
                        (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, (int64_t)0, (int64_t)0, (int64_t)0,     \
-                       (int64_t)0, tm, tn, total, 0, (const uint8_t*)nullptr)
+                       (int64_t)0, tm, tn, total, 0, (const uint8_t*)nullptr, pace)
     if (!ta && tb) K2_TR(false, true);
     else if (ta && tb) K2_TR(true, true);
     else return hipErrorInvalidValue;
@@ -513,9 +556,10 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
     const int grid = total < cus ? total : cus;
     const bf16_t* a = (const bf16_t*)A;
     const bf16_t* b = (const bf16_t*)B;
+    const int pace = pace_launch(grid, total, s);
 #define K2_WS(BL, KM)                                                                                              \
     hipLaunchKernelGGL((k2_contract_ws<BL, KM, BL>), dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K, \
-                       (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask)
+                       (int)lda, (int)ldb, ldc, sA, sB, sC, tm, tn, total, accumulate, kmask, pace)
     if (kmask) {
         if (blocked) K2_WS(true, true);
         else K2_WS(false, true);
