@@ -144,6 +144,26 @@ int tri_mul_outgoing(tri_mul_handle_t h, const void* z, const uint8_t* mask, int
 int tri_mul_incoming(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
                      void* out, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, hosts that forbid hipMalloc): the full update
+ * of tri_mul_outgoing (direction TRI_MUL_OUTGOING) or tri_mul_incoming
+ * (TRI_MUL_INCOMING), with the same z, mask, N, out and stream arguments and
+ * the same results, but no workspace argument.  The workspace lives in a
+ * fixed device scratch array of 256 MiB (268435456 bytes) that every GPU the
+ * library runs on holds until the process ends; the call itself allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine).
+ *   - N is limited to sizes whose tri_mul_workspace_size fits the scratch
+ *     (bf16 storage: N <= 512); larger N returns TRI_MUL_EUNSUPPORTED.
+ *   - Every call on one GPU shares that GPU's scratch, which keeps the last
+ *     call's contents: calls that overlap in time on one GPU (different
+ *     streams, threads or handles) race and corrupt each other's results.
+ *     Serialise them (one stream, or events between streams).
+ *   - The scratch needs no clearing: every element a call reads was written
+ *     earlier in the same call.
+ * Errors: those of tri_mul_outgoing, plus TRI_MUL_EINVAL for a bad direction. */
+int tri_mul_update_noalloc(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                           int32_t direction, void* out, void* stream);
+
 /* One ring step of one device tile (Section 3.3, Fig. 2b):
  *   acc (+)= A_c * diag(m_k) * B_c^T   for every hidden channel c
  *   a_panel  [c][rows][ld_a]  dtype, a_panel[c][i][k] = a at (row0+i, k0+k)

@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -146,6 +147,35 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
     return ok();
 }
 
+// ------------------------------------------------ no-allocation entry point
+//
+// Device scratch of tri_mul_update_noalloc: the workspace of the full update
+// (A and B panels, fp32 result), kScratchBytes per GPU, held from the
+// library's load until the process ends.  Host code never uses the array's
+// name as an address: each device's copy is reached through the pointer
+// hipGetSymbolAddress returned with that device current (g_scratch).
+constexpr size_t kScratchBytes = size_t(256) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The current device's scratch address, resolved once per device.
+int scratch_for(int device, void** ptr) {
+    if (device < 0 || device >= kMaxDevices) return fail(TRI_MUL_EUNSUPPORTED, "device %d outside [0, %d)", device, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[device]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "scratch symbol address");
+        if (!p) return fail(TRI_MUL_EHIP, "scratch symbol address is null");
+        g_scratch[device] = p;
+    }
+    *ptr = g_scratch[device];
+    return TRI_MUL_OK;
+}
+
 // Workspace of the layer backward (bf16 path), in this order: A, B and the
 // four operands of the contraction backward (panels), C, dA, dB (result
 // layout), dx_g [N*N][c_z] fp32, nine unit-block tensors, and the partial
@@ -279,6 +309,11 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
     if (e != hipSuccess) {
         delete h;
         return hip_fail(e, "device query");
+    }
+    void* scr = nullptr;   // the no-allocation entry point's scratch on this device
+    if (int rc = scratch_for(h->device, &scr)) {
+        delete h;
+        return rc;
     }
 
     const int cz = p->c_z, c = p->c;
@@ -416,6 +451,24 @@ int tri_mul_outgoing(tri_mul_handle_t h, const void* z, const uint8_t* mask, int
 int tri_mul_incoming(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, void* out, void* ws,
                      size_t ws_bytes, void* stream) {
     return run_full(h, z, mask, N, out, ws, ws_bytes, stream, 1);
+}
+
+int tri_mul_update_noalloc(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, int32_t direction,
+                           void* out, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (direction != TRI_MUL_OUTGOING && direction != TRI_MUL_INCOMING) return fail(TRI_MUL_EINVAL, "bad direction %d", direction);
+    if (int rc = check_n(N)) return rc;
+    size_t need = 0;
+    if (int rc = tri_mul_workspace_size(h, N, &need)) return rc;
+    if (need > kScratchBytes)
+        return fail(TRI_MUL_EUNSUPPORTED, "N = %lld needs %zu bytes of workspace; the no-allocation scratch holds %zu",
+                    (long long)N, need, kScratchBytes);
+    int device = 0;
+    const hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(e, "device query");
+    void* ws = nullptr;
+    if (int rc = scratch_for(device, &ws)) return rc;
+    return run_full(h, z, mask, N, out, ws, kScratchBytes, stream, direction);
 }
 
 int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, int32_t direction,

@@ -79,6 +79,7 @@ SIGNATURES = {
     "tri_mul_panel_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
     "tri_mul_outgoing": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
     "tri_mul_incoming": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_update_noalloc": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp]),
     "tri_mul_block_accumulate": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "tri_mul_block_workspace_size": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), ctypes.POINTER(ctypes.c_size_t)]),
     "tri_mul_block_accumulate_ws": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
@@ -196,6 +197,10 @@ def tri_mul_outgoing(h, z, mask, N, out, ws, ws_bytes, stream=None):
 
 def tri_mul_incoming(h, z, mask, N, out, ws, ws_bytes, stream=None):
     _check(lib().tri_mul_incoming(h, _ptr(z), _ptr(mask), N, _ptr(out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def tri_mul_update_noalloc(h, z, mask, N, direction, out, stream=None):
+    _check(lib().tri_mul_update_noalloc(h, _ptr(z), _ptr(mask), N, direction, _ptr(out), _stream(stream)))
 
 
 def tri_mul_block_accumulate(h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, stream=None):
