@@ -366,7 +366,7 @@ def main():
         del z3
         print(f"[bench] N=2048 channel-scaled layer {c3['ms_per_layer']:.3f} ms", file=sys.stderr, flush=True)
 
-    bwd_ms = lbwd_ms = sbwd_ms = opm_ms = ta_ms = tile_ms = None
+    bwd_ms = lbwd_ms = sbwd_ms = opm_ms = ta_ms = tile_ms = tile_ws_ms = None
     ta_scores = 2048 * 4 * 2048 * 2048
     opm_flops = 2 * 4096 * (1024 * 32) ** 2
     if not args.no_extras:
@@ -479,22 +479,55 @@ def main():
         tws = torch.empty(layer.block_workspace_size(T.BlockView(bn, brow, brow, bb, bb, 0, bb, bld, bld, 0, bg)),
                           dtype=torch.uint8, device=dev)
 
-        def ring_tile():
-            for p in range(bg):
-                v = T.BlockView(bn, brow, brow, bb, bb, p * bb, bb, bld, bld, p, bg)
-                layer.block_accumulate(v, bpa[p & 1], bpb[p & 1], bacc, bmask, bz, bout, stream, ws=tws)
+        bviews = [T.BlockView(bn, brow, brow, bb, bb, p * bb, bb, bld, bld, p, bg) for p in range(bg)]
 
-        ring_tile()
-        t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0e.record(stream)
-        for _ in range(2):
-            ring_tile()
-        t1e.record(stream)
-        torch.cuda.synchronize()
-        tile_ms = t0e.elapsed_time(t1e) / 2
-        del bpa, bpb, bz, bacc, bout, tws
+        def ring_tile_ws():   # one stream: repack, contraction, (epilogue) per step
+            for p in range(bg):
+                layer.block_accumulate(bviews[p], bpa[p & 1], bpb[p & 1], bacc, bmask, bz, bout, stream, ws=tws)
+
+        # the pipelined ring step: panel p + 1 repacked on a second stream while
+        # panel p is contracted (on 32 fewer compute units) into the packed
+        # accumulator; two workspaces, ordered by events
+        tws2 = torch.empty_like(tws)
+        pacc = torch.empty(layer.block_accumulator_size(bviews[0]) // 4, dtype=torch.float32, device=dev)
+        side = torch.cuda.Stream()
+
+        def ring_tile():
+            packed = [torch.cuda.Event() for _ in range(bg)]
+            done = [torch.cuda.Event() for _ in range(bg)]
+            wss = (tws, tws2)
+            layer.block_repack(bviews[0], bpa[0], bpb[0], bmask, wss[0], stream)
+            packed[0].record(stream)
+            side.wait_stream(stream)
+            for p in range(bg):
+                if p + 1 < bg:
+                    if p >= 1:
+                        side.wait_event(done[p - 1])
+                    layer.block_repack(bviews[p + 1], bpa[(p + 1) & 1], bpb[(p + 1) & 1], bmask, wss[(p + 1) % 2],
+                                       side)
+                    packed[p + 1].record(side)
+                stream.wait_event(packed[p])
+                layer.block_accumulate_packed(bviews[p], wss[p % 2], pacc, bmask, bz, bout,
+                                              reserve_cus=32 if p + 1 < bg else 0, stream=stream)
+                done[p].record(stream)
+            stream.wait_stream(side)
+
+        def time_ring(fn):
+            fn()
+            t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0e.record(stream)
+            for _ in range(2):
+                fn()
+            t1e.record(stream)
+            torch.cuda.synchronize()
+            return t0e.elapsed_time(t1e) / 2
+
+        tile_ms = time_ring(ring_tile)
+        tile_ws_ms = time_ring(ring_tile_ws)
+        del bpa, bpb, bz, bacc, bout, tws, tws2, pacc
         torch.cuda.empty_cache()
-        print(f"[bench] ring tile {tile_ms:.3f} ms", file=sys.stderr, flush=True)
+        print(f"[bench] ring tile {tile_ms:.3f} ms (one-stream repacking entry point {tile_ws_ms:.3f} ms)",
+              file=sys.stderr, flush=True)
 
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
@@ -571,9 +604,13 @@ def main():
         "ring_tile": None if tile_ms is None else {"ms": round(tile_ms, 4),
                       "TFLOP_per_s": round(tile_flops / (tile_ms * 1e-3) / 1e12, 2),
                       "roofline": mfma_roof(tile_flops, tile_ms),
-                      "what": "tile (7,7) of an 8x8 grid at N=30000: 8 tri_mul_block_accumulate_ws ring steps (3750x3750 "
-                              "outputs, 3750-token k-panels, 128 channels; 108.0 TFLOP contraction) with the "
-                              "epilogue on the last step; fp32 accumulator and output; not part of ms_per_step"},
+                      "ms_one_stream_ws": round(tile_ws_ms, 4),
+                      "what": "tile (7,7) of an 8x8 grid at N=30000: 8 ring steps (3750x3750 outputs, 3750-token "
+                              "k-panels, 128 channels; 108.0 TFLOP contraction) through tri_mul_block_repack + "
+                              "tri_mul_block_accumulate_packed, the next panel's repack on a second stream while "
+                              "the current one is contracted on 224 CUs (32 left to the repack), packed fp32 accumulator, epilogue on the "
+                              "last step, fp32 output (ms_one_stream_ws: the same steps through "
+                              "tri_mul_block_accumulate_ws on one stream); not part of ms_per_step"},
         "backward_layer_saved": None if sbwd_ms is None else {"ms": round(sbwd_ms, 4),
                            "roofline": {"bound": "mfma + hbm", "floor_ms": round(bws_["floor_ms"], 3),
                                         "frac": round(bws_["floor_ms"] / sbwd_ms, 4),

@@ -183,11 +183,12 @@ int tri_mul_block_accumulate(tri_mul_handle_t h, const tri_mul_block_view_t* v,
                              const uint8_t* mask, const void* z_tile, void* out_tile,
                              void* stream);
 
-/* Bytes of device workspace tri_mul_block_accumulate_ws needs for the view's
- * sizes (rows, cols, klen): both panels repacked, masked, into the blocked
- * operand layout (see tri_mul_project), 128 * ceil(rows/256) *
- * ceil(klen/32) * 16 KB + the same for cols, each part 256-byte aligned; 0
- * for the fp32 path.  *bytes is a HOST pointer. */
+/* Bytes of device workspace tri_mul_block_accumulate_ws and
+ * tri_mul_block_repack need for the view's sizes (rows, cols, klen): both
+ * panels repacked, masked, into the blocked operand layout (see
+ * tri_mul_project), 128 * ceil(rows/256) * ceil(klen/32) * 16 KB + the same
+ * for cols, and the staged k-mask (ceil(klen/32) * 32 bytes), each part
+ * 256-byte aligned; 0 for the fp32 path.  *bytes is a HOST pointer. */
 int tri_mul_block_workspace_size(tri_mul_handle_t h, const tri_mul_block_view_t* v, size_t* bytes);
 
 /* The same ring step as tri_mul_block_accumulate (same arguments, results
@@ -200,6 +201,44 @@ int tri_mul_block_accumulate_ws(tri_mul_handle_t h, const tri_mul_block_view_t* 
                                 const void* a_panel, const void* b_panel, float* acc,
                                 const uint8_t* mask, const void* z_tile, void* out_tile,
                                 void* ws, size_t ws_bytes, void* stream);
+
+/* The ring step of tri_mul_block_accumulate_ws split in two, with the
+ * accumulator in the pair-blocked result layout, so that a caller can
+ * repack the next k-panel on a second stream while the current one is
+ * contracted (Section 3.3, Fig. 2b: each ring step adds one panel product
+ * into the output block; the repack of panel p + 1 has no dependence on
+ * the product of panel p).  bf16 storage path only (else
+ * TRI_MUL_EUNSUPPORTED).
+ *
+ * tri_mul_block_accumulator_size: bytes of the packed accumulator for the
+ *   view's rows and cols: element (hidden channel c, tile row i, tile
+ *   column j) at ((i * J + j / 32) * 128 + c) * 32 + j % 32 floats, J =
+ *   ceil(cols / 32) (the result layout of tri_mul_contract); rows * J * 32 *
+ *   128 * 4 bytes.  *bytes is a HOST pointer.
+ * tri_mul_block_repack: repacks a_panel and b_panel (the arguments of
+ *   tri_mul_block_accumulate), with the k-range of mask applied, into ws
+ *   (tri_mul_block_workspace_size bytes, 256-byte aligned; TRI_MUL_ENOMEM if
+ *   smaller).  Only the view's sizes, k0 and strides are used.
+ * tri_mul_block_accumulate_packed: acc (+)= the product of the panels
+ *   repacked in ws by tri_mul_block_repack for the same view (overwritten
+ *   when k_index == 0, accumulated into otherwise); when k_index ==
+ *   k_count - 1 also the epilogue into out_tile, as tri_mul_block_accumulate.
+ *   reserve_cus compute units (0 .. CUs - 8) are left to concurrent work,
+ *   e.g. the next panel's repack on another stream (the contraction runs on
+ *   the rest, rounded down to a multiple of 8).  acc is 16-byte aligned.
+ * The caller orders the calls with events: the repack of a panel before its
+ * accumulate, and a workspace reused only after the accumulate that read it
+ * has finished.  tri_mul_block_repack touches no device buffer of the handle
+ * (its staged k-mask lives in ws), so it may run on a second stream while
+ * other calls of the same handle run on the first -- the one exception to
+ * the one-stream-per-handle rule.  Results equal tri_mul_block_accumulate's up to the order
+ * of the fp32 additions over k-panels (identical per panel). */
+int tri_mul_block_accumulator_size(tri_mul_handle_t h, const tri_mul_block_view_t* v, size_t* bytes);
+int tri_mul_block_repack(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                         const void* b_panel, const uint8_t* mask, void* ws, size_t ws_bytes, void* stream);
+int tri_mul_block_accumulate_packed(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* ws,
+                                    size_t ws_bytes, float* acc, const uint8_t* mask, const void* z_tile,
+                                    void* out_tile, int32_t reserve_cus, void* stream);
 
 /* The three stages of tri_mul_outgoing / tri_mul_incoming, exposed so that
  * callers can time or check them one by one.

@@ -369,7 +369,7 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
     if (!rc) rc = upload(h, &h->w.wo_t, wo_t, s);
     if (!rc) rc = upload(h, &h->w.wg_t, wg_t, s);
     if (!rc) {
-        std::vector<uint8_t> zeros((size_t)trimul::kMaxKPanel + 64, 0);
+        std::vector<uint8_t> zeros((size_t)trimul::kMaskStageBytes, 0);
         rc = upload(h, &h->w.kmask_pad, zeros, s);
     }
     if (!rc && p->dtype == TRI_MUL_BF16) {
@@ -560,11 +560,10 @@ int tri_mul_contract_backward(tri_mul_handle_t h, const float* dC, const void* a
 
 namespace {
 
-// Argument checks shared by the two block entry points.
-int check_block(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel, const void* b_panel,
-                const float* acc, const void* z_tile, const void* out_tile) {
+// Checks of a block view's sizes, ranges and panel strides, shared by the
+// block entry points.
+int check_view(const tri_mul_block_view_t* v) {
     if (!v) return fail(TRI_MUL_EINVAL, "null view");
-    if (!a_panel || !b_panel || !acc) return fail(TRI_MUL_EINVAL, "null panel or accumulator pointer");
     if (v->n_total < 1 || v->rows < 1 || v->cols < 1 || v->klen < 1) return fail(TRI_MUL_EINVAL, "empty or negative view sizes");
     if (v->row0 < 0 || v->col0 < 0 || v->k0 < 0 || v->row0 + v->rows > v->n_total || v->col0 + v->cols > v->n_total ||
         v->k0 + v->klen > v->n_total)
@@ -577,6 +576,16 @@ int check_block(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a
     if (v->ld_a > kMaxN || v->ld_b > kMaxN)
         return fail(TRI_MUL_EUNSUPPORTED, "ld_a / ld_b are limited to %lld elements", (long long)kMaxN);
     if (v->k_count < 1 || v->k_index < 0 || v->k_index >= v->k_count) return fail(TRI_MUL_EINVAL, "bad k_index %d / k_count %d", v->k_index, v->k_count);
+    return TRI_MUL_OK;
+}
+
+// Pointer checks of a ring step: panels (or the workspace holding them
+// repacked), accumulator, and on the last k-panel the tile's z and output.
+int check_block(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel, const void* b_panel,
+                const float* acc, const void* z_tile, const void* out_tile) {
+    (void)h;
+    if (int rc = check_view(v)) return rc;
+    if (!a_panel || !b_panel || !acc) return fail(TRI_MUL_EINVAL, "null panel or accumulator pointer");
     if (!aligned16(a_panel) || !aligned16(b_panel) || !aligned16(acc)) return fail(TRI_MUL_EINVAL, "panels and accumulator must be 16-byte aligned");
     const bool last = v->k_index == v->k_count - 1;
     if (last) {
@@ -594,6 +603,34 @@ size_t block_ws_a(const tri_mul_block_view_t* v) {
 size_t block_ws_b(const tri_mul_block_view_t* v) {
     const size_t nk = (size_t)((v->klen + 31) / 32);
     return round256((size_t)128 * (size_t)((v->cols + 255) / 256) * nk * 256 * 32 * 2);
+}
+// Bytes of the staged k-mask kept at the end of the workspace (0/1 per k,
+// zero-padded to a multiple of 32), so that a repack on one stream never
+// shares staging with an epilogue on another.
+size_t block_ws_m(const tri_mul_block_view_t* v) { return round256((size_t)((v->klen + 31) / 32 * 32)); }
+size_t block_ws_total(const tri_mul_block_view_t* v) { return block_ws_a(v) + block_ws_b(v) + block_ws_m(v); }
+
+// Validation shared by the repacking entry points: the view's sizes, and a
+// workspace of block_ws_total bytes, 256-byte aligned.
+int check_block_ws(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* ws, size_t ws_bytes) {
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "repacked panels exist for the bf16 storage path only");
+    if (!ws) return fail(TRI_MUL_EINVAL, "null workspace");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
+    const size_t need = block_ws_total(v);
+    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    return TRI_MUL_OK;
+}
+
+// Stage the view's k-mask into the workspace and repack both panels.
+hipError_t block_repack(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel, const void* b_panel,
+                        const uint8_t* mask, void* ws, hipStream_t s) {
+    char* wa = static_cast<char*>(ws);
+    char* wb = wa + block_ws_a(v);
+    uint8_t* km = reinterpret_cast<uint8_t*>(wb + block_ws_b(v));
+    hipError_t e = trimul::launch_stage_kmask(mask ? mask + v->k0 : nullptr, v->klen, km, s);
+    if (e == hipSuccess) e = trimul::launch_panel_block(a_panel, v->rows, v->ld_a, v->klen, h->c, km, wa, s);
+    if (e == hipSuccess) e = trimul::launch_panel_block(b_panel, v->cols, v->ld_b, v->klen, h->c, km, wb, s);
+    return e;
 }
 
 }  // namespace
@@ -633,7 +670,7 @@ int tri_mul_block_workspace_size(tri_mul_handle_t h, const tri_mul_block_view_t*
     if (v->rows < 1 || v->cols < 1 || v->klen < 1 || v->rows > kMaxN || v->cols > kMaxN ||
         v->klen > trimul::kMaxKPanel)
         return fail(TRI_MUL_EINVAL, "tile sides and k-panel length must lie in [1, %lld]", (long long)kMaxN);
-    *bytes = h->dtype == TRI_MUL_BF16 ? block_ws_a(v) + block_ws_b(v) : 0;
+    *bytes = h->dtype == TRI_MUL_BF16 ? block_ws_total(v) : 0;
     return ok();
 }
 
@@ -644,23 +681,63 @@ int tri_mul_block_accumulate_ws(tri_mul_handle_t h, const tri_mul_block_view_t* 
     if (int rc = check_block(h, v, a_panel, b_panel, acc, z_tile, out_tile)) return rc;
     if (h->dtype != TRI_MUL_BF16)   // the fp32 path has no blocked form: the plain call is the same op
         return tri_mul_block_accumulate(h, v, a_panel, b_panel, acc, mask, z_tile, out_tile, stream);
-    const size_t need = block_ws_a(v) + block_ws_b(v);
-    if (!ws) return fail(TRI_MUL_EINVAL, "null workspace");
-    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(TRI_MUL_EINVAL, "workspace must be 256-byte aligned");
-    if (ws_bytes < need) return fail(TRI_MUL_ENOMEM, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    if (int rc = check_block_ws(h, v, ws, ws_bytes)) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* wa = static_cast<char*>(ws);
     char* wb = wa + block_ws_a(v);
     const bool last = v->k_index == v->k_count - 1;
-    hipError_t e = trimul::launch_stage_kmask(mask ? mask + v->k0 : nullptr, v->klen, h->w.kmask_pad, s);
-    if (e == hipSuccess) e = trimul::launch_panel_block(a_panel, v->rows, v->ld_a, v->klen, h->c, h->w.kmask_pad, wa, s);
-    if (e == hipSuccess) e = trimul::launch_panel_block(b_panel, v->cols, v->ld_b, v->klen, h->c, h->w.kmask_pad, wb, s);
+    hipError_t e = block_repack(h, v, a_panel, b_panel, mask, ws, s);
     if (e != hipSuccess) return hip_fail(e, "panel repack kernel launch");
     e = trimul::launch_contract_blocked_rowc(wa, wb, acc, v->rows, v->cols, v->klen, h->c, v->k_index > 0, h->w.cus, s);
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     if (last) {
         const int64_t sC = v->rows * v->cols;
         trimul::EpilogueArgs ea{acc, 0, v->cols, sC, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
+        e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    }
+    return ok();
+}
+
+int tri_mul_block_accumulator_size(tri_mul_handle_t h, const tri_mul_block_view_t* v, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (!v || !bytes) return fail(TRI_MUL_EINVAL, "null view or bytes pointer");
+    if (v->rows < 1 || v->cols < 1 || v->rows > kMaxN || v->cols > kMaxN)
+        return fail(TRI_MUL_EINVAL, "tile sides must lie in [1, %lld]", (long long)kMaxN);
+    *bytes = (size_t)v->rows * (size_t)((v->cols + 31) / 32 * 32) * (size_t)h->c * 4;
+    return ok();
+}
+
+int tri_mul_block_repack(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                         const void* b_panel, const uint8_t* mask, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_view(v)) return rc;
+    if (!a_panel || !b_panel) return fail(TRI_MUL_EINVAL, "null panel pointer");
+    if (!aligned16(a_panel) || !aligned16(b_panel)) return fail(TRI_MUL_EINVAL, "panels must be 16-byte aligned");
+    if (int rc = check_block_ws(h, v, ws, ws_bytes)) return rc;
+    hipError_t e = block_repack(h, v, a_panel, b_panel, mask, ws, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "panel repack kernel launch");
+    return ok();
+}
+
+int tri_mul_block_accumulate_packed(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* ws,
+                                    size_t ws_bytes, float* acc, const uint8_t* mask, const void* z_tile,
+                                    void* out_tile, int32_t reserve_cus, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    // the panels live in ws: pass ws in their place for the shared checks
+    if (int rc = check_block(h, v, ws, ws, acc, z_tile, out_tile)) return rc;
+    if (int rc = check_block_ws(h, v, ws, ws_bytes)) return rc;
+    if (reserve_cus < 0 || reserve_cus > h->w.cus - 8)
+        return fail(TRI_MUL_EINVAL, "reserve_cus = %d outside [0, %d]", reserve_cus, h->w.cus - 8);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const char* wa = static_cast<const char*>(ws);
+    const char* wb = wa + block_ws_a(v);
+    const int cus = (h->w.cus - reserve_cus) & ~7;   // whole XCD groups
+    hipError_t e = trimul::launch_contract_blocked_packed(wa, wb, acc, v->rows, v->cols, v->klen, h->c,
+                                                          v->k_index > 0, cus, s);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    if (v->k_index == v->k_count - 1) {
+        trimul::EpilogueArgs ea{acc, 1, 0, 0, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
         e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
         if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
     }

@@ -434,6 +434,19 @@ __global__ __launch_bounds__(256) void k2_contract_f32(const float* __restrict__
         }
 }
 
+// Token mask of a tile's columns (0/1 bytes, zero from cols to cpad) followed
+// by its rows (from byte cpad, zero from rows to rpad).
+__global__ void k_stage_tile_mask(const uint8_t* __restrict__ mask, int64_t row0, int rows, int64_t col0, int cols,
+                                  int cpad, int rpad, uint8_t* __restrict__ dst) {
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < cpad) {
+        dst[k] = (k < cols && (!mask || mask[col0 + k] != 0)) ? 1 : 0;
+    } else if (k < cpad + rpad) {
+        const int r = k - cpad;
+        dst[k] = (r < rows && (!mask || mask[row0 + r] != 0)) ? 1 : 0;
+    }
+}
+
 __global__ void k_stage_kmask(const uint8_t* __restrict__ mask, int klen, int padded, uint8_t* __restrict__ dst) {
     const int k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k < padded) dst[k] = (k < klen && (!mask || mask[k] != 0)) ? 1 : 0;
@@ -511,6 +524,19 @@ hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, 
     return hipGetLastError();
 }
 
+hipError_t launch_contract_blocked_packed(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
+                                          int batch, int accumulate, int cus, hipStream_t s) {
+    constexpr int BM = 256;
+    const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
+    const int total = tm * tn * batch;
+    const int grid = total < cus ? total : cus;
+    const int pace = pace_launch(grid, total, s);
+    hipLaunchKernelGGL((k2_contract_ws<true, false, true>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A,
+                       (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, (int64_t)0, (int64_t)0, (int64_t)0,
+                       (int64_t)0, tm, tn, total, accumulate, (const uint8_t*)nullptr, pace);
+    return hipGetLastError();
+}
+
 hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void* B, float* C, int64_t M, int64_t N,
                                       int64_t K, int batch, int cus, hipStream_t s) {
     constexpr int BM = 256;
@@ -527,6 +553,14 @@ hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void*
     else if (ta && tb) K2_TR(true, true);
     else return hipErrorInvalidValue;
 #undef K2_TR
+    return hipGetLastError();
+}
+
+hipError_t launch_stage_tile_mask(const uint8_t* mask, int64_t row0, int64_t rows, int64_t col0, int64_t cols,
+                                  uint8_t* dst, hipStream_t s) {
+    const int cpad = (int)((cols + 31) / 32 * 32), rpad = (int)((rows + 3) / 4 * 4);
+    hipLaunchKernelGGL(k_stage_tile_mask, dim3((unsigned)((cpad + rpad + 255) / 256)), dim3(256), 0, s, mask, row0,
+                       (int)rows, col0, (int)cols, cpad, rpad, dst);
     return hipGetLastError();
 }
 

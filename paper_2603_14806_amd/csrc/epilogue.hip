@@ -337,15 +337,17 @@ void k3_epilogue_mfma(EpilogueArgs a, int nchunk, int64_t nunits, const bf16_t* 
 //                   afterwards y_hi [0, 8192) and y_lo [8192, 16384)
 //   [16384, 24576)  z of the unit, [32 pairs][128] bf16: chunk q of pair row p
 //                   at slot q ^ (p & 1); afterwards x_hi
-//   [24576, 25600)  per-wave mask bytes: m[j0 .. j0 + 31] at 0, the dword of
-//                   m[i] at 32 (0/1 bytes, zero past N)
+//   [24576, 25600)  per-wave mask bytes: column mask bytes j0 .. j0 + 31 at 0,
+//                   the dword of row mask byte i at 32 (0/1 bytes staged by
+//                   launch_stage_tile_mask: columns, zero past cols, then rows
+//                   from byte rmoff)
 constexpr int kRC = 16384, kRZ = 8192, kRM = 1024;
 constexpr int kRSt = kRC + kRZ + kRM;
 
 template <typename TO>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
 void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z, const uint8_t* __restrict__ tmask,
-                      int N, int nunits, TO* __restrict__ out, const bf16_t* __restrict__ wepi,
+                      int rows, int cols, int rmoff, int nunits, TO* __restrict__ out, const bf16_t* __restrict__ wepi,
                       const float* __restrict__ lnin_w, const float* __restrict__ lnin_b,
                       const float* __restrict__ lnout_w, const float* __restrict__ lnout_b, float eps) {
     // fp32 output leaves straight from the accumulators (a register holds 32
@@ -364,7 +366,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
     const int lp = t >> 3, lq = t & 7;     // LayerNorms: pair lp, 8 lanes per pair
     const int G = gridDim.x;
     const int first = (G & 7) == 0 ? (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3) : blockIdx.x;
-    const int nchunk = (N + kP3 - 1) / kP3;
+    const int nchunk = (cols + kP3 - 1) / kP3;
     constexpr int kStores = (int)(kP3 * kCz * sizeof(TO)) / (4 * 1024);   // staged path: 16-byte stores per lane
     constexpr int kS = kDirect ? 16 : kStores;                             // stores per lane per unit
 
@@ -381,7 +383,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
     const int drow = w * 8 + (lane >> 4);
     const uint32_t dchunk = (uint32_t)(((lane & 15) ^ (drow & 1)) << 4);
     const uint32_t dv0 = (uint32_t)drow * kYRow + dchunk, dv1 = (uint32_t)(drow + 4) * kYRow + dchunk;
-    const uint32_t mpad = (uint32_t)((N + 31) / 32 * 32);
+    const uint32_t mpad = (uint32_t)rmoff + (uint32_t)((rows + 3) / 4 * 4);   // staged mask bytes
     auto decode = [&](int u, int& i, int& j0) {
         i = u / nchunk;
         j0 = (u - i * nchunk) * kP3;
@@ -390,16 +392,16 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         const bool valid = u < nunits;
         int i = 0, j0 = 0;
         if (valid) decode(u, i, j0);
-        const int np = valid ? min(kP3, N - j0) : 0;
+        const int np = valid ? min(kP3, cols - j0) : 0;
         const uint32_t st = ring_base + (uint32_t)(stage * kRSt);
         const v4i_t rc = buffer_desc(C + result_off(nchunk, kCh, 0, i, j0), valid ? (uint32_t)kRC : 0u);
 #pragma unroll
         for (int k = 0; k < 4; ++k) lds_load16(rc, cvo[k >> 1] + k * 1024, 0, st + w * 4096 + k * 1024);
-        const v4i_t rz = buffer_desc(z + ((int64_t)i * N + j0) * kCz, (uint32_t)np * kYRow);
+        const v4i_t rz = buffer_desc(z + ((int64_t)i * cols + j0) * kCz, (uint32_t)np * kYRow);
         lds_load16(rz, dv0, 0, st + kRC + w * 2048);
         lds_load16(rz, dv1, 0, st + kRC + w * 2048 + 1024);
         const v4i_t rm = buffer_desc(tmask, valid ? mpad : 0u);
-        const uint32_t mo = lane < 8 ? (uint32_t)(j0 + 4 * lane) : lane == 8 ? (uint32_t)(i & ~3) : 0xfffffff0u;
+        const uint32_t mo = lane < 8 ? (uint32_t)(j0 + 4 * lane) : lane == 8 ? (uint32_t)(rmoff + (i & ~3)) : 0xfffffff0u;
         lds_load4(rm, mo, 0, st + kRC + kRZ + w * 256);
     };
     issue(first, 0);
@@ -542,10 +544,10 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         // 8 (r / 4) + 4 (lane / 32) + r % 4 (tail pairs come out as zeros and
         // are not stored).
         const int d = w * 32 + (lane & 31);
-        const int np = min(kP3, N - uj0);
+        const int np = min(kP3, cols - uj0);
         if constexpr (kDirect) {
             // bytes past the row's last pair fall outside the descriptor
-            const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * N + uj0) * kCz,
+            const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * cols + uj0) * kCz,
                                                         (uint32_t)(np * kCz * 4));
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -565,7 +567,7 @@ void k3_epilogue_ring(const float* __restrict__ C, const bf16_t* __restrict__ z,
         // bf16: the unit's [32 pairs][128] block is contiguous in out: store k
         // of the work-group covers its bytes [4096 k, 4096 k + 4096), 16 per
         // thread; bytes past the row's last pair fall outside the descriptor.
-        const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * N + uj0) * kCz,
+        const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + ((int64_t)ui * cols + uj0) * kCz,
                                                     (uint32_t)(np * kCz * (int)sizeof(TO)));
 #pragma unroll
         for (int k = 0; k < kStores; ++k) {
@@ -596,12 +598,13 @@ hipError_t launch_mfma(const DeviceWeights& w, const EpilogueArgs& a, hipStream_
     const int64_t cap = 2 * (int64_t)w.cus;
     const unsigned g = (unsigned)(nunits < cap ? nunits : cap);
     const bool vec = (a.ldc % 4) == 0 && (a.sc % 4) == 0 && (reinterpret_cast<uintptr_t>(a.C) & 15u) == 0;
-    if (a.cblocked) {   // the full update: rows = cols = N, row0 = col0 = 0
-        hipError_t e = launch_stage_kmask(a.mask, a.cols, w.kmask_pad, s);
+    if (a.cblocked) {   // C in the pair-blocked layout: the full update, or a tile's packed accumulator
+        const int rmoff = (int)((a.cols + 31) / 32 * 32);
+        hipError_t e = launch_stage_tile_mask(a.mask, a.row0, a.rows, a.col0, a.cols, w.kmask_pad, s);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL((k3_epilogue_ring<TO>), dim3(g), dim3(256), 0, s, a.C, (const bf16_t*)a.z, w.kmask_pad,
-                           (int)a.cols, (int)nunits, (TO*)a.out, w.epi_bf, w.ln_in_w, w.ln_in_b, w.ln_out_w,
-                           w.ln_out_b, w.eps);
+                           (int)a.rows, (int)a.cols, rmoff, (int)nunits, (TO*)a.out, w.epi_bf, w.ln_in_w, w.ln_in_b,
+                           w.ln_out_w, w.ln_out_b, w.eps);
     } else if (vec)
         hipLaunchKernelGGL((k3_epilogue_mfma<TO, true, false>), dim3(g), dim3(256), 0, s, a, nchunk, nunits, w.epi_bf,
                            w.ln_in_w, w.ln_in_b, w.ln_out_w, w.ln_out_b, w.eps);

@@ -26,14 +26,20 @@ struct DeviceWeights {
     uint16_t* projt_bf = nullptr; // [c_z][4*c]: row d = W_a[:, d], W_ga[:, d], W_b[:, d], W_gb[:, d] (backward)
     float eps = 1e-5f;
     int cus = 256;                // compute units of the device (persistent grids)
-    uint8_t* kmask_pad = nullptr; // 0/1 staging of a token mask (k-panel or whole sequence), kMaxKPanel + 64 bytes
+    uint8_t* kmask_pad = nullptr; // 0/1 staging of a token mask (k-panel, sequence, or a tile's columns and rows), kMaskStageBytes
 };
 
 constexpr int64_t kMaxKPanel = 65536;   // longest k-panel of one block call
+constexpr int64_t kMaskStageBytes = 2 * kMaxKPanel + 128;   // size of DeviceWeights::kmask_pad
 
 // Copies mask[0, klen) into dst as 0/1 bytes (mask NULL: all ones) and zero-fills dst up to the next
 // multiple of 32 (so the contraction can read whole 4-byte words of it).
 hipError_t launch_stage_kmask(const uint8_t* mask, int64_t klen, uint8_t* dst, hipStream_t s);
+// Stages a tile's token mask for the epilogue: dst[0, ceil(cols/32)*32) = 0/1 of mask[col0 + k] (zero
+// past cols), then dst[ceil(cols/32)*32 + r] = 0/1 of mask[row0 + r] for r < ceil(rows/4)*4 (zero past
+// rows); mask NULL: all ones.  dst must hold kMaskStageBytes.
+hipError_t launch_stage_tile_mask(const uint8_t* mask, int64_t row0, int64_t rows, int64_t col0, int64_t cols,
+                                  uint8_t* dst, hipStream_t s);
 // Row-major bf16 panel [nch][rows][ld] -> blocked [nch][ceil(rows/256)][ceil(klen/32)][256][32],
 // staged k-mask applied, padding zero.
 hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t klen, int nch, const uint8_t* kst,
@@ -41,6 +47,10 @@ hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t k
 // bf16 contraction of blocked operands into a row-major fp32 C [batch][M][N].
 hipError_t launch_contract_blocked_rowc(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
                                         int batch, int accumulate, int cus, hipStream_t s);
+// bf16 contraction of blocked operands into the pair-blocked fp32 result layout over (M, N) (a device
+// tile's packed accumulator), overwritten or accumulated into.
+hipError_t launch_contract_blocked_packed(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
+                                          int batch, int accumulate, int cus, hipStream_t s);
 // bf16 contraction of blocked operands, either given as its transpose in the
 // panel layout (ta: A[c][i][k] = X[c][k][i], X with K rows and M columns; tb
 // likewise with N columns), into the pair-blocked fp32 result layout.

@@ -84,6 +84,10 @@ SIGNATURES = {
     "tri_mul_block_workspace_size": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), ctypes.POINTER(ctypes.c_size_t)]),
     "tri_mul_block_accumulate_ws": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                                     ctypes.c_size_t, _vp]),
+    "tri_mul_block_accumulator_size": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_block_repack": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tri_mul_block_accumulate_packed": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, ctypes.c_size_t, _vp, _vp,
+                                                        _vp, _vp, _i32, _vp]),
     "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
@@ -218,6 +222,22 @@ def tri_mul_block_accumulate_ws(h, view, a_panel, b_panel, acc, mask, z_tile, ou
     _check(lib().tri_mul_block_accumulate_ws(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(acc),
                                              _ptr(mask), _ptr(z_tile), _ptr(out_tile), _ptr(ws), ws_bytes,
                                              _stream(stream)))
+
+
+def tri_mul_block_accumulator_size(h, view):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_block_accumulator_size(h, ctypes.byref(view), ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_block_repack(h, view, a_panel, b_panel, mask, ws, ws_bytes, stream=None):
+    _check(lib().tri_mul_block_repack(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(mask), _ptr(ws),
+                                      ws_bytes, _stream(stream)))
+
+
+def tri_mul_block_accumulate_packed(h, view, ws, ws_bytes, acc, mask, z_tile, out_tile, reserve_cus=0, stream=None):
+    _check(lib().tri_mul_block_accumulate_packed(h, ctypes.byref(view), _ptr(ws), ws_bytes, _ptr(acc), _ptr(mask),
+                                                 _ptr(z_tile), _ptr(out_tile), reserve_cus, _stream(stream)))
 
 
 def tri_mul_project(h, z, mask, N, direction, a_panels, b_panels, stream=None):
@@ -393,6 +413,17 @@ class TriMul:
     def block_workspace_size(self, view):
         return tri_mul_block_workspace_size(self.h, view)
 
+    def block_accumulator_size(self, view):
+        return tri_mul_block_accumulator_size(self.h, view)
+
+    def block_repack(self, view, a_panel, b_panel, mask, ws, stream=None):
+        tri_mul_block_repack(self.h, view, a_panel, b_panel, mask, ws, ws.numel() * ws.element_size(), stream)
+
+    def block_accumulate_packed(self, view, ws, acc, mask=None, z_tile=None, out_tile=None, reserve_cus=0,
+                                stream=None):
+        tri_mul_block_accumulate_packed(self.h, view, ws, ws.numel() * ws.element_size(), acc, mask, z_tile,
+                                        out_tile, reserve_cus, stream)
+
 
 # ------------------------------------------------------ panel layout views
 
@@ -417,10 +448,12 @@ def dense_to_panel(X):
     return Y.reshape(c, T, 256, S, 32).permute(0, 1, 3, 2, 4).contiguous().reshape(-1)
 
 
-def result_to_dense(Cr, N, c=128):
-    """Result-layout C (flat) -> dense [c][N][N]."""
-    J = -(-N // 32)
-    return Cr.reshape(N, J, c, 32).permute(2, 0, 1, 3).reshape(c, N, J * 32)[:, :, :N]
+def result_to_dense(Cr, N, c=128, cols=None):
+    """Result-layout C (flat) over N rows and `cols` columns (default N) ->
+    dense [c][N][cols] (a device tile's packed accumulator has this layout)."""
+    cols = N if cols is None else cols
+    J = -(-cols // 32)
+    return Cr.reshape(N, J, c, 32).permute(2, 0, 1, 3).reshape(c, N, J * 32)[:, :, :cols]
 
 
 def dense_to_result(C):

@@ -26,6 +26,31 @@ def sample_index(N, n_rand, seed, extra=()):
     return np.array(sorted(idx))
 
 
+def ring_packed(layer, views, aps, bps, mask, z_tile, out, pacc, wss, reserve_cus=0):
+    """The ring steps of one tile through tri_mul_block_repack +
+    tri_mul_block_accumulate_packed: panel p + 1 is repacked on a second
+    stream while panel p is contracted on the current one, alternating
+    between two workspaces (ordered by events)."""
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    n = len(views)
+    packed = [torch.cuda.Event() for _ in range(n)]
+    done = [torch.cuda.Event() for _ in range(n)]
+    layer.block_repack(views[0], aps[0], bps[0], mask, wss[0], main)
+    packed[0].record(main)
+    side.wait_stream(main)
+    for p in range(n):
+        if p + 1 < n:
+            if p >= 1:
+                side.wait_event(done[p - 1])   # that step read the workspace this repack overwrites
+            layer.block_repack(views[p + 1], aps[p + 1], bps[p + 1], mask, wss[(p + 1) % 2], side)
+            packed[p + 1].record(side)
+        main.wait_event(packed[p])
+        layer.block_accumulate_packed(views[p], wss[p % 2], pacc, mask, z_tile, out,
+                                      reserve_cus=reserve_cus if p + 1 < n else 0, stream=main)
+        done[p].record(main)
+    main.wait_stream(side)
+
+
 @pytest.mark.parametrize("direction", DIRS)
 def test_config3_bf16_n2048_channel_scaled(direction):
     N = 2048
@@ -89,10 +114,12 @@ def test_config4_full_rows_n4096():
 def test_config5_tile_of_8x8_grid_n30000():
     """Tile (7, 7) of an 8 x 8 grid at N = 30000: 3750 x 3750 outputs, 8
     k-panels of 3750 tokens, the last 300 tokens padded (rows, columns and the
-    last k-panel).  Panels ~ N(0,1) bf16 generated on the device.  Both
-    entry points run on the same panels: tri_mul_block_accumulate (row-major
-    panels read in place) and tri_mul_block_accumulate_ws (panels repacked
-    through the workspace, the one the benchmark times)."""
+    last k-panel).  Panels ~ N(0,1) bf16 generated on the device.  Three
+    ways run on the same panels: tri_mul_block_accumulate (row-major panels
+    read in place), tri_mul_block_accumulate_ws (panels repacked through the
+    workspace), and tri_mul_block_repack + tri_mul_block_accumulate_packed
+    with the next panel's repack on a second stream and a packed
+    accumulator (the one the benchmark times)."""
     n_total, g = 30000, 8
     b = n_total // g
     row0 = col0 = 7 * b
@@ -117,16 +144,25 @@ def test_config5_tile_of_8x8_grid_n30000():
                                   [mask_h[p * b:(p + 1) * b] for p in range(g)])
     ref = oracle.block_epilogue(ref_C, oracle.take_pairs(z_tile, I, J), mask_h[row0 + I], mask_h[col0 + J], W)
     valid = (mask_h[row0 + I] != 0)[:, None] & (mask_h[col0 + J] != 0)[None, :]
-    ws = torch.empty(layer.block_workspace_size(T.BlockView(n_total, row0, col0, b, b, 0, b, ld, ld, 0, g)),
-                     dtype=torch.uint8, device="cuda")
-    for use_ws in (False, True):
+    v0 = T.BlockView(n_total, row0, col0, b, b, 0, b, ld, ld, 0, g)
+    ws = torch.empty(layer.block_workspace_size(v0), dtype=torch.uint8, device="cuda")
+    for mode in ("plain", "ws", "packed"):
         acc.fill_(float("nan"))   # the first ring step must overwrite every element
         out.fill_(float("nan"))
-        for p in range(g):
-            v = T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g)
-            layer.block_accumulate(v, aps[p], bps[p], acc, mask, z_tile, out, ws=ws if use_ws else None)
+        if mode == "packed":
+            # the next panel's repack on a second stream while the current one
+            # is contracted on 16 fewer compute units; two workspaces
+            pacc = torch.full((layer.block_accumulator_size(v0) // 4,), float("nan"), device="cuda")
+            ring_packed(layer, [T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g) for p in range(g)],
+                        aps, bps, mask, z_tile, out, pacc, [ws, torch.empty_like(ws)], reserve_cus=16)
+            torch.cuda.synchronize()
+            acc.copy_(T.result_to_dense(pacc, b, cols=b))
+        else:
+            for p in range(g):
+                v = T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g)
+                layer.block_accumulate(v, aps[p], bps[p], acc, mask, z_tile, out, ws=ws if mode == "ws" else None)
         torch.cuda.synchronize()
-        say(f"  device run done ({'tri_mul_block_accumulate_ws' if use_ws else 'tri_mul_block_accumulate'})")
+        say(f"  device run done ({mode})")
         got_C = host(acc[:, It][:, :, Jt]).transpose(1, 2, 0)
         mx, rel = errors(got_C, ref_C)
         say(f"  accumulator: max_abs={mx:.3e} rel_fro={rel:.3e}")
@@ -139,13 +175,14 @@ def test_config5_tile_of_8x8_grid_n30000():
 
 @pytest.mark.parametrize("direction", DIRS)
 @pytest.mark.parametrize("N,g,use_ws", [(1024, 2, False), (1024, 4, False), (1000, 4, False), (1024, 2, True),
-                                        (1000, 4, True)])
+                                        (1000, 4, True), (1024, 2, "packed"), (1000, 4, "packed")])
 def test_block_decomposition_matches_full(direction, N, g, use_ws):
     """The one-GPU stand-in for the paper's ring: split the full problem into
     a g x g grid of tiles, run each tile as g block_accumulate calls (one per
     k-panel, as in the Cannon ring; with use_ws through the repacking entry
-    point) from the same projected panels, and compare with the single-call
-    contraction and update."""
+    point, or with "packed" through tri_mul_block_repack and
+    tri_mul_block_accumulate_packed on two streams) from the same projected
+    panels, and compare with the single-call contraction and update."""
     say(f"block == full: N={N} g={g} {direction} ws={use_ws}")
     layer, W = make_layer("bf16")
     z = synth.pair_tensor(N, dtype="bf16", device="cuda")
@@ -171,6 +208,7 @@ def test_block_decomposition_matches_full(direction, N, g, use_ws):
             acc = torch.empty((128, bsz, bsz), dtype=torch.float32, device="cuda")
             z_tile = z[r0:r0 + bsz, c0:c0 + bsz].contiguous()
             o_tile = torch.empty((bsz, bsz, 128), dtype=torch.float32, device="cuda")
+            aps, bps, views = [], [], []
             for p in range(g):
                 k0 = p * bsz
                 ap = torch.zeros((128, bsz, ld), dtype=torch.bfloat16, device="cuda")
@@ -178,7 +216,13 @@ def test_block_decomposition_matches_full(direction, N, g, use_ws):
                 ap[:, :, :bsz] = A[:, r0:r0 + bsz, k0:k0 + bsz]
                 bp[:, :, :bsz] = B[:, c0:c0 + bsz, k0:k0 + bsz]
                 v = T.BlockView(N, r0, c0, bsz, bsz, k0, bsz, ld, ld, p, g)
-                layer.block_accumulate(v, ap, bp, acc, mask, z_tile, o_tile, ws=ws)
+                aps.append(ap), bps.append(bp), views.append(v)
+                if use_ws != "packed":
+                    layer.block_accumulate(v, ap, bp, acc, mask, z_tile, o_tile, ws=ws)
+            if use_ws == "packed":
+                pacc = torch.full((layer.block_accumulator_size(views[0]) // 4,), float("nan"), device="cuda")
+                ring_packed(layer, views, aps, bps, mask, z_tile, o_tile, pacc, [ws, torch.empty_like(ws)])
+                acc = T.result_to_dense(pacc, bsz, cols=bsz)
             mx, rel = errors(host(acc), host(C_full[:, r0:r0 + bsz, c0:c0 + bsz]))
             assert rel <= 1e-5, (r, c, rel)
             out_blk[r0:r0 + bsz, c0:c0 + bsz] = o_tile

@@ -69,8 +69,8 @@ def test_block_accumulate_kmask_exact(dtype, use_ws):
 
 
 def test_block_accumulate_ws_errors():
-    """The workspace entry point rejects a short or misaligned workspace
-    before launching anything."""
+    """The workspace entry points reject a short or misaligned workspace (and
+    a bad CU reserve) before launching anything."""
     layer, _ = make_layer("bf16")
     rows, cols, klen, ld = 64, 40, 50, 56
     ap = torch.zeros((128, rows, ld), dtype=torch.bfloat16, device="cuda")
@@ -78,13 +78,26 @@ def test_block_accumulate_ws_errors():
     acc = torch.zeros((128, rows, cols), device="cuda")
     v = T.BlockView(200, 0, 0, rows, cols, 0, klen, ld, ld, 0, 2)
     need = layer.block_workspace_size(v)
-    assert need == 128 * 1 * 2 * 16384 * 2        # one 256-row tile and two k-steps per operand
+    # one 256-row tile and two k-steps per operand, then the staged k-mask (64 bytes, 256-byte aligned)
+    assert need == 128 * 1 * 2 * 16384 * 2 + 256
     ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
     with pytest.raises(T.TriMulError) as e:
         T.tri_mul_block_accumulate_ws(layer.h, v, ap, bp, acc, None, None, None, ws, need - 1)
     assert e.value.code == T.TRI_MUL_ENOMEM
     with pytest.raises(T.TriMulError) as e:
         T.tri_mul_block_accumulate_ws(layer.h, v, ap, bp, acc, None, None, None, ws[16:], need)
+    assert e.value.code == T.TRI_MUL_EINVAL
+    # the split form: the same workspace checks, a packed accumulator of
+    # rows * ceil(cols / 32) * 32 * 128 floats, and the CU reserve's range
+    assert layer.block_accumulator_size(v) == rows * 64 * 128 * 4
+    with pytest.raises(T.TriMulError) as e:
+        T.tri_mul_block_repack(layer.h, v, ap, bp, None, ws, need - 1)
+    assert e.value.code == T.TRI_MUL_ENOMEM
+    with pytest.raises(T.TriMulError) as e:
+        T.tri_mul_block_accumulate_packed(layer.h, v, ws, need, acc, None, None, None, reserve_cus=-1)
+    assert e.value.code == T.TRI_MUL_EINVAL
+    with pytest.raises(T.TriMulError) as e:
+        T.tri_mul_block_accumulate_packed(layer.h, v, ws[16:], need, acc, None, None, None)
     assert e.value.code == T.TRI_MUL_EINVAL
 
 
