@@ -237,8 +237,9 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the untimed extras (backward passes, outer product mean), e.g. for profiling runs "
-                         "that attribute the contraction kernel's statistics to the forward layer alone")
+                    help="skip the untimed extras (the N=2048 workload, backward passes, outer product mean, "
+                         "triangle attention, ring tile), e.g. for profiling runs that attribute the kernels' "
+                         "statistics to the timed N=4096 layer alone")
     ap.add_argument("--copy-calibration", type=float, default=0.0,
                     help="GiB moved by one plain device-to-device copy before the run (HBM counter calibration)")
     args = ap.parse_args()
@@ -325,7 +326,7 @@ def main():
     # the N = 2048 workload with channel-scaled z (s_c ~ U(0.5, 2)), both
     # directions through the three kernels, outside the timed region
     c3 = None
-    if N != 2048:
+    if N != 2048 and not args.no_extras:
         N3 = 2048
         z3 = synth.pair_tensor(N3, dtype="bf16", scale=synth.channel_scale(), device=dev)
         np3 = T.tri_mul_panel_size(h, N3) // 2
