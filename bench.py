@@ -367,7 +367,7 @@ def main():
         del z3
         print(f"[bench] N=2048 channel-scaled layer {c3['ms_per_layer']:.3f} ms", file=sys.stderr, flush=True)
 
-    bwd_ms = lbwd_ms = sbwd_ms = opm_ms = ta_ms = tile_ms = tile_ws_ms = None
+    bwd_ms = lbwd_ms = sbwd_ms = opm_ms = ta_ms = tile_ms = tile_pk_ms = tile_ws_ms = None
     ta_scores = 2048 * 4 * 2048 * 2048
     opm_flops = 2 * 4096 * (1024 * 32) ** 2
     if not args.no_extras:
@@ -513,6 +513,27 @@ def main():
                 done[p].record(stream)
             stream.wait_stream(side)
 
+        # the ring with the panels in the contraction's blocked layout: the
+        # device projects its own tile (the a and b panels of k-block 7 it
+        # contributes to the ring) and contracts the eight panel pairs as they
+        # arrive, with no repack; the other seven pairs alternate between two
+        # projected tiles (made before the timed calls, as a ring delivers them)
+        n_bp = layer.block_panel_size(bb, bb) // 2
+        own = [torch.empty(n_bp, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+        arrived = []
+        for p in range(2):
+            zt = synth.pair_tensor(0, dtype="bf16", device=dev, name="z_tile", seed=synth.SEED + 1 + p,
+                                   shape=(bb, bb, 128))
+            arrived.append(layer.block_project(zt, bmask, bn, brow, p * bb, "outgoing"))
+            del zt
+
+        def ring_tile_blocked():
+            T.tri_mul_block_project(layer.h, bz, bb, bmask, bn, brow, brow, bb, bb, T.TRI_MUL_OUTGOING,
+                                    own[0], own[1], stream)
+            for p in range(bg):
+                a_, b_ = own if p == bg - 1 else arrived[p & 1]
+                layer.block_accumulate_blocked(bviews[p], a_, b_, pacc, bmask, bz, bout, stream=stream)
+
         def time_ring(fn):
             fn()
             t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -523,12 +544,13 @@ def main():
             torch.cuda.synchronize()
             return t0e.elapsed_time(t1e) / 2
 
-        tile_ms = time_ring(ring_tile)
+        tile_ms = time_ring(ring_tile_blocked)
+        tile_pk_ms = time_ring(ring_tile)
         tile_ws_ms = time_ring(ring_tile_ws)
-        del bpa, bpb, bz, bacc, bout, tws, tws2, pacc
+        del bpa, bpb, bz, bacc, bout, tws, tws2, pacc, own, arrived
         torch.cuda.empty_cache()
-        print(f"[bench] ring tile {tile_ms:.3f} ms (one-stream repacking entry point {tile_ws_ms:.3f} ms)",
-              file=sys.stderr, flush=True)
+        print(f"[bench] ring tile {tile_ms:.3f} ms (row-major panels: pipelined repack {tile_pk_ms:.3f} ms, "
+              f"one-stream repacking entry point {tile_ws_ms:.3f} ms)", file=sys.stderr, flush=True)
 
     fl = perf.flops(N)
     by = perf.bytes_moved(N)
@@ -605,13 +627,18 @@ def main():
         "ring_tile": None if tile_ms is None else {"ms": round(tile_ms, 4),
                       "TFLOP_per_s": round(tile_flops / (tile_ms * 1e-3) / 1e12, 2),
                       "roofline": mfma_roof(tile_flops, tile_ms),
+                      "ms_rowmajor_pipelined": round(tile_pk_ms, 4),
                       "ms_one_stream_ws": round(tile_ws_ms, 4),
-                      "what": "tile (7,7) of an 8x8 grid at N=30000: 8 ring steps (3750x3750 outputs, 3750-token "
-                              "k-panels, 128 channels; 108.0 TFLOP contraction) through tri_mul_block_repack + "
-                              "tri_mul_block_accumulate_packed, the next panel's repack on a second stream while "
-                              "the current one is contracted on 224 CUs (32 left to the repack), packed fp32 accumulator, epilogue on the "
-                              "last step, fp32 output (ms_one_stream_ws: the same steps through "
-                              "tri_mul_block_accumulate_ws on one stream); not part of ms_per_step"},
+                      "what": "one device's share of a layer on an 8x8 grid at N=30000, tile (7,7): the projection "
+                              "of its 3750x3750 z tile into blocked a, b panels (tri_mul_block_project), 8 ring "
+                              "steps on blocked panels (tri_mul_block_accumulate_blocked: 3750x3750 outputs, "
+                              "3750-token k-panels, 128 channels, 108.0 TFLOP contraction, packed fp32 "
+                              "accumulator) and the tile epilogue on the last step, fp32 output; TFLOP/s counts "
+                              "the contraction only.  With row-major panels instead (no projection): "
+                              "ms_rowmajor_pipelined = tri_mul_block_repack of panel p + 1 on a second stream while "
+                              "panel p is contracted on 224 CUs (tri_mul_block_accumulate_packed), "
+                              "ms_one_stream_ws = tri_mul_block_accumulate_ws on one stream; not part of "
+                              "ms_per_step"},
         "backward_layer_saved": None if sbwd_ms is None else {"ms": round(sbwd_ms, 4),
                            "roofline": {"bound": "mfma + hbm", "floor_ms": round(bws_["floor_ms"], 3),
                                         "frac": round(bws_["floor_ms"] / sbwd_ms, 4),

@@ -240,6 +240,56 @@ int tri_mul_block_accumulate_packed(tri_mul_handle_t h, const tri_mul_block_view
                                     size_t ws_bytes, float* acc, const uint8_t* mask, const void* z_tile,
                                     void* out_tile, int32_t reserve_cus, void* stream);
 
+/* The ring with the panels travelling in the contraction's blocked operand
+ * layout (Section 3.3, Fig. 2b).  Each device projects its own tile of z
+ * once per layer; the panels it passes round the ring are those projections,
+ * so writing them in the layout the contraction reads removes the repack
+ * from every ring step.  bf16 storage path only (else TRI_MUL_EUNSUPPORTED).
+ *
+ * Blocked panel of m rows and klen contraction indices: for hidden channel c,
+ *   element (c, i, k) at ((c * T + i / 256) * S + k / 32) * 8192 + (i % 256) * 32 + k % 32
+ * with T = ceil(m / 256), S = ceil(klen / 32) (the operand layout of
+ * tri_mul_project for a rectangle); entries with i >= m hold unspecified
+ * values and never contribute, entries with k >= klen are zero.
+ *
+ * tri_mul_block_panel_size: bytes of a blocked panel of m = rows rows and
+ *   klen contraction indices, 128 * T * S * 16 KB.  *bytes is a HOST pointer.
+ *   rows, klen <= 65536.
+ * tri_mul_block_project: the tile's input LayerNorm, gated projections and
+ *   pair mask (as tri_mul_project) written as two blocked panels.
+ *     z_tile   [rows][ld_z][c_z] dtype: pair (row0 + i, col0 + j) at
+ *              z_tile[i][j], ld_z >= cols (at most 65536)
+ *     mask     [n_total] uint8 token mask (NULL = all real); a(p, q) and
+ *              b(p, q) are 0 unless mask[p] and mask[q] are both nonzero
+ *   direction TRI_MUL_OUTGOING: a_panel[c][i][k] = a at (row0 + i, col0 + k),
+ *     m = rows, klen = cols: the a-panel of k-range [col0, col0 + cols) for
+ *     output rows [row0, row0 + rows), and likewise b the b-panel for output
+ *     columns [row0, row0 + rows) (Eq. 2 contracts the second token index).
+ *   direction TRI_MUL_INCOMING: a_panel[c][i][k] = a at (row0 + k, col0 + i),
+ *     m = cols, klen = rows: the a-panel of k-range [row0, row0 + rows) for
+ *     output rows [col0, col0 + cols), and likewise b the b-panel for output
+ *     columns [col0, col0 + cols) (Eq. 3 contracts the first token index).
+ *   a_panel, b_panel: tri_mul_block_panel_size(m, klen) bytes each, 16-byte
+ *   aligned.  Uses the handle's staging buffer: one stream per handle.
+ * tri_mul_block_accumulate_blocked: the ring step of
+ *   tri_mul_block_accumulate_packed with the two panels given directly in the
+ *   blocked layout (a_panel: m = rows, b_panel: m = cols, both klen; the mask
+ *   was applied when they were projected, so mask serves only the epilogue);
+ *   ld_a and ld_b of the view are not used.  acc is the packed accumulator
+ *   of tri_mul_block_accumulator_size (overwritten when k_index == 0,
+ *   accumulated into otherwise); the call with k_index == k_count - 1 also
+ *   runs the epilogue into out_tile.  reserve_cus as for
+ *   tri_mul_block_accumulate_packed.  Given the panels that
+ *   tri_mul_block_repack writes for the same values, the results are
+ *   identical to tri_mul_block_accumulate_packed's. */
+int tri_mul_block_panel_size(tri_mul_handle_t h, int64_t rows, int64_t klen, size_t* bytes);
+int tri_mul_block_project(tri_mul_handle_t h, const void* z_tile, int64_t ld_z, const uint8_t* mask, int64_t n_total,
+                          int64_t row0, int64_t col0, int64_t rows, int64_t cols, int32_t direction, void* a_panel,
+                          void* b_panel, void* stream);
+int tri_mul_block_accumulate_blocked(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                                     const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                                     void* out_tile, int32_t reserve_cus, void* stream);
+
 /* The three stages of tri_mul_outgoing / tri_mul_incoming, exposed so that
  * callers can time or check them one by one.
  *

@@ -744,6 +744,71 @@ int tri_mul_block_accumulate_packed(tri_mul_handle_t h, const tri_mul_block_view
     return ok();
 }
 
+int tri_mul_block_panel_size(tri_mul_handle_t h, int64_t rows, int64_t klen, size_t* bytes) {
+    if (int rc = check_handle(h)) return rc;
+    if (!bytes) return fail(TRI_MUL_EINVAL, "null bytes pointer");
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "blocked panels exist for the bf16 storage path only");
+    if (rows < 1 || klen < 1) return fail(TRI_MUL_EINVAL, "empty or negative panel sizes");
+    if (rows > kMaxN || klen > trimul::kMaxKPanel)
+        return fail(TRI_MUL_EUNSUPPORTED, "panel sides are limited to %lld", (long long)kMaxN);
+    *bytes = (size_t)h->c * (size_t)((rows + 255) / 256) * (size_t)((klen + 31) / 32) * 256 * 32 * 2;
+    return ok();
+}
+
+int tri_mul_block_project(tri_mul_handle_t h, const void* z_tile, int64_t ld_z, const uint8_t* mask, int64_t n_total,
+                          int64_t row0, int64_t col0, int64_t rows, int64_t cols, int32_t direction, void* a_panel,
+                          void* b_panel, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "blocked panels exist for the bf16 storage path only");
+    if (direction != TRI_MUL_OUTGOING && direction != TRI_MUL_INCOMING) return fail(TRI_MUL_EINVAL, "bad direction %d", direction);
+    if (!z_tile || !a_panel || !b_panel) return fail(TRI_MUL_EINVAL, "null z_tile or panel pointer");
+    if (!aligned16(z_tile) || !aligned16(a_panel) || !aligned16(b_panel))
+        return fail(TRI_MUL_EINVAL, "z_tile and the panels must be 16-byte aligned");
+    if (n_total < 1 || rows < 1 || cols < 1) return fail(TRI_MUL_EINVAL, "empty or negative tile sizes");
+    if (row0 < 0 || col0 < 0 || row0 + rows > n_total || col0 + cols > n_total)
+        return fail(TRI_MUL_EINVAL, "tile ranges exceed n_total = %lld", (long long)n_total);
+    if (rows > trimul::kMaxKPanel || cols > trimul::kMaxKPanel)
+        return fail(TRI_MUL_EUNSUPPORTED, "tile sides are limited to %lld", (long long)trimul::kMaxKPanel);
+    if (ld_z < cols) return fail(TRI_MUL_EINVAL, "ld_z = %lld < cols = %lld", (long long)ld_z, (long long)cols);
+    // the projection addresses 32 pairs of a tile column with 32-bit byte offsets
+    if (ld_z > kMaxN) return fail(TRI_MUL_EUNSUPPORTED, "ld_z is limited to %lld pairs", (long long)kMaxN);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // operand rows i and contraction index k: the tile's rows and columns
+    // (outgoing) or its columns and rows (incoming)
+    const bool in = direction == TRI_MUL_INCOMING;
+    const int64_t m0 = in ? col0 : row0, M = in ? cols : rows, k0 = in ? row0 : col0, K = in ? rows : cols;
+    hipError_t e = trimul::launch_stage_tile_mask(mask, m0, M, k0, K, h->w.kmask_pad, s);
+    if (e == hipSuccess)
+        e = trimul::launch_project_mfma(h->w, z_tile, ld_z, h->w.kmask_pad, (K + 31) / 32 * 32, M, K, in ? 1 : 0,
+                                        a_panel, b_panel, s);
+    if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
+    return ok();
+}
+
+int tri_mul_block_accumulate_blocked(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
+                                     const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                                     void* out_tile, int32_t reserve_cus, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "blocked panels exist for the bf16 storage path only");
+    if (!v) return fail(TRI_MUL_EINVAL, "null view");
+    tri_mul_block_view_t w = *v;   // the strides of row-major panels do not apply
+    w.ld_a = w.ld_b = (v->klen + 7) / 8 * 8;
+    if (int rc = check_block(h, &w, a_panel, b_panel, acc, z_tile, out_tile)) return rc;
+    if (reserve_cus < 0 || reserve_cus > h->w.cus - 8)
+        return fail(TRI_MUL_EINVAL, "reserve_cus = %d outside [0, %d]", reserve_cus, h->w.cus - 8);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int cus = (h->w.cus - reserve_cus) & ~7;   // whole XCD groups
+    hipError_t e = trimul::launch_contract_blocked_packed(a_panel, b_panel, acc, v->rows, v->cols, v->klen, h->c,
+                                                          v->k_index > 0, cus, s);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    if (v->k_index == v->k_count - 1) {
+        trimul::EpilogueArgs ea{acc, 1, 0, 0, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
+        e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    }
+    return ok();
+}
+
 int tri_mul_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
     if (int rc = check_handle(h)) return rc;
     if (int rc = check_n(N)) return rc;

@@ -87,6 +87,13 @@ struct EpilogueArgs {
 // K1: LN_in + gated projections + pair mask -> channel-major operands A, B in
 // the blocked panel layout (common.h) of N rows and K = N.  Padding rows are
 // left untouched; the k padding of a row's last k-step is written with zeros.
+// The bf16 projection of an M x K operand pair (A, B in the blocked layout of
+// panel_geom(M, K)): operand row i, contraction index k is pair (i, k) of z
+// (outgoing) or (k, i) (incoming), z rows ldz pairs apart; tmask holds the
+// staged 0/1 bytes of the k-range at [0, ceil(K/32)*32) and of operand row i
+// at rmoff + i.
+hipError_t launch_project_mfma(const DeviceWeights& w, const void* z, int64_t ldz, const uint8_t* tmask, int64_t rmoff,
+                               int64_t M, int64_t K, int incoming, void* A, void* B, hipStream_t s);
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
                           int64_t N, int incoming, void* A, void* B, hipStream_t s);
 

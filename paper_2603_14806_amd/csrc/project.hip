@@ -6,6 +6,8 @@
 // (r, k0): pairs (r, k0..k0+63), A[c][r][k0+p] = a(r, k0+p).  Incoming line
 // (r, k0): pairs (k0..k0+63, r), A[c][r][k0+p] = a(k0+p, r).  Either way the
 // 64 results of one channel are contiguous in A and B.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -118,12 +120,18 @@ __device__ __forceinline__ uint32_t xoff(int p, int chunk) {
     return (uint32_t)(p * kXRow + ((chunk ^ (p & 15)) << 4));
 }
 
-// tmask: the token mask as 0/1 bytes, zero from N up to mpad = ceil(N/32)*32.
+// The operands are M x K: operand row i (M of them) and contraction index k
+// (K).  Outgoing, pair (i, k) is z[i][k]; incoming, pair (k, i) is z[k][i];
+// z rows are ldz pairs apart (the full update: M = K = ldz = N; a device
+// tile: its rows and columns).  tmask: the staged 0/1 token bytes, the
+// k-range's at [0, ceil(K/32)*32) (zero past K) and operand row i's at
+// rmoff + i; mrange bytes of it are readable.
 template <bool INCOMING>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
-void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ tmask, int N, int nchunk,
-                     int nlines, const bf16_t* __restrict__ wproj, const float* __restrict__ lnw,
-                     const float* __restrict__ lnb, float eps, bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
+void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __restrict__ tmask, int rmoff,
+                     int mrange, int M, int K, int nlines, const bf16_t* __restrict__ wproj,
+                     const float* __restrict__ lnw, const float* __restrict__ lnb, float eps,
+                     bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
     __shared__ __attribute__((aligned(16))) char ring[kRing * kSt];     // z rows [p][256 B], mask
     __shared__ __attribute__((aligned(16))) char xs[2][kP1 * kXRow];   // x_hi, x_lo
     __shared__ __attribute__((aligned(16))) float os[2][kCh][kP1];      // a, b as [c][p]
@@ -133,8 +141,8 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
     const int t = threadIdx.x, lane = t & 63;
     const int g = __builtin_amdgcn_readfirstlane(t >> 6);
     const int lp = t >> 3, lq = t & 7;     // LayerNorm: pair lp, channels 16 lq .. 16 lq + 15
-    // Line order: rows fastest (line = kc * N + r covers pairs k0 = 32 kc ..
-    // k0 + 31 of row r), and the work-groups of one XCD take consecutive
+    // Line order: rows fastest (line = kc * M + r covers pairs k0 = 32 kc ..
+    // k0 + 31 of operand row r), and the work-groups of one XCD take consecutive
     // lines; the grid's lines of one round then fill whole 256-row blocks of
     // the operands and read long runs of z in either direction.
     const int G = gridDim.x;
@@ -145,29 +153,29 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
     // neighbouring rows hit disjoint banks.  Wave g loads rows 8 g .. 8 g + 7
     // (two 1 KB loads: lane i -> row 8 g + 4 h + i / 16, slot i % 16) and its
     // own copy of the line's mask bytes: m[k0 .. k0 + 31] at 0, the dword of
-    // m[r] at 32.  Lines past the end load nothing (zero-size descriptor).
-    const uint32_t zstep = INCOMING ? (uint32_t)N * kXRow : (uint32_t)kXRow;   // bytes between pairs
+    // row r's byte at 32.  Lines past the end load nothing (zero-size
+    // descriptor).
+    const uint32_t zstep = INCOMING ? (uint32_t)ldz * kXRow : (uint32_t)kXRow;   // bytes between pairs
     const uint32_t ring_base = lds_addr(ring);
     const int drow = g * 8 + (lane >> 4);
     const uint32_t dchunk = (uint32_t)(((lane & 15) ^ (drow & 1)) << 4);
     const uint32_t dv0 = (uint32_t)drow * zstep + dchunk, dv1 = (uint32_t)(drow + 4) * zstep + dchunk;
-    const uint32_t mpad = (uint32_t)((N + 31) / 32 * 32);
     auto issue = [&](int line, int stage) {
         const bool valid = line < nlines;
         int r = 0, k0 = 0;
         if (valid) {
-            const int kc = line / N;
-            r = line - kc * N;
+            const int kc = line / M;
+            r = line - kc * M;
             k0 = kc * kP1;
         }
-        const int np = valid ? min(kP1, N - k0) : 0;
-        const int64_t pair0 = INCOMING ? (int64_t)k0 * N + r : (int64_t)r * N + k0;
+        const int np = valid ? min(kP1, K - k0) : 0;
+        const int64_t pair0 = INCOMING ? (int64_t)k0 * ldz + r : (int64_t)r * ldz + k0;
         const v4i_t rz = buffer_desc(z + pair0 * kCz, np > 0 ? (uint32_t)(np - 1) * zstep + kXRow : 0u);
         const uint32_t st = ring_base + (uint32_t)(stage * kSt);
         lds_load16(rz, dv0, 0, st + g * 2048);
         lds_load16(rz, dv1, 0, st + g * 2048 + 1024);
-        const v4i_t rm = buffer_desc(tmask, valid ? mpad : 0u);
-        const uint32_t mo = lane < 8 ? (uint32_t)(k0 + 4 * lane) : lane == 8 ? (uint32_t)(r & ~3) : 0xfffffff0u;
+        const v4i_t rm = buffer_desc(tmask, valid ? (uint32_t)mrange : 0u);
+        const uint32_t mo = lane < 8 ? (uint32_t)(k0 + 4 * lane) : lane == 8 ? (uint32_t)(rmoff + (r & ~3)) : 0xfffffff0u;
         lds_load4(rm, mo, 0, st + kZSt + g * 256);
     };
     issue(first, 0);
@@ -184,7 +192,7 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
         gb[0][(t >> 4) * 20 + (t & 15)] = lnw[t];
         gb[1][(t >> 4) * 20 + (t & 15)] = lnb[t];
     }
-    const PanelGeom pg = panel_geom(N, N);
+    const PanelGeom pg = panel_geom(M, K);
     // Store mapping: thread t writes pairs 8 (t & 3) .. 8 (t & 3) + 7 of
     // channel (t >> 2) + 64 (i & 1) of A (i < 2) or B (i >= 2).
     const int64_t ch_stride = panel_elems(pg);
@@ -272,8 +280,8 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
 
         // Gate, mask, stage as [c][p] fp32.  Lane holds pair (lane & 31); in
         // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.  The
-        // staged mask is zero past N, which also zeroes a ragged line's tail.
-        const int kc = line / N, r0 = line - kc * N, k0 = kc * kP1;
+        // staged mask is zero past K, which also zeroes a ragged line's tail.
+        const int kc = line / M, r0 = line - kc * M, k0 = kc * kP1;
         const uint8_t* ms = reinterpret_cast<const uint8_t*>(zs + kZSt + g * 256);
         const uint32_t keep = (ms[bp] & ms[32 + (r0 & 3)]) ? 0xffffffffu : 0u;   // branch-free select
 #pragma unroll
@@ -304,6 +312,23 @@ void k1_project_mfma(const bf16_t* __restrict__ z, const uint8_t* __restrict__ t
 
 }  // namespace
 
+hipError_t launch_project_mfma(const DeviceWeights& w, const void* z, int64_t ldz, const uint8_t* tmask, int64_t rmoff,
+                               int64_t M, int64_t K, int incoming, void* A, void* B, hipStream_t s) {
+    const int nch = (int)((K + kP1 - 1) / kP1);
+    const int nlines = (int)(M * nch);
+    const unsigned g = (unsigned)(nlines < 2 * w.cus ? nlines : 2 * w.cus);
+    const int mrange = (int)std::max((K + 31) / 32 * 32, rmoff + (M + 3) / 4 * 4);
+    if (incoming)
+        hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, (int)ldz, tmask,
+                           (int)rmoff, mrange, (int)M, (int)K, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps,
+                           (bf16_t*)A, (bf16_t*)B);
+    else
+        hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, (int)ldz, tmask,
+                           (int)rmoff, mrange, (int)M, (int)K, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps,
+                           (bf16_t*)A, (bf16_t*)B);
+    return hipGetLastError();
+}
+
 hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, const uint8_t* mask,
                           int64_t N, int incoming, void* A, void* B, hipStream_t s) {
     const int64_t nchunk = (N + kLine - 1) / kLine;
@@ -317,17 +342,9 @@ hipError_t launch_project(int dtype, const DeviceWeights& w, const void* z, cons
             hipLaunchKernelGGL((k1_project_valu<float, false>), grid, block, 0, s, (const float*)z, mask, N,
                                nchunk, p4, w.ln_in_w, w.ln_in_b, w.eps, (float*)A, (float*)B);
     } else {
-        const int nch = (int)((N + kP1 - 1) / kP1);
-        const int nlines = (int)(N * nch);
-        const unsigned g = (unsigned)(nlines < 2 * w.cus ? nlines : 2 * w.cus);
         hipError_t e = launch_stage_kmask(mask, N, w.kmask_pad, s);
         if (e != hipSuccess) return e;
-        if (incoming)
-            hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, w.kmask_pad,
-                               (int)N, nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
-        else
-            hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, w.kmask_pad,
-                               (int)N, nch, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps, (bf16_t*)A, (bf16_t*)B);
+        return launch_project_mfma(w, z, N, w.kmask_pad, 0, N, N, incoming, A, B, s);
     }
     return hipGetLastError();
 }

@@ -88,6 +88,10 @@ SIGNATURES = {
     "tri_mul_block_repack": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "tri_mul_block_accumulate_packed": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, ctypes.c_size_t, _vp, _vp,
                                                         _vp, _vp, _i32, _vp]),
+    "tri_mul_block_panel_size": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "tri_mul_block_project": (ctypes.c_int, [_vp, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _vp, _vp]),
+    "tri_mul_block_accumulate_blocked": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp,
+                                                         _vp, _i32, _vp]),
     "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
@@ -238,6 +242,25 @@ def tri_mul_block_repack(h, view, a_panel, b_panel, mask, ws, ws_bytes, stream=N
 def tri_mul_block_accumulate_packed(h, view, ws, ws_bytes, acc, mask, z_tile, out_tile, reserve_cus=0, stream=None):
     _check(lib().tri_mul_block_accumulate_packed(h, ctypes.byref(view), _ptr(ws), ws_bytes, _ptr(acc), _ptr(mask),
                                                  _ptr(z_tile), _ptr(out_tile), reserve_cus, _stream(stream)))
+
+
+def tri_mul_block_panel_size(h, rows, klen):
+    n = ctypes.c_size_t()
+    _check(lib().tri_mul_block_panel_size(h, rows, klen, ctypes.byref(n)))
+    return n.value
+
+
+def tri_mul_block_project(h, z_tile, ld_z, mask, n_total, row0, col0, rows, cols, direction, a_panel, b_panel,
+                          stream=None):
+    _check(lib().tri_mul_block_project(h, _ptr(z_tile), ld_z, _ptr(mask), n_total, row0, col0, rows, cols,
+                                       direction, _ptr(a_panel), _ptr(b_panel), _stream(stream)))
+
+
+def tri_mul_block_accumulate_blocked(h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, reserve_cus=0,
+                                     stream=None):
+    _check(lib().tri_mul_block_accumulate_blocked(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(acc),
+                                                  _ptr(mask), _ptr(z_tile), _ptr(out_tile), reserve_cus,
+                                                  _stream(stream)))
 
 
 def tri_mul_project(h, z, mask, N, direction, a_panels, b_panels, stream=None):
@@ -424,6 +447,28 @@ class TriMul:
         tri_mul_block_accumulate_packed(self.h, view, ws, ws.numel() * ws.element_size(), acc, mask, z_tile,
                                         out_tile, reserve_cus, stream)
 
+    def block_panel_size(self, rows, klen):
+        return tri_mul_block_panel_size(self.h, rows, klen)
+
+    def block_project(self, z_tile, mask, n_total, row0, col0, direction="outgoing", ld_z=None, stream=None):
+        """The tile's two blocked panels (new bf16 device tensors of
+        block_panel_size elements / 2): z_tile [rows][ld_z][c_z] holds pairs
+        (row0 + i, col0 + j), j < cols = z_tile.shape[1] unless ld_z is given."""
+        d = TRI_MUL_INCOMING if direction in (TRI_MUL_INCOMING, "incoming") else TRI_MUL_OUTGOING
+        rows, cols = z_tile.shape[0], z_tile.shape[1]
+        ldz = cols if ld_z is None else ld_z
+        m, k = (cols, rows) if d == 1 else (rows, cols)
+        n = tri_mul_block_panel_size(self.h, m, k) // 2
+        a = torch.empty(n, dtype=torch.bfloat16, device=z_tile.device)
+        b = torch.empty_like(a)
+        tri_mul_block_project(self.h, z_tile, ldz, mask, n_total, row0, col0, rows, cols, d, a, b, stream)
+        return a, b
+
+    def block_accumulate_blocked(self, view, a_panel, b_panel, acc, mask=None, z_tile=None, out_tile=None,
+                                 reserve_cus=0, stream=None):
+        tri_mul_block_accumulate_blocked(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, reserve_cus,
+                                         stream)
+
 
 # ------------------------------------------------------ panel layout views
 
@@ -432,11 +477,13 @@ def _panel_dims(N, c=128):
     return c, T, S
 
 
-def panel_to_dense(P, N, c=128):
-    """Panel-layout operand (flat) -> dense [c][N][N] (a view copy)."""
-    c, T, S = _panel_dims(N, c)
+def panel_to_dense(P, N, c=128, klen=None):
+    """Panel-layout operand (flat) of N rows and klen (default N)
+    contraction indices -> dense [c][N][klen] (a view copy)."""
+    K = N if klen is None else klen
+    T, S = -(-N // 256), -(-K // 32)
     X = P.reshape(c, T, S, 256, 32).permute(0, 1, 3, 2, 4).reshape(c, T * 256, S * 32)
-    return X[:, :N, :N]
+    return X[:, :N, :K]
 
 
 def dense_to_panel(X):
