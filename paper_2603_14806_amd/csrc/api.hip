@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <cmath>
 #include <mutex>
 #include <new>
 #include <string>
@@ -85,6 +86,26 @@ double to_double(const unsigned char* p, int dtype) {
     float f;
     memcpy(&f, &u, 4);
     return f;
+}
+
+// Round to the nearest fp16 value, ties to even (subnormals included;
+// magnitudes beyond the largest finite value become infinity).
+uint16_t to_f16(double v) {
+    const uint16_t sign = std::signbit(v) ? 0x8000u : 0u;
+    double a = std::fabs(v);
+    if (std::isnan(v)) return 0x7e00u;
+    if (a >= 65520.0) return sign | 0x7c00u;
+    int e;
+    std::frexp(a, &e);                      // a = f * 2^e, f in [0.5, 1)
+    const int q = std::max(e - 11, -24);    // spacing of fp16 values near a: 2^q
+    const double m = std::nearbyint(std::ldexp(a, -q));   // round-half-even (default mode)
+    const double r = std::ldexp(m, q);
+    if (r == 0) return sign;
+    int er;
+    std::frexp(r, &er);
+    if (er <= -14) return sign | (uint16_t)std::ldexp(r, 24);            // subnormal: r / 2^-24
+    const int mant = (int)std::ldexp(r, 11 - er) - 1024;                 // 10 stored bits
+    return sign | (uint16_t)(((er - 1 + 15) << 10) | mant);
 }
 
 uint16_t to_bf16_exact(double v) {   // v is already a bf16 value
@@ -400,6 +421,50 @@ int tri_mul_init(tri_mul_handle_t* out, const tri_mul_params_t* p, void* stream)
                 const std::vector<double>& src = m == 0 ? wa : m == 1 ? wga : m == 2 ? wb : wgb;
                 for (int ch = 0; ch < c; ++ch) pbt[((size_t)d * 4 + m) * c + ch] = to_bf16_exact(src[(size_t)ch * cz + d]);
             }
+        // fp16 projection operands with power-of-two scales: |x| <= sqrt(c_z - 1)
+        // max|gamma| + max|beta| after LayerNorm, and each weight matrix's
+        // largest entry, both brought into [2^14, 2^15] (scales clamped to
+        // 2^-40 .. 2^40; operands that would still exceed the fp16 range
+        // are refused).
+        auto pow2_scale = [](double bound) -> int {
+            if (!(bound > 0)) return 0;
+            int s2 = (int)std::floor(std::log2(32768.0 / bound));
+            return std::max(-40, std::min(40, s2));
+        };
+        double gmax = 0, bmax = 0;
+        for (int d = 0; d < cz; ++d) gmax = std::max(gmax, std::fabs(lnw[d])), bmax = std::max(bmax, std::fabs(lnb[d]));
+        const double xbound = std::sqrt((double)cz - 1.0) * gmax + bmax;
+        const int sx = pow2_scale(xbound);
+        int sw[4];
+        for (int m = 0; m < 4; ++m) {
+            const std::vector<double>& src = m == 0 ? wa : m == 1 ? wga : m == 2 ? wb : wgb;
+            double mx = 0;
+            for (double v2 : src) mx = std::max(mx, std::fabs(v2));
+            sw[m] = pow2_scale(mx);
+            if (mx * std::ldexp(1.0, sw[m]) > 65504.0) rc = fail(TRI_MUL_EUNSUPPORTED, "projection weights beyond the supported range");
+        }
+        if (xbound * std::ldexp(1.0, sx) > 65504.0) rc = fail(TRI_MUL_EUNSUPPORTED, "input LayerNorm parameters beyond the supported range");
+        std::vector<uint16_t> ph((size_t)4 * c * cz);
+        for (int g = 0; g < c / 32; ++g)
+            for (int m = 0; m < 4; ++m)
+                for (int r = 0; r < 32; ++r) {
+                    const std::vector<double>& src = m == 0 ? wa : m == 1 ? wga : m == 2 ? wb : wgb;
+                    const size_t row = (size_t)g * 128 + m * 32 + r;
+                    for (int d = 0; d < cz; ++d) ph[row * cz + d] = to_f16(std::ldexp(src[(size_t)(g * 32 + r) * cz + d], sw[m]));
+                }
+        std::vector<float> lnw_h(cz), lnb_h(cz);
+        for (int d = 0; d < cz; ++d) lnw_h[d] = (float)std::ldexp(lnw[d], sx), lnb_h[d] = (float)std::ldexp(lnb[d], sx);
+        const double log2e = 1.4426950408889634;
+        auto& k = h->w.k1s;
+        k.kv_a = (float)std::ldexp(1.0, sx + sw[0]);
+        k.cg_a = (float)(-log2e * std::ldexp(1.0, -(sx + sw[1])));
+        k.sv_a = (float)(sx + sw[0]);
+        k.kv_b = (float)std::ldexp(1.0, sx + sw[2]);
+        k.cg_b = (float)(-log2e * std::ldexp(1.0, -(sx + sw[3])));
+        k.sv_b = (float)(sx + sw[2]);
+        if (!rc) rc = upload(h, &h->w.proj_h, ph, s);
+        if (!rc) rc = upload(h, &h->w.ln_in_w_h, lnw_h, s);
+        if (!rc) rc = upload(h, &h->w.ln_in_b_h, lnb_h, s);
         if (!rc) rc = upload(h, &h->w.proj_bf, pb, s);
         if (!rc) rc = upload(h, &h->w.epi_bf, eb, s);
         if (!rc) rc = upload(h, &h->w.epit_bf, ebt, s);

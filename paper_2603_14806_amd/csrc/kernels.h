@@ -24,6 +24,19 @@ struct DeviceWeights {
     uint16_t* epi_bf = nullptr;   // [2*c_z][128]: W_o rows then W_g rows
     uint16_t* epit_bf = nullptr;  // [2*128][c_z]: W_o^T rows then W_g^T rows (backward)
     uint16_t* projt_bf = nullptr; // [c_z][4*c]: row d = W_a[:, d], W_ga[:, d], W_b[:, d], W_gb[:, d] (backward)
+    // fp16 copies for the bf16-path projection (K1), each matrix scaled by a
+    // power of two 2^s_m and the LayerNorm gain and bias by 2^s_x, so that
+    // the largest possible |W x| operand lies in [2^14, 2^15]; the gating
+    // undoes the scales (K1Scales).
+    uint16_t* proj_h = nullptr;   // [4*c][c_z] fp16 bits, rows as proj_bf, W_m * 2^s_m
+    float* ln_in_w_h = nullptr;   // [c_z] gamma * 2^s_x
+    float* ln_in_b_h = nullptr;   // [c_z] beta * 2^s_x
+    struct K1Scales {
+        // a = v * sigmoid(g) from accumulators v' = 2^Sv v, g' = 2^Sg g:
+        // a = v' / (2^Sv + 2^(Sv - g log2 e)) = v' * rcp(kv + exp2(g' * cg + Sv))
+        float kv_a, cg_a, sv_a;   // 2^Sv, -log2(e) 2^-Sg, Sv of a
+        float kv_b, cg_b, sv_b;   // the same for b
+    } k1s{};
     float eps = 1e-5f;
     int cus = 256;                // compute units of the device (persistent grids)
     uint8_t* kmask_pad = nullptr; // 0/1 staging of a token mask (k-panel, sequence, or a tile's columns and rows), kMaskStageBytes

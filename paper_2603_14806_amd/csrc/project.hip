@@ -103,11 +103,16 @@ __global__ __launch_bounds__(256) void k1_project_valu(
 // the same number of vector-memory instructions per line (3 loads, 4 stores,
 // tails included), which makes the vmcnt waits exact constants.
 //
-// Precision: the LayerNormed input x (fp32) is split into x_hi = bf16(x) and
-// x_lo = bf16(x - x_hi); with exact bf16 weights W x_hi + W x_lo carries ~16
-// mantissa bits for the projections W_a x and W_b x, so their main error is
-// one bf16 rounding (the store of a and b).  The gates take x_hi alone, as
-// in the epilogue: the logistic's slope (<= 1/4) scales that rounding down.
+// Precision: the matrix cores take fp16 operands, 11 significant bits
+// against bf16's 8.  The weights (bf16 values) and the LayerNormed x
+// (fp32) are scaled by powers of two chosen at initialisation so that the
+// largest possible operand lies in [2^14, 2^15]: the weights convert
+// exactly (down to 2^-17 of that largest entry) and x rounds once to
+// 2^-11 relative, with no overflow and no subnormal x.  So values and gates
+// carry ~11 bits, and the main error of a and b stays their bf16 store.
+// The gating undoes the scales (DeviceWeights::K1Scales) inside the
+// logistic at no extra instruction.
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 constexpr int kP1 = 32;                 // pairs per line
 constexpr int kXRow = kCz * 2;          // bytes of one bf16 row of 128 channels (256)
 constexpr int kZSt = kP1 * kXRow;       // z bytes of one line (8 KB)
@@ -129,11 +134,11 @@ __device__ __forceinline__ uint32_t xoff(int p, int chunk) {
 template <bool INCOMING>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
 void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __restrict__ tmask, int rmoff,
-                     int mrange, int M, int K, int nlines, const bf16_t* __restrict__ wproj,
+                     int mrange, int M, int K, int nlines, const uint16_t* __restrict__ wproj,
                      const float* __restrict__ lnw, const float* __restrict__ lnb, float eps,
-                     bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
+                     DeviceWeights::K1Scales ks, bf16_t* __restrict__ A, bf16_t* __restrict__ B) {
     __shared__ __attribute__((aligned(16))) char ring[kRing * kSt];     // z rows [p][256 B], mask
-    __shared__ __attribute__((aligned(16))) char xs[2][kP1 * kXRow];   // x_hi, x_lo
+    __shared__ __attribute__((aligned(16))) char xs[kP1 * kXRow];      // x (fp16, scaled)
     __shared__ __attribute__((aligned(16))) float os[2][kCh][kP1];      // a, b as [c][p]
     // LayerNorm gain, bias; channel c at (c / 16) * 20 + c % 16, so that the
     // 8 broadcast addresses of a read (c = 16 lq + 4 i) fall in distinct banks
@@ -181,13 +186,13 @@ void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __res
     issue(first, 0);
     issue(first + G, 1);
 
-    bf16x8_t w[4][8];
+    f16x8_t w[4][8];
 #pragma unroll
     for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks)
-            w[ob][ks] = *reinterpret_cast<const bf16x8_t*>(
-                wproj + (size_t)(g * 128 + ob * 32 + (lane & 31)) * kCz + ks * 16 + 8 * (lane >> 5));
+        for (int kq = 0; kq < 8; ++kq)
+            w[ob][kq] = *reinterpret_cast<const f16x8_t*>(
+                wproj + (size_t)(g * 128 + ob * 32 + (lane & 31)) * kCz + kq * 16 + 8 * (lane >> 5));
     if (t < kCz) {
         gb[0][(t >> 4) * 20 + (t & 15)] = lnw[t];
         gb[1][(t >> 4) * 20 + (t & 15)] = lnb[t];
@@ -244,23 +249,14 @@ void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __res
             gam[4 * i] = a4.x; gam[4 * i + 1] = a4.y; gam[4 * i + 2] = a4.z; gam[4 * i + 3] = a4.w;
             bet[4 * i] = b4.x; bet[4 * i + 1] = b4.y; bet[4 * i + 2] = b4.z; bet[4 * i + 3] = b4.w;
         }
-        uint32_t hi[8], lo[8];
+        f16x8_t xh[2];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const float x0 = v[2 * i] * rs * gam[2 * i] + bet[2 * i];
-            const float x1 = v[2 * i + 1] * rs * gam[2 * i + 1] + bet[2 * i + 1];
-            hi[i] = pack_bf16x2(x0, x1);
-            lo[i] = pack_bf16x2(x0 - __uint_as_float(hi[i] << 16), x1 - __uint_as_float(hi[i] & 0xffff0000u));
-        }
-        *reinterpret_cast<uint4*>(xs[0] + xoff(lp, 2 * lq)) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-        *reinterpret_cast<uint4*>(xs[0] + xoff(lp, 2 * lq + 1)) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
-        *reinterpret_cast<uint4*>(xs[1] + xoff(lp, 2 * lq)) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-        *reinterpret_cast<uint4*>(xs[1] + xoff(lp, 2 * lq + 1)) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+        for (int i = 0; i < 16; ++i) xh[i >> 3][i & 7] = (_Float16)(v[i] * rs * gam[i] + bet[i]);
+        *reinterpret_cast<f16x8_t*>(xs + xoff(lp, 2 * lq)) = xh[0];
+        *reinterpret_cast<f16x8_t*>(xs + xoff(lp, 2 * lq + 1)) = xh[1];
         __syncthreads();
 
-        // [W_a; W_b](32 channels) x [x_hi + x_lo](32 pairs); the gates
-        // [W_ga; W_gb] x x_hi (the logistic's slope <= 1/4 damps x_hi's
-        // rounding below that of the bf16 store of a and b)
+        // [W_a; W_ga; W_b; W_gb](32 channels each) x x (32 pairs), all scaled
         f32x16_t acc[4];
 #pragma unroll
         for (int ob = 0; ob < 4; ++ob)
@@ -268,14 +264,11 @@ void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __res
             for (int r = 0; r < 16; ++r) acc[ob][r] = 0.f;
         const int bp = lane & 31;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            const bf16x8_t xh = *reinterpret_cast<const bf16x8_t*>(xs[0] + xoff(bp, 2 * ks + (lane >> 5)));
-            const bf16x8_t xl = *reinterpret_cast<const bf16x8_t*>(xs[1] + xoff(bp, 2 * ks + (lane >> 5)));
+        for (int kq = 0; kq < 8; ++kq) {
+            const f16x8_t xk = *reinterpret_cast<const f16x8_t*>(xs + xoff(bp, 2 * kq + (lane >> 5)));
 #pragma unroll
-            for (int ob = 0; ob < 4; ++ob) {
-                acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xh, acc[ob], 0, 0, 0);
-                if ((ob & 1) == 0) acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ob][ks], xl, acc[ob], 0, 0, 0);
-            }
+            for (int ob = 0; ob < 4; ++ob)
+                acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w[ob][kq], xk, acc[ob], 0, 0, 0);
         }
 
         // Gate, mask, stage as [c][p] fp32.  Lane holds pair (lane & 31); in
@@ -287,8 +280,10 @@ void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __res
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int c = g * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            os[0][c][bp] = __uint_as_float(__float_as_uint(sigmoidf_(acc[1][r]) * acc[0][r]) & keep);
-            os[1][c][bp] = __uint_as_float(__float_as_uint(sigmoidf_(acc[3][r]) * acc[2][r]) & keep);
+            const float ga = __builtin_amdgcn_rcpf(ks.kv_a + __builtin_amdgcn_exp2f(fmaf(acc[1][r], ks.cg_a, ks.sv_a)));
+            const float gb2 = __builtin_amdgcn_rcpf(ks.kv_b + __builtin_amdgcn_exp2f(fmaf(acc[3][r], ks.cg_b, ks.sv_b)));
+            os[0][c][bp] = __uint_as_float(__float_as_uint(ga * acc[0][r]) & keep);
+            os[1][c][bp] = __uint_as_float(__float_as_uint(gb2 * acc[2][r]) & keep);
         }
         __syncthreads();
 
@@ -320,12 +315,12 @@ hipError_t launch_project_mfma(const DeviceWeights& w, const void* z, int64_t ld
     const int mrange = (int)std::max((K + 31) / 32 * 32, rmoff + (M + 3) / 4 * 4);
     if (incoming)
         hipLaunchKernelGGL((k1_project_mfma<true>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, (int)ldz, tmask,
-                           (int)rmoff, mrange, (int)M, (int)K, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps,
-                           (bf16_t*)A, (bf16_t*)B);
+                           (int)rmoff, mrange, (int)M, (int)K, nlines, w.proj_h, w.ln_in_w_h, w.ln_in_b_h, w.eps,
+                           w.k1s, (bf16_t*)A, (bf16_t*)B);
     else
         hipLaunchKernelGGL((k1_project_mfma<false>), dim3(g), dim3(256), 0, s, (const bf16_t*)z, (int)ldz, tmask,
-                           (int)rmoff, mrange, (int)M, (int)K, nlines, w.proj_bf, w.ln_in_w, w.ln_in_b, w.eps,
-                           (bf16_t*)A, (bf16_t*)B);
+                           (int)rmoff, mrange, (int)M, (int)K, nlines, w.proj_h, w.ln_in_w_h, w.ln_in_b_h, w.eps,
+                           w.k1s, (bf16_t*)A, (bf16_t*)B);
     return hipGetLastError();
 }
 
