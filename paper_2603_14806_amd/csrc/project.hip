@@ -252,8 +252,17 @@ void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __res
         f16x8_t xh[2];
 #pragma unroll
         for (int i = 0; i < 16; ++i) xh[i >> 3][i & 7] = (_Float16)(v[i] * rs * gam[i] + bet[i]);
-        *reinterpret_cast<f16x8_t*>(xs + xoff(lp, 2 * lq)) = xh[0];
-        *reinterpret_cast<f16x8_t*>(xs + xoff(lp, 2 * lq + 1)) = xh[1];
+        // A masked pair (and a ragged line's tail: the staged mask is zero
+        // past K) gets x = 0, so W x and with it a and b are exactly 0; the
+        // AND also clears what a NaN in z would have left.
+        const int kc = line / M, r0 = line - kc * M, k0 = kc * kP1;
+        const uint8_t* ms = reinterpret_cast<const uint8_t*>(zs + kZSt + g * 256);   // this wave's copy
+        const uint32_t keep = (ms[lp] & ms[32 + (r0 & 3)]) ? 0xffffffffu : 0u;
+        uint4 x0 = __builtin_bit_cast(uint4, xh[0]), x1 = __builtin_bit_cast(uint4, xh[1]);
+        x0 = make_uint4(x0.x & keep, x0.y & keep, x0.z & keep, x0.w & keep);
+        x1 = make_uint4(x1.x & keep, x1.y & keep, x1.z & keep, x1.w & keep);
+        *reinterpret_cast<uint4*>(xs + xoff(lp, 2 * lq)) = x0;
+        *reinterpret_cast<uint4*>(xs + xoff(lp, 2 * lq + 1)) = x1;
         __syncthreads();
 
         // [W_a; W_ga; W_b; W_gb](32 channels each) x x (32 pairs), all scaled
@@ -271,19 +280,15 @@ void k1_project_mfma(const bf16_t* __restrict__ z, int ldz, const uint8_t* __res
                 acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w[ob][kq], xk, acc[ob], 0, 0, 0);
         }
 
-        // Gate, mask, stage as [c][p] fp32.  Lane holds pair (lane & 31); in
-        // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.  The
-        // staged mask is zero past K, which also zeroes a ragged line's tail.
-        const int kc = line / M, r0 = line - kc * M, k0 = kc * kP1;
-        const uint8_t* ms = reinterpret_cast<const uint8_t*>(zs + kZSt + g * 256);
-        const uint32_t keep = (ms[bp] & ms[32 + (r0 & 3)]) ? 0xffffffffu : 0u;   // branch-free select
+        // Gate and stage as [c][p] fp32.  Lane holds pair (lane & 31); in
+        // register r, channel 32 g + 8 (r / 4) + 4 (lane / 32) + r % 4.
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int c = g * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
             const float ga = __builtin_amdgcn_rcpf(ks.kv_a + __builtin_amdgcn_exp2f(fmaf(acc[1][r], ks.cg_a, ks.sv_a)));
             const float gb2 = __builtin_amdgcn_rcpf(ks.kv_b + __builtin_amdgcn_exp2f(fmaf(acc[3][r], ks.cg_b, ks.sv_b)));
-            os[0][c][bp] = __uint_as_float(__float_as_uint(ga * acc[0][r]) & keep);
-            os[1][c][bp] = __uint_as_float(__float_as_uint(gb2 * acc[2][r]) & keep);
+            os[0][c][bp] = ga * acc[0][r];
+            os[1][c][bp] = gb2 * acc[2][r];
         }
         __syncthreads();
 
