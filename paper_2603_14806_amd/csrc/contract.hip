@@ -291,16 +291,63 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         if constexpr (TB) return lds_read_tr8(st + A_ST + trb + (4 * wn + j) * 2048 + sub * 16 * ROWB);
         else return *reinterpret_cast<const bf16x8_t*>(st + rdB[sub] + j * 32 * ROWB);
     };
+    // Pair-blocked C (CBLOCKED): the wave's 64 rows of each of its four
+    // 32-column blocks go through one buffer descriptor per block, from the
+    // block's first element, with the byte offset (row and lane) in a VGPR,
+    // so that rows >= M fall outside the descriptor (loads read 0, stores
+    // are dropped); a block past C's last column block gets an empty
+    // descriptor.  Columns >= N of C's last block are the layout's padding.
+    const int64_t jblocks = (N + kResJ - 1) / kResJ;
+    const uint32_t crs = (uint32_t)jblocks * (uint32_t)nchan * kResJ;   // floats between rows of C
+    const uint32_t cvo = (4u * (uint32_t)(lane >> 5) * crs + (uint32_t)(lane & 31)) * 4u;
+    auto cdesc = [&](const K2Tile& tl, __amdgpu_buffer_rsrc_t* rc) {
+        const int wrow0 = tl.m0 + (wave >> 1) * 64, wcol0 = tl.n0 + (wave & 1) * 128;
+        const int nrows = min(64, M - wrow0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const bool live = nrows > 0 && wcol0 / kResJ + j < jblocks;
+            rc[j] = make_rsrc(C + result_off(jblocks, nchan, tl.ch, live ? wrow0 : 0, live ? wcol0 + 32 * j : 0),
+                              live ? ((uint32_t)(nrows - 1) * crs + kResJ) * 4u : 0u);
+        }
+    };
+    // byte offset of register r of 32 x 32 block x (rows 32 (x / 4) ..,
+    // column block x % 4) from the lane's base vo.  Each use site passes a
+    // fresh copy of the base (opaque to the compiler), so that the 32 row
+    // offsets are formed where they are used instead of being hoisted out
+    // of the tile loop and kept in registers the accumulators need.
+    auto coff = [&](uint32_t vo, int x, int r) -> uint32_t {
+        return vo + (uint32_t)((x >> 2) * 32 + 8 * (r >> 2) + (r & 3)) * crs * 4u;
+    };
+    auto fresh = [](uint32_t v) {
+        asm volatile("" : "+v"(v));
+        return v;
+    };
     int c_stage = 0;
     for (int it = 0; it < my_tiles; ++it) {
         bf16x8_t a0[MI], b0[4];  // sub-step 0 operands, read one step ahead within a tile
         f32x16_t acc[MI][4];
+        if (CBLOCKED && accumulate) {
+            // accumulating: the accumulators start from C, all 128 loads
+            // issued together and waited for once (one HBM round trip per
+            // tile instead of one per 32 x 32 block at the end)
+            __amdgpu_buffer_rsrc_t rc[4];
+            cdesc(k2_decode(it * G + perm, tiles_m, tiles_n), rc);
+            const uint32_t vo = fresh(cvo);
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+            for (int x = 0; x < 4 * MI; ++x)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+                for (int r = 0; r < 16; ++r)
+                    acc[x >> 2][x & 3][r] =
+                        __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc[x & 3], coff(vo, x, r), 0, 0));
+            wait_vmcnt_pinned<0>();
+        } else {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+        }
 
         // a tile's first step: barrier, then its sub-step 0 operands (nothing
         // is read ahead across the C stores)
@@ -344,9 +391,20 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         const int ch = tl.ch, m0 = tl.m0, n0 = tl.n0;
         const int row0 = m0 + wm * 64 + 4 * hi, col0 = n0 + wn * 128 + rl;
         const bool full = m0 + BM <= M && n0 + BN <= N;
-        const int64_t jblocks = (N + kResJ - 1) / kResJ;
-        float* Cb = CBLOCKED ? C + result_off(jblocks, nchan, ch, row0, col0) : C + ch * sC + (int64_t)row0 * ldc + col0;
-        const int64_t row_step = CBLOCKED ? jblocks * nchan * kResJ : ldc;   // elements between rows
+        if constexpr (CBLOCKED) {   // the sums (C included when accumulating) go straight out
+            __amdgpu_buffer_rsrc_t rc[4];
+            cdesc(tl, rc);
+            const uint32_t vo = fresh(cvo);
+#pragma unroll
+            for (int x = 0; x < 4 * MI; ++x)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[x >> 2][x & 3][r]), rc[x & 3],
+                                                          coff(vo, x, r), 0, 0);
+            continue;
+        }
+        float* Cb = C + ch * sC + (int64_t)row0 * ldc + col0;
+        const int64_t row_step = ldc;   // elements between rows
         // One 32 x 32 block at a time.  Accumulating, the block's 16 loads
         // go out together (a lane outside C reads C[0] instead) and are
         // waited for once, before its 16 guarded stores; element by element
@@ -355,7 +413,7 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                float* pb = Cb + (CBLOCKED ? (int64_t)j * nchan * kResJ : j * 32);   // column block j
+                float* pb = Cb + j * 32;   // column block j
                 const bool colok = full || col0 + j * 32 < N;
                 float v[16];
 #pragma unroll
@@ -500,6 +558,14 @@ hipError_t launch_panel_block(const void* P, int64_t rows, int64_t ld, int64_t k
     return hipGetLastError();
 }
 
+// The pair-blocked result is addressed per 64 rows of a column block with
+// 32-bit byte offsets: 64 rows of jblocks * batch * 32 floats must stay
+// below 4 GiB (N = 65536 with 128 channels uses half of it).
+bool cblocked_fits(int64_t N, int batch) {
+    const int64_t rs = (N + kResJ - 1) / kResJ * batch * kResJ;
+    return 64 * rs * 4 < ((int64_t)1 << 32);
+}
+
 // Pacing needs whole XCD groups (G a multiple of 8, all resident) and at
 // least two full rounds; it resets the counters first (a kernel, not a
 // memset, so that the sequence can be captured in a graph).
@@ -530,6 +596,7 @@ hipError_t launch_contract_blocked_packed(const void* A, const void* B, float* C
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
     const int grid = total < cus ? total : cus;
+    if (!cblocked_fits(N, batch)) return hipErrorInvalidValue;
     const int pace = pace_launch(grid, total, s);
     hipLaunchKernelGGL((k2_contract_ws<true, false, true>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A,
                        (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, (int64_t)0, (int64_t)0, (int64_t)0,
@@ -543,7 +610,7 @@ hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void*
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
     const int grid = total < cus ? total : cus;
-    if (!tb) return hipErrorInvalidValue;
+    if (!tb || !cblocked_fits(N, batch)) return hipErrorInvalidValue;
     const int pace = pace_launch(grid, total, s);
 #define K2_TR(TA_, TB_)                                                                                             \
     hipLaunchKernelGGL((k2_contract_ws<true, false, true, TA_, TB_>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A, \
@@ -590,6 +657,7 @@ hipError_t launch_contract(int dtype, int blocked, const void* A, const void* B,
     const int grid = total < cus ? total : cus;
     const bf16_t* a = (const bf16_t*)A;
     const bf16_t* b = (const bf16_t*)B;
+    if (blocked && !cblocked_fits(N, batch)) return hipErrorInvalidValue;
     const int pace = pace_launch(grid, total, s);
 #define K2_WS(BL, KM)                                                                                              \
     hipLaunchKernelGGL((k2_contract_ws<BL, KM, BL>), dim3(grid), dim3(768), 0, s, a, b, C, (int)M, (int)N, (int)K, \
