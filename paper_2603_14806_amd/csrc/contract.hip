@@ -521,7 +521,16 @@ __global__ void k_stage_kmask(const uint8_t* __restrict__ mask, int klen, int pa
 __global__ __launch_bounds__(256) void k_panel_block(const bf16_t* __restrict__ P, int rows, int ld, int64_t sP,
                                                      int tiles, int nk, const uint8_t* __restrict__ kst,
                                                      bf16_t* __restrict__ dst) {
-    const int kp = blockIdx.x, tile = blockIdx.y, c = blockIdx.z, t = threadIdx.x;
+    // Work-groups are dealt to the 8 XCDs round-robin by linear index; give
+    // each XCD a contiguous run of (k-step pair, tile, channel) units, k-step
+    // pairs fastest, so that the two 128-byte lines a row segment straddles
+    // (rows are ld * 2 bytes apart, rarely a multiple of 128) are fetched
+    // into one XCD's L2 and serve both neighbouring units.
+    const unsigned gx = gridDim.x, gy = gridDim.y;
+    const unsigned nu = gx * gy * gridDim.z, lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+    const unsigned per = nu >> 3, extra = nu & 7, xcd = lin & 7;
+    const unsigned u = xcd * per + min(xcd, extra) + (lin >> 3);   // a bijection of [0, nu)
+    const int kp = (int)(u % gx), tile = (int)((u / gx) % gy), c = (int)(u / (gx * gy)), t = threadIdx.x;
     const int r0 = tile * 256;
     const int nrow = min(256, rows - r0);
     const int e = t & 7, h = e >> 2, q = e & 3;   // k-step 2 kp + h, k = 8 q .. + 7 within it
