@@ -52,6 +52,24 @@ int tri_mul_check_contract_loads(int a_mode, int b_mode, int64_t M, int64_t N, i
                                  int64_t ldb, int64_t a_stride, int64_t b_stride, int batch, uint64_t a_bytes,
                                  uint64_t b_bytes, int grid, int all_channels, tri_mul_load_check_t* out);
 
+/*
+ * The same walk over the contraction kernel's accesses to its result C in
+ * the pair-blocked result layout (tri_mul_contract): M rows, N columns,
+ * `batch` channels, element (b, i, j) at ((i * J + j / 32) * batch + b) * 32
+ * + j % 32 floats with J = ceil(N / 32), c_bytes allocated.  Each MFMA wave
+ * reads (when accumulating) and writes its 64 x 128 part of a tile through
+ * one buffer descriptor per 32-column block.  Reports in *out: tiles, the
+ * 64-lane register groups visited (loads), the elements with row < M and
+ * column < N visited (elems), descriptors reaching outside c_bytes
+ * (bad_desc), and accesses at an address other than the layout's, inside
+ * the descriptor but outside C's rows or column blocks, or elements
+ * accessed never or more than once (bad_elem); bad_tiles is 0.
+ * all_channels as above.  Host only.  Returns TRI_MUL_OK, or
+ * TRI_MUL_EINVAL for null `out` or sizes outside [1, 65536].
+ */
+int tri_mul_check_contract_result(int64_t M, int64_t N, int batch, uint64_t c_bytes, int all_channels,
+                                  tri_mul_load_check_t* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1162,4 +1162,15 @@ int tri_mul_check_contract_loads(int a_mode, int b_mode, int64_t M, int64_t N, i
     return ok();
 }
 
+int tri_mul_check_contract_result(int64_t M, int64_t N, int batch, uint64_t c_bytes, int all_channels,
+                                  tri_mul_load_check_t* out) {
+    if (!out) return fail(TRI_MUL_EINVAL, "null out");
+    if (M < 1 || N < 1 || batch < 1 || M > kMaxN || N > kMaxN)
+        return fail(TRI_MUL_EINVAL, "sizes must lie in [1, %lld]", (long long)kMaxN);
+    trimul::K2CheckCounts n;
+    trimul::k2_check_c(M, N, batch, c_bytes, all_channels, n);
+    *out = tri_mul_load_check_t{n.tiles, n.loads, n.elems, n.bad_tiles, n.bad_desc, n.bad_elem};
+    return ok();
+}
+
 }  // extern "C"

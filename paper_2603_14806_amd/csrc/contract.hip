@@ -291,33 +291,24 @@ void k2_contract_ws(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, 
         if constexpr (TB) return lds_read_tr8(st + A_ST + trb + (4 * wn + j) * 2048 + sub * 16 * ROWB);
         else return *reinterpret_cast<const bf16x8_t*>(st + rdB[sub] + j * 32 * ROWB);
     };
-    // Pair-blocked C (CBLOCKED): the wave's 64 rows of each of its four
-    // 32-column blocks go through one buffer descriptor per block, from the
-    // block's first element, with the byte offset (row and lane) in a VGPR,
-    // so that rows >= M fall outside the descriptor (loads read 0, stores
-    // are dropped); a block past C's last column block gets an empty
-    // descriptor.  Columns >= N of C's last block are the layout's padding.
-    const int64_t jblocks = (N + kResJ - 1) / kResJ;
-    const uint32_t crs = (uint32_t)jblocks * (uint32_t)nchan * kResJ;   // floats between rows of C
-    const uint32_t cvo = (4u * (uint32_t)(lane >> 5) * crs + (uint32_t)(lane & 31)) * 4u;
+    // Pair-blocked C (CBLOCKED): descriptors and offsets from k2_addr.h
+    // (rows past M fall outside a block's descriptor: loads read 0, stores
+    // are dropped).
+    const uint32_t crs = k2_c_row_floats(N, nchan);
+    const uint32_t cvo = k2_c_lane_off(crs, lane);
     auto cdesc = [&](const K2Tile& tl, __amdgpu_buffer_rsrc_t* rc) {
-        const int wrow0 = tl.m0 + (wave >> 1) * 64, wcol0 = tl.n0 + (wave & 1) * 128;
-        const int nrows = min(64, M - wrow0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const bool live = nrows > 0 && wcol0 / kResJ + j < jblocks;
-            rc[j] = make_rsrc(C + result_off(jblocks, nchan, tl.ch, live ? wrow0 : 0, live ? wcol0 + 32 * j : 0),
-                              live ? ((uint32_t)(nrows - 1) * crs + kResJ) * 4u : 0u);
+            const K2Desc d = k2_c_desc(M, N, nchan, tl, wave, j);
+            rc[j] = make_rsrc(C + d.base, d.range);
         }
     };
-    // byte offset of register r of 32 x 32 block x (rows 32 (x / 4) ..,
-    // column block x % 4) from the lane's base vo.  Each use site passes a
-    // fresh copy of the base (opaque to the compiler), so that the 32 row
-    // offsets are formed where they are used instead of being hoisted out
-    // of the tile loop and kept in registers the accumulators need.
-    auto coff = [&](uint32_t vo, int x, int r) -> uint32_t {
-        return vo + (uint32_t)((x >> 2) * 32 + 8 * (r >> 2) + (r & 3)) * crs * 4u;
-    };
+    // byte offset of register r of 32 x 32 block x from the lane's base vo.
+    // Each use site passes a fresh copy of the base (opaque to the
+    // compiler), so that the 32 row offsets are formed where they are used
+    // instead of being hoisted out of the tile loop and kept in registers
+    // the accumulators need.
+    auto coff = [&](uint32_t vo, int x, int r) -> uint32_t { return vo + k2_c_reg_off(crs, x, r); };
     auto fresh = [](uint32_t v) {
         asm volatile("" : "+v"(v));
         return v;
@@ -745,6 +736,53 @@ void k2_check_operand(const K2Operand& op, uint64_t bytes, int ch, K2CheckCounts
     }
 }
 }  // namespace
+
+void k2_check_c(int64_t M, int64_t N, int batch, uint64_t c_bytes, int all_channels, K2CheckCounts& n) {
+    n = K2CheckCounts{};
+    const int tm = (int)((M + kK2Tile - 1) / kK2Tile), tn = (int)((N + kK2Tile - 1) / kK2Tile);
+    const int J = (int)((N + kResJ - 1) / kResJ);
+    const uint32_t crs = k2_c_row_floats((int)N, batch);
+    n.tiles = (int64_t)tm * tn * batch;
+    for (int ch = 0; ch < batch; ++ch) {
+        if (!all_channels && ch != 0 && ch != batch - 1) continue;
+        std::vector<uint8_t> hit((size_t)M * (size_t)N, 0);
+        for (int ti = 0; ti < tm; ++ti)
+            for (int tj = 0; tj < tn; ++tj) {
+                const K2Tile t{ch, ti * kK2Tile, tj * kK2Tile};
+                for (int wave = 0; wave < 8; ++wave)
+                    for (int j = 0; j < 4; ++j) {
+                        const K2Desc d = k2_c_desc((int)M, (int)N, batch, t, wave, j);
+                        if (d.range && (d.base < 0 || (uint64_t)d.base * 4 + d.range > c_bytes)) ++n.bad_desc;
+                        for (int xr = 0; xr < 2; ++xr) {
+                            const int x = 4 * xr + j;
+                            ++n.loads;
+                            for (int r = 0; r < 16; ++r)
+                                for (int lane = 0; lane < 64; ++lane) {
+                                    int row, col;
+                                    k2_c_elem(t, wave, lane, x, r, row, col);
+                                    const uint64_t off = (uint64_t)k2_c_lane_off(crs, lane) + k2_c_reg_off(crs, x, r);
+                                    const bool in = off < d.range;
+                                    if (!in) {   // must be a row past M or a column block past C's last
+                                        if (row < M && col / kResJ < J) ++n.bad_elem;
+                                        continue;
+                                    }
+                                    // accessed: the element the layout puts there, inside C
+                                    const int64_t want = result_off(J, batch, ch, row, col);
+                                    if (off % 4 || d.base + (int64_t)(off / 4) != want || row >= M || col / kResJ >= J)
+                                        ++n.bad_elem;
+                                    if (row < M && col < N) {
+                                        ++n.elems;
+                                        uint8_t& h = hit[(size_t)row * N + col];
+                                        if (h) ++n.bad_elem;
+                                        h = 1;
+                                    }
+                                }
+                        }
+                    }
+            }
+        for (uint8_t h : hit) n.bad_elem += h ? 0 : 1;
+    }
+}
 
 void k2_check_loads(int a_mode, int b_mode, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t sA,
                     int64_t sB, int batch, uint64_t a_bytes, uint64_t b_bytes, int grid, int all_channels,

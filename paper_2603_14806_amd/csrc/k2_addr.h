@@ -155,4 +155,45 @@ __host__ __device__ __forceinline__ uint32_t k2_lds_off(int lw, int jj) {
     return (uint32_t)(lw * 64 + 16 * jj) * kK2Row;
 }
 
+// ------------------------------------------------------------- pair-blocked C
+//
+// The result C of nch channels in the pair-blocked layout (result_off):
+// element (ch, i, j) at ((i * J + j / 32) * nch + ch) * 32 + j % 32 floats,
+// J = ceil(N / 32); a row is crs = J * nch * 32 floats long.  MFMA wave w
+// (0..7) of a tile owns its rows 64 (w / 2) .. + 63 and columns
+// 128 (w % 2) .. + 127, as eight 32 x 32 blocks x = 4 (rows / 32) + column
+// block; in the accumulator layout lane l holds column l % 32 and, in
+// register r, row 8 (r / 4) + 4 (l / 32) + r % 4 of a block.  Each of the
+// wave's four column blocks goes through one descriptor from the block's
+// first element whose range covers the rows < M, so that rows past M fall
+// outside it; a column block past C's last gets the empty descriptor (its
+// memory belongs to the next row).  Columns past N inside C's last block
+// are the layout's padding and are accessed like the rest.  The byte offset
+// is the lane part (k2_c_lane_off) plus the wave-uniform part of block x,
+// register r (k2_c_reg_off); both travel in the lane offset.
+__host__ __device__ __forceinline__ uint32_t k2_c_row_floats(int N, int nch) {
+    return (uint32_t)((N + kResJ - 1) / kResJ) * (uint32_t)nch * kResJ;
+}
+__host__ __device__ __forceinline__ K2Desc k2_c_desc(int M, int N, int nch, const K2Tile& t, int wave, int j) {
+    const int jblocks = (N + kResJ - 1) / kResJ;
+    const int wrow0 = t.m0 + (wave >> 1) * 64, wcol0 = t.n0 + (wave & 1) * 128;
+    const int nrows = M - wrow0 < 64 ? M - wrow0 : 64;
+    const bool live = nrows > 0 && wcol0 / kResJ + j < jblocks;
+    K2Desc d;
+    d.base = live ? result_off(jblocks, nch, t.ch, wrow0, wcol0 + kResJ * j) : 0;
+    d.range = live ? ((uint32_t)(nrows - 1) * k2_c_row_floats(N, nch) + kResJ) * 4u : 0u;
+    return d;
+}
+__host__ __device__ __forceinline__ uint32_t k2_c_lane_off(uint32_t crs, int lane) {
+    return (4u * (uint32_t)(lane >> 5) * crs + (uint32_t)(lane & 31)) * 4u;
+}
+__host__ __device__ __forceinline__ uint32_t k2_c_reg_off(uint32_t crs, int x, int r) {
+    return (uint32_t)((x >> 2) * 32 + 8 * (r >> 2) + (r & 3)) * crs * 4u;
+}
+// The logical row and column of that element (for the host check).
+__host__ __device__ __forceinline__ void k2_c_elem(const K2Tile& t, int wave, int lane, int x, int r, int& row, int& col) {
+    row = t.m0 + (wave >> 1) * 64 + (x >> 2) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    col = t.n0 + (wave & 1) * 128 + (x & 3) * 32 + (lane & 31);
+}
+
 }  // namespace trimul

@@ -84,6 +84,11 @@ struct K2CheckCounts {
 void k2_check_loads(int a_mode, int b_mode, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t sA,
                     int64_t sB, int batch, uint64_t a_bytes, uint64_t b_bytes, int grid, int all_channels,
                     K2CheckCounts& n);
+// The same for the accesses to a pair-blocked C of M rows, N columns and `batch` channels (the result layout,
+// c_bytes allocated): every load / store descriptor inside the allocation, every accessed element at the
+// layout's address, every element (row < M, column < N) accessed exactly once (loads counts the 64-lane
+// register groups visited).
+void k2_check_c(int64_t M, int64_t N, int batch, uint64_t c_bytes, int all_channels, K2CheckCounts& n);
 
 struct EpilogueArgs {
     const float* C;      // fp32 contraction result: pair-blocked (cblocked) or [c][rows][ldc]

@@ -117,6 +117,8 @@ SIGNATURES = {
     "tri_mul_check_contract_loads": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64,
                                                     _i64, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int,
                                                     ctypes.c_int, ctypes.POINTER(LoadCheck)]),
+    "tri_mul_check_contract_result": (ctypes.c_int, [_i64, _i64, ctypes.c_int, ctypes.c_uint64, ctypes.c_int,
+                                                      ctypes.POINTER(LoadCheck)]),
     "tri_attn_state_size": (ctypes.c_int, [ctypes.POINTER(TriAttnView), ctypes.POINTER(ctypes.c_size_t)]),
     "tri_attn_chunk": (ctypes.c_int, [ctypes.POINTER(TriAttnView), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "tri_attn_forward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, ctypes.c_int32, _i64, ctypes.c_int32,
@@ -641,4 +643,12 @@ def check_contract_loads(a_mode, b_mode, M, N, K, lda=0, ldb=0, a_stride=0, b_st
     out = LoadCheck()
     _check(lib().tri_mul_check_contract_loads(a_mode, b_mode, M, N, K, lda, ldb, a_stride, b_stride, batch, a_bytes,
                                               b_bytes, grid, int(all_channels), ctypes.byref(out)))
+    return {name: getattr(out, name) for name, _ in LoadCheck._fields_}
+
+
+def check_contract_result(M, N, batch=128, c_bytes=0, all_channels=False):
+    """Host-side walk over the contraction kernel's accesses to a pair-blocked
+    C (tri_mul_check_contract_result); returns the counts as a dict."""
+    out = LoadCheck()
+    _check(lib().tri_mul_check_contract_result(M, N, batch, c_bytes, int(all_channels), ctypes.byref(out)))
     return {name: getattr(out, name) for name, _ in LoadCheck._fields_}

@@ -129,3 +129,47 @@ def test_bad_arguments_rejected():
                                b_bytes=1 << 20)
     with pytest.raises(T.TriMulError):
         T.check_contract_loads(3, BLK, 10, 10, 10, a_bytes=1 << 20, b_bytes=1 << 20)
+
+
+# ------------------------------------------------- the result C (pair-blocked)
+
+def result_bytes(rows, cols, nch=128):
+    """[rows][ceil(cols/32)][nch][32] fp32 (tri_mul_contract's result layout)."""
+    return rows * ceil(cols, 32) * nch * 32 * 4
+
+
+def assert_clean_result(r, rows, cols, channels_visited):
+    assert r["bad_desc"] == 0, r
+    assert r["bad_elem"] == 0, r
+    assert r["elems"] == rows * cols * channels_visited, r
+
+
+@pytest.mark.parametrize("n", SIZES)
+def test_result_full_update(n):
+    # the full update's C, the backward products' dA / dB, the stage call's C
+    r = T.check_contract_result(n, n, 128, c_bytes=result_bytes(n, n), all_channels=n <= 33)
+    assert_clean_result(r, n, n, 128 if n <= 33 else 2)
+
+
+@pytest.mark.parametrize("view", VIEWS)
+def test_result_packed_accumulator(view):
+    # a device tile's packed accumulator (tri_mul_block_accumulator_size)
+    rows, cols = view[0], view[1]
+    r = T.check_contract_result(rows, cols, 128, c_bytes=result_bytes(rows, cols), all_channels=rows * cols < 1e4)
+    assert_clean_result(r, rows, cols, 128 if rows * cols < 1e4 else 2)
+
+
+@pytest.mark.parametrize("shape", [(1024, 1024), (100, 257), (3, 5)])
+def test_result_outer_product_mean(shape):
+    rows, cols = shape
+    # sums: (token, c) rows and columns, one channel; counts: tokens
+    r = T.check_contract_result(32 * rows, 32 * cols, 1, c_bytes=result_bytes(32 * rows, 32 * cols, 1))
+    assert_clean_result(r, 32 * rows, 32 * cols, 1)
+    r = T.check_contract_result(rows, cols, 1, c_bytes=result_bytes(rows, cols, 1))
+    assert_clean_result(r, rows, cols, 1)
+
+
+def test_result_short_allocation_is_reported():
+    n = 300
+    r = T.check_contract_result(n, n, 128, c_bytes=result_bytes(n, n) - 4)
+    assert r["bad_desc"] > 0
