@@ -146,10 +146,23 @@ def test_config5_tile_of_8x8_grid_n30000():
     valid = (mask_h[row0 + I] != 0)[:, None] & (mask_h[col0 + J] != 0)[None, :]
     v0 = T.BlockView(n_total, row0, col0, b, b, 0, b, ld, ld, 0, g)
     ws = torch.empty(layer.block_workspace_size(v0), dtype=torch.uint8, device="cuda")
-    for mode in ("plain", "ws", "packed"):
+    outs = {}
+    for mode in ("plain", "ws", "packed", "blocked"):
         acc.fill_(float("nan"))   # the first ring step must overwrite every element
         out.fill_(float("nan"))
-        if mode == "packed":
+        if mode == "blocked":
+            # the panels in the contraction's blocked layout (here made by the
+            # repack, as tri_mul_block_project would send them) contracted by
+            # tri_mul_block_accumulate_blocked
+            pacc = torch.full((layer.block_accumulator_size(v0) // 4,), float("nan"), device="cuda")
+            ob = -(-layer.block_panel_size(b, b) // 256) * 256
+            for p in range(g):
+                v = T.BlockView(n_total, row0, col0, b, b, p * b, b, ld, ld, p, g)
+                layer.block_repack(v, aps[p], bps[p], mask, ws)
+                layer.block_accumulate_blocked(v, ws, ws[ob:], pacc, mask, z_tile, out)
+            torch.cuda.synchronize()
+            acc.copy_(T.result_to_dense(pacc, b, cols=b))
+        elif mode == "packed":
             # the next panel's repack on a second stream while the current one
             # is contracted on 16 fewer compute units; two workspaces
             pacc = torch.full((layer.block_accumulator_size(v0) // 4,), float("nan"), device="cuda")
@@ -171,6 +184,60 @@ def test_config5_tile_of_8x8_grid_n30000():
         assert_close(got[valid], ref[valid], "bf16", "c5 sampled valid pairs")
         assert np.all(got[~valid] == 0)
         assert torch.isfinite(out).all() and torch.isfinite(acc).all()
+        outs[mode] = out.clone()
+    # the same kernel on the same blocked panels, in one stream or two
+    assert torch.equal(outs["blocked"], outs["packed"])
+    del outs
+
+
+@pytest.mark.parametrize("direction", DIRS)
+def test_config5_tile_projection_sampled(direction):
+    """tri_mul_block_project on the 3750 x 3750 z tile (7, 7) of the 8 x 8
+    grid at N = 30000 (the last 300 tokens padded): the blocked a and b
+    panels at sampled (operand row, k) positions, every channel, against the
+    oracle's projection of those pairs, to the projection's per-element
+    bound (one bf16 rounding of the result; values and gates from x rounded
+    once to fp16, 2^-11 |W| |x| and, through the 1/4-Lipschitz logistic,
+    2^-13 |W_g| |x| |W x|)."""
+    n_total, g = 30000, 8
+    b = n_total // g
+    row0 = col0 = 7 * b
+    say(f"config 5 tile projection: {b}x{b} at ({row0},{col0}) {direction}")
+    layer, W = make_layer("bf16", affine=True)
+    mask = synth.token_mask(n_total, 300, device="cuda")
+    z_tile = synth.pair_tensor(0, dtype="bf16", device="cuda", name="z_tile", shape=(b, b, 128))
+    A, B = layer.block_project(z_tile, mask, n_total, row0, col0, direction)
+    torch.cuda.synchronize()
+    I = sample_index(b, 50, 15, extra=(3449, 3450, 3451, 3700, 3749))   # operand rows
+    K = sample_index(b, 50, 16, extra=(3449, 3450, 3451, 3700, 3749))   # contraction index
+    Tt, S = -(-b // 256), -(-b // 32)
+    c = np.arange(128)[:, None, None]
+    i, k = I[None, :, None], K[None, None, :]
+    flat = ((c * Tt + i // 256) * S + k // 32) * 8192 + (i % 256) * 32 + k % 32
+    fi = torch.as_tensor(flat.reshape(-1), device="cuda")
+    got_a = host(A[fi]).reshape(128, len(I), len(K))
+    got_b = host(B[fi]).reshape(128, len(I), len(K))
+    # pair of operand row i, index k: (row0 + i, col0 + k) outgoing, (row0 + k, col0 + i) incoming
+    zi, zk = (K, I) if direction == "incoming" else (I, K)
+    It, Kt = torch.as_tensor(zi, device="cuda"), torch.as_tensor(zk, device="cuda")
+    zp = host(z_tile[It][:, Kt])                                        # [len(zi)][len(zk)][128]
+    mh = host(mask)
+    mp = oracle.pair_mask(mh[row0 + zi], mh[col0 + zk])
+    ra, rb, _ = oracle.project(zp, mp, W)
+    x = oracle.layer_norm(zp, W["ln_in_w"], W["ln_in_b"])
+    ax = np.abs(x)
+    for got, ref, wv, wg, name in ((got_a, ra, "w_a", "w_ga", "a"), (got_b, rb, "w_b", "w_gb", "b")):
+        p = np.abs(oracle.linear(x, W[wv]))
+        extra = mp[..., None] * (2.0 ** -13 * (ax @ np.abs(W[wg]).T) * p + 2.0 ** -11 * (ax @ np.abs(W[wv]).T))
+        if direction == "incoming":
+            ref, extra = ref.transpose(1, 0, 2), extra.transpose(1, 0, 2)
+        ref, extra = ref.transpose(2, 0, 1), extra.transpose(2, 0, 1)   # [c][operand row][k]
+        bound = 2.0 ** -8 * np.abs(ref) + (1 + 2.0 ** -8) * extra + 1e-5
+        mx, rel = errors(got, ref)
+        say(f"  {name}: max_abs={mx:.2e} rel_fro={rel:.2e}")
+        assert not (np.abs(got - ref) > bound).any(), f"{name}: elements beyond the bound"
+        dead = mp == 0 if direction == "outgoing" else (mp == 0).T
+        assert np.all(got[:, dead] == 0)
 
 
 @pytest.mark.parametrize("direction", DIRS)
