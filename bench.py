@@ -220,7 +220,7 @@ def measured_traffic():
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "k2_contract_traffic.json")))
         csrc = os.path.join(ROOT, "paper_2603_14806_amd", "csrc")
-        src = open(os.path.join(csrc, "contract.hip"), "rb").read() + open(os.path.join(csrc, "common.h"), "rb").read()
+        src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("contract.hip", "common.h", "k2_addr.h"))
         if hashlib.sha256(src).hexdigest() == rec["source_sha256"]:
             return rec["traffic_bytes_per_launch"]
     except (OSError, KeyError, ValueError):
