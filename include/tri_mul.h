@@ -117,7 +117,11 @@ typedef struct {
 
 /* Create a handle: validates `p`, allocates device buffers for the repacked
  * weights and copies them (synchronously with respect to `stream`).
- * Returns TRI_MUL_EUNSUPPORTED unless c_z == c == 128. */
+ * Returns TRI_MUL_EUNSUPPORTED unless c_z == c == 128, and (bf16 storage)
+ * when a projection weight matrix or the input LayerNorm's gain and bias are
+ * so large that the projection's fp16 matrix-core operands would overflow
+ * even scaled by 2^-40 (a largest |W| entry, or sqrt(c_z - 1) max|gamma| +
+ * max|beta|, above about 6.5e4 * 2^40). */
 int tri_mul_init(tri_mul_handle_t* h, const tri_mul_params_t* p, void* stream);
 
 /* Free the handle's device buffers (after the device has finished with

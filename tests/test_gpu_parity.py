@@ -324,3 +324,34 @@ def test_abi_errors_on_device():
     torch.cuda.synchronize()
     layer.close()
     layer.close()
+
+
+def test_init_range_of_projection_operands():
+    """The bf16 path's projection runs on fp16 operands scaled by powers of
+    two chosen at init: weights and LayerNorm parameters far apart in
+    magnitude still give the oracle's projections (to the projection's
+    per-element bound, through the whole update), and values beyond what
+    the largest scale can bring into fp16 range are refused."""
+    W = synth.weights(128, 128, dtype="bf16", affine=True)
+    for name, f in (("w_a", 2.0 ** -30), ("w_gb", 2.0 ** 20), ("ln_in_w", 2.0 ** -25), ("ln_in_b", 2.0 ** -25)):
+        W[name] = (W[name].double() * f).to(torch.bfloat16)
+    layer = T.TriMul(W, dtype="bf16", out_dtype="f32")
+    Wd = {k: oracle.f64(v) for k, v in W.items()}
+    N = 40
+    z = synth.pair_tensor(N, dtype="bf16")
+    mask = synth.random_mask(N, 0.9)
+    for direction in DIRS:
+        A, B = layer.project(z.cuda(), mask.cuda(), direction)
+        torch.cuda.synchronize()
+        rA, rB = oracle.projected_panels(z, mask, Wd, direction)
+        for got, ref in ((A, rA), (B, rB)):
+            mx, rel = errors(host(T.panel_to_dense(got, N)), ref)
+            say(f"  scaled weights {direction}: rel_fro={rel:.2e}")
+            assert rel <= 4e-3
+    layer.close()
+    for name in ("w_ga", "ln_in_w"):
+        Wb = dict(W)
+        Wb[name] = torch.full_like(W[name], 1e30)
+        with pytest.raises(T.TriMulError) as e:
+            T.TriMul(Wb, dtype="bf16", out_dtype="f32")
+        assert "supported range" in str(e.value)
