@@ -136,6 +136,13 @@ class ClockSampler:
         v = sorted(self.samples)
         return {"mean_MHz": round(sum(v) / len(v), 1), "min_MHz": v[0], "max_MHz": v[-1], "samples": len(v)}
 
+    def adjusted_basis(self, min_samples=10):
+        """The mean clock for the clock-adjusted fraction, or None when the
+        timed region was too short for a steady reading (a one-step run
+        catches the clock still ramping and would overstate the fraction)."""
+        c = self.summary()
+        return None if c is None or c["samples"] < min_samples else c
+
 
 def gpu_state():
     """Current graphics and memory clocks (and socket power, where exposed) of
@@ -600,6 +607,7 @@ def main():
     layer_flops = 2 * fl["total"]
     contract_tflops = fl["contract"] / (k_ms["contract"] * 1e-3) / 1e12
     clk = clocks.summary()
+    clk_adj = clocks.adjusted_basis()
 
     def hbm_roof(nbytes, ms):
         a = nbytes / (ms * 1e-3) / 1e9
@@ -622,8 +630,8 @@ def main():
         "ms_per_layer_median": round(step_median, 4), "ms_per_layer_min": round(per_step[0], 4),
         "gpu_state": {"before": state_before, "after": gpu_state()},
         "contract_pct_of_bf16_peak": round(100 * contract_tflops / perf.PEAK_BF16_TFLOPS, 2),
-        "contract_pct_of_bf16_peak_clock_adjusted": None if clk is None else
-            round(100 * contract_tflops / perf.bf16_peak_at(clk["mean_MHz"]), 2),
+        "contract_pct_of_bf16_peak_clock_adjusted": None if clk_adj is None else
+            round(100 * contract_tflops / perf.bf16_peak_at(clk_adj["mean_MHz"]), 2),
         "sclk_during_timed_steps": clk,
         "kernels": {
             "project": {"ms": round(k_ms["project"], 4),
@@ -692,8 +700,8 @@ def main():
                                    "contraction, dz and all ten weight gradients; not part of ms_per_step"},
         "roofline": {"bound": "mfma", "achieved": round(contract_tflops, 2), "peak": perf.PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(contract_tflops / perf.PEAK_BF16_TFLOPS, 4),
-                     "frac_clock_adjusted": None if clk is None else
-                         round(contract_tflops / perf.bf16_peak_at(clk["mean_MHz"]), 4),
+                     "frac_clock_adjusted": None if clk_adj is None else
+                         round(contract_tflops / perf.bf16_peak_at(clk_adj["mean_MHz"]), 4),
                      "traffic": measured_traffic(), "kernel": "k2_contract_ws",
                      "per_launch": f"2*N^3*c = {fl['contract']:.4e} flop (128 channels of one {N}^3 product)"},
         "cpu_baseline": None,
