@@ -313,14 +313,19 @@ def main():
     outs = [torch.empty((N, N, 128), dtype=torch.float32, device=dev) for _ in range(2)]
     stream = torch.cuda.current_stream()
     h = layer.h
+    OPPOSITE = {T.TRI_MUL_OUTGOING: T.TRI_MUL_INCOMING, T.TRI_MUL_INCOMING: T.TRI_MUL_OUTGOING}
 
+    # The three kernels of the full calls, in their order: the projection
+    # with the opposite direction's pair indexing writes the direction's
+    # operands transposed, which the contraction reads transposed
+    # (tri_mul_contract_transposed; bitwise the same C as the plain order).
     def step(evs):
         for d, direction in enumerate((T.TRI_MUL_OUTGOING, T.TRI_MUL_INCOMING)):
             e = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if evs is not None else None
             if e: e[0].record(stream)
-            T.tri_mul_project(h, z, mask, N, direction, A, B, stream)
+            T.tri_mul_project(h, z, mask, N, OPPOSITE[direction], A, B, stream)
             if e: e[1].record(stream)
-            T.tri_mul_contract(h, A, B, N, C, stream)
+            T.tri_mul_contract_transposed(h, A, B, N, C, stream)
             if e: e[2].record(stream)
             T.tri_mul_epilogue(h, C, z, mask, N, outs[d], stream)
             if e: e[3].record(stream)
@@ -377,16 +382,16 @@ def main():
         ev3 = {}
         for direction, code in (("outgoing", T.TRI_MUL_OUTGOING), ("incoming", T.TRI_MUL_INCOMING)):
             for _ in range(2):   # warm-up
-                T.tri_mul_project(h, z3, None, N3, code, A3, B3, stream)
-                T.tri_mul_contract(h, A3, B3, N3, C3, stream)
+                T.tri_mul_project(h, z3, None, N3, OPPOSITE[code], A3, B3, stream)
+                T.tri_mul_contract_transposed(h, A3, B3, N3, C3, stream)
                 T.tri_mul_epilogue(h, C3, z3, None, N3, o3, stream)
             es = []
             for _ in range(5):
                 e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
                 e[0].record(stream)
-                T.tri_mul_project(h, z3, None, N3, code, A3, B3, stream)
+                T.tri_mul_project(h, z3, None, N3, OPPOSITE[code], A3, B3, stream)
                 e[1].record(stream)
-                T.tri_mul_contract(h, A3, B3, N3, C3, stream)
+                T.tri_mul_contract_transposed(h, A3, B3, N3, C3, stream)
                 e[2].record(stream)
                 T.tri_mul_epilogue(h, C3, z3, None, N3, o3, stream)
                 e[3].record(stream)
@@ -446,8 +451,8 @@ def main():
         lbwd_ms = l0.elapsed_time(l1) / 2
         print(f"[bench] layer backward {lbwd_ms:.3f} ms", file=sys.stderr, flush=True)
         # the same backward from the forward's saved A, B, C (training keeps them)
-        T.tri_mul_project(h, z, mask, N, T.TRI_MUL_OUTGOING, A, B, stream)
-        T.tri_mul_contract(h, A, B, N, C, stream)
+        T.tri_mul_project(h, z, mask, N, T.TRI_MUL_INCOMING, A, B, stream)   # the outgoing operands transposed
+        T.tri_mul_contract_transposed(h, A, B, N, C, stream)
         T.tri_mul_layer_backward_saved(h, "outgoing", z, mask, N, A, B, C, dout, dz, grads, lws, lws_n, stream)
         l0.record(stream)
         for _ in range(2):

@@ -134,7 +134,10 @@ const char* tri_mul_last_error(void);
 /* Bytes of device workspace tri_mul_outgoing / tri_mul_incoming need for N
  * tokens: the two contraction operands (panel layout, see tri_mul_project)
  * and the fp32 contraction result (result layout, see tri_mul_contract), each
- * 256-byte aligned.  *bytes is a HOST pointer. */
+ * 256-byte aligned.  *bytes is a HOST pointer.  With bf16 storage the full
+ * calls keep the operands transposed there -- the panels tri_mul_project
+ * writes for the opposite direction, contracted by
+ * tri_mul_contract_transposed; with fp32 storage the direction's own. */
 int tri_mul_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes);
 
 /* The full update, Eq. 2 (outgoing) / Eq. 3 (incoming).
@@ -323,6 +326,19 @@ int tri_mul_project(tri_mul_handle_t h, const void* z, const uint8_t* mask, int6
 int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_panels,
                      int64_t N, float* c_out, void* stream);
 
+/* tri_mul_contract_transposed: the same C from the operands given
+ * transposed, AT_c = A_c^T and BT_c = B_c^T in the panel layout:
+ * C_c[i][j] = sum_k AT_c[k][i] * BT_c[k][j].  Since the outgoing operands
+ * are the incoming ones transposed and vice versa, tri_mul_project with the
+ * opposite direction writes exactly AT and BT, and
+ *     tri_mul_contract_transposed(project(z, opposite direction))
+ * is bitwise equal to tri_mul_contract(project(z, direction)).  On gfx950
+ * this order is the faster one (the full calls use it with bf16 storage).
+ * bf16 storage only (TRI_MUL_EUNSUPPORTED otherwise); other arguments and
+ * errors as tri_mul_contract. */
+int tri_mul_contract_transposed(tri_mul_handle_t h, const void* at_panels, const void* bt_panels,
+                                int64_t N, float* c_out, void* stream);
+
 /* tri_mul_epilogue: out[i][j] = m_ij * sigmoid(W_g LN_in(z_ij)) * W_o LN_out(C_.[i][j])
  * (C float32 in the result layout of tri_mul_contract, z [N][N][c_z] dtype,
  * out [N][N][c_z] out_dtype). */
@@ -395,12 +411,15 @@ int tri_mul_incoming_backward(tri_mul_handle_t h, const void* z, const uint8_t* 
                               void* dz, const tri_mul_grads_t* grads, void* ws, size_t ws_bytes, void* stream);
 
 /* The same backward from the forward's saved state instead of recomputing
- * it: a_panels, b_panels (panel layout, as tri_mul_project wrote them for
- * this z, mask and direction) and c_result (result layout, as
- * tri_mul_contract wrote it from them) replace the recomputed projections
- * and contraction; the full calls tri_mul_outgoing / tri_mul_incoming leave
- * exactly these in their workspace, at byte offsets 0, P and 2 P with
- * P = tri_mul_panel_size rounded up to a multiple of 256.  Results are
+ * it: a_panels, b_panels -- the direction's operands TRANSPOSED, i.e. the
+ * panels tri_mul_project writes for this z and mask with the OPPOSITE
+ * direction -- and c_result (result layout, the contraction of the
+ * direction, as tri_mul_contract_transposed writes it from those panels, or
+ * tri_mul_contract from the direction's own) replace the recomputed
+ * projections and contraction; the full calls tri_mul_outgoing /
+ * tri_mul_incoming (bf16 storage) leave exactly these in their workspace,
+ * at byte offsets 0, P and 2 P with P = tri_mul_panel_size rounded up to a
+ * multiple of 256.  Results are
  * identical to tri_mul_outgoing_backward / tri_mul_incoming_backward on the
  * same inputs; the saved tensors are only read and must not alias ws.  Same
  * workspace size, alignment and errors (16-byte aligned saved pointers). */

@@ -142,6 +142,28 @@ void free_all(tri_mul_handle_t h) {
     h->allocations.clear();
 }
 
+// K1 and K2 of the full update.  bf16 storage: the projection runs with the
+// opposite direction's pair indexing, which writes the direction's operands
+// transposed (X_c = A_c^T, the panels tri_mul_project writes for the other
+// direction), and the contraction reads both of them transposed -- the same
+// sums in the same order, so C is bitwise the one of the plain order, and
+// about 4% faster on gfx950 (its LDS stages are unswizzled 2 KB pieces read
+// with ds_read_b64_tr_b16).  fp32 storage keeps the plain order (its
+// contraction has no transposed reads).  A and B then hold what the layer
+// backward's saved form takes.
+hipError_t forward_operands_and_contraction(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N,
+                                            int incoming, void* A, void* B, float* C, hipStream_t s) {
+    if (h->dtype != TRI_MUL_BF16) {
+        hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, A, B, s);
+        if (e != hipSuccess) return e;
+        return trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr,
+                                       h->w.cus, s);
+    }
+    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, !incoming, A, B, s);
+    if (e != hipSuccess) return e;
+    return trimul::launch_contract_transposed(1, 1, A, B, C, N, N, N, h->c, h->w.cus, s);
+}
+
 int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, void* out, void* ws,
              size_t ws_bytes, void* stream, int incoming) {
     if (int rc = check_handle(h)) return rc;
@@ -158,10 +180,8 @@ int run_full(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t N, 
     void* B = base + round256(panel);
     float* C = reinterpret_cast<float*>(base + 2 * round256(panel));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, A, B, s);
-    if (e != hipSuccess) return hip_fail(e, "projection kernel launch");
-    e = trimul::launch_contract(h->dtype, 1, A, B, C, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, h->w.cus, s);
-    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    hipError_t e = forward_operands_and_contraction(h, z, mask, N, incoming, A, B, C, s);
+    if (e != hipSuccess) return hip_fail(e, "projection or contraction kernel launch");
     trimul::EpilogueArgs ea{C, 1, 0, 0, z, mask, 0, 0, N, N, out};
     e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
     if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
@@ -268,16 +288,15 @@ int run_backward(tri_mul_handle_t h, const void* z, const uint8_t* mask, int64_t
     const int cus = h->w.cus, G = L.grid_pair, GW = L.grid_w, GW4 = L.grid_w4;
 
     hipError_t e = hipSuccess;
-    if (!saved) {   // recompute the forward's operands and contraction
-        e = trimul::launch_project(h->dtype, h->w, z, mask, N, incoming, const_cast<void*>(A), const_cast<void*>(B), s);
-        if (e == hipSuccess)
-            e = trimul::launch_contract(h->dtype, 1, A, B, const_cast<float*>(C), N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0,
-                                        nullptr, cus, s);
-    }
+    if (!saved)   // recompute the forward's operands (stored transposed) and contraction
+        e = forward_operands_and_contraction(h, z, mask, N, incoming, const_cast<void*>(A), const_cast<void*>(B),
+                                             const_cast<float*>(C), s);
     if (e == hipSuccess) e = trimul::launch_epilogue_backward(h->out_dtype, h->w, C, z, mask, dout, N, dCp, dxg, bb, peb, G, s);
-    // dA = dC B and dB = dC^T A, reading B, dC and A transposed straight from their panels
-    if (e == hipSuccess) e = trimul::launch_contract_transposed(0, 1, dCp, B, dA, N, N, N, h->c, cus, s);
-    if (e == hipSuccess) e = trimul::launch_contract_transposed(1, 1, dCp, A, dB, N, N, N, h->c, cus, s);
+    // A and B hold A^T and B^T: dA = dC B is the plain product of the dC panel
+    // with the B^T panel, dB = dC^T A reads dC transposed and A^T as it is
+    if (e == hipSuccess)
+        e = trimul::launch_contract(h->dtype, 1, dCp, B, dA, N, N, N, 0, 0, N, 0, 0, N * N, h->c, 0, nullptr, cus, s);
+    if (e == hipSuccess) e = trimul::launch_contract_transposed(1, 0, dCp, A, dB, N, N, N, h->c, cus, s);
     if (e == hipSuccess) e = trimul::launch_projection_backward(h->w, z, mask, N, incoming, dA, dB, dxg, dz, bb, ppb, G, s);
     const struct { const bf16_t* u; const bf16_t* v; float* out; } wg[] = {{bb.du, bb.y, g->w_o}, {bb.dgg, bb.xe, g->w_g}};
     for (const auto& q : wg) {
@@ -556,6 +575,20 @@ int tri_mul_contract(tri_mul_handle_t h, const void* a_panels, const void* b_pan
     if (!aligned16(a_panels) || !aligned16(b_panels) || !aligned16(c_out)) return fail(TRI_MUL_EINVAL, "panels and output must be 16-byte aligned");
     hipError_t e = trimul::launch_contract(h->dtype, 1, a_panels, b_panels, c_out, N, N, N, 0, 0, N, 0, 0, N * N, h->c,
                                            0, nullptr, h->w.cus, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    return ok();
+}
+
+int tri_mul_contract_transposed(tri_mul_handle_t h, const void* at_panels, const void* bt_panels, int64_t N,
+                                float* c_out, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (int rc = check_n(N)) return rc;
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "transposed operands exist for the bf16 storage path only");
+    if (!at_panels || !bt_panels || !c_out) return fail(TRI_MUL_EINVAL, "null panel or output pointer");
+    if (!aligned16(at_panels) || !aligned16(bt_panels) || !aligned16(c_out))
+        return fail(TRI_MUL_EINVAL, "panels and output must be 16-byte aligned");
+    hipError_t e = trimul::launch_contract_transposed(1, 1, at_panels, bt_panels, c_out, N, N, N, h->c, h->w.cus,
+                                                      static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
     return ok();
 }

@@ -614,7 +614,7 @@ hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void*
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
     const int grid = total < cus ? total : cus;
-    if (!tb || !cblocked_fits(N, batch)) return hipErrorInvalidValue;
+    if ((!ta && !tb) || !cblocked_fits(N, batch)) return hipErrorInvalidValue;
     const int pace = pace_launch(grid, total, s);
 #define K2_TR(TA_, TB_)                                                                                             \
     hipLaunchKernelGGL((k2_contract_ws<true, false, true, TA_, TB_>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A, \
@@ -622,7 +622,7 @@ hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void*
                        (int64_t)0, tm, tn, total, 0, (const uint8_t*)nullptr, pace)
     if (!ta && tb) K2_TR(false, true);
     else if (ta && tb) K2_TR(true, true);
-    else return hipErrorInvalidValue;
+    else K2_TR(true, false);
 #undef K2_TR
     return hipGetLastError();
 }

@@ -94,6 +94,7 @@ SIGNATURES = {
                                                          _vp, _i32, _vp]),
     "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
+    "tri_mul_contract_transposed": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_epilogue": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_contract_backward_workspace_size": (ctypes.c_int, [_vp, _i64, ctypes.POINTER(ctypes.c_size_t)]),
     "tri_mul_contract_backward": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
@@ -274,6 +275,10 @@ def tri_mul_contract(h, a_panels, b_panels, N, c_out, stream=None):
     _check(lib().tri_mul_contract(h, _ptr(a_panels), _ptr(b_panels), N, _ptr(c_out), _stream(stream)))
 
 
+def tri_mul_contract_transposed(h, at_panels, bt_panels, N, c_out, stream=None):
+    _check(lib().tri_mul_contract_transposed(h, _ptr(at_panels), _ptr(bt_panels), N, _ptr(c_out), _stream(stream)))
+
+
 def tri_mul_epilogue(h, c_in, z, mask, N, out, stream=None):
     _check(lib().tri_mul_epilogue(h, _ptr(c_in), _ptr(z), _ptr(mask), N, _ptr(out), _stream(stream)))
 
@@ -384,6 +389,13 @@ class TriMul:
         tri_mul_contract(self.h, A, B, N, C, stream)
         return C
 
+    def contract_transposed(self, AT, BT, N, stream=None):
+        """The same C as contract(A, B, N) from the operands transposed,
+        i.e. from project(z, mask, <the opposite direction>)."""
+        C = torch.empty(N * (-(-N // 32) * 32) * 128, dtype=torch.float32, device=self.device)
+        tri_mul_contract_transposed(self.h, AT, BT, N, C, stream)
+        return C
+
     def epilogue(self, C, z, mask=None, out=None, stream=None):
         """C in the result layout (contract / dense_to_result)."""
         N = z.shape[0]
@@ -405,8 +417,10 @@ class TriMul:
     def backward(self, z, dout, mask=None, direction="outgoing", stream=None, saved=None):
         """Gradients of sum(out * dout) for the update of z: returns (dz,
         grads) with grads a dict of float32 tensors shaped like the weights.
-        saved = (A, B, C) from project / contract of the same z, mask and
-        direction skips the recomputation of the forward."""
+        saved = (AT, BT, C) skips the recomputation of the forward: AT, BT
+        from project(z, mask, <the opposite direction>) -- the direction's
+        operands transposed, as the full calls leave them in their workspace
+        -- and C the direction's contraction (contract_transposed(AT, BT))."""
         N = z.shape[0]
         cz = 128
         if tuple(z.shape) != (N, N, cz) or tuple(dout.shape) != (N, N, cz):

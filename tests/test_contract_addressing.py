@@ -55,12 +55,16 @@ def test_full_update_blocked_operands(n):
 
 
 @pytest.mark.parametrize("n", SIZES)
-@pytest.mark.parametrize("ta", [0, 1])
-def test_backward_products_transposed_operands(n, ta):
-    # dA = dC B (B read transposed from its panel), dB = dC^T A (both transposed)
+@pytest.mark.parametrize("ta,tb", [(0, 1), (1, 1), (1, 0)])
+def test_transposed_operands(n, ta, tb):
+    # (0, 1): dA = dC B with B read transposed from its panel; (1, 1): the
+    # forward from the opposite direction's panels, and dB = dC^T A from the
+    # direction's own; (1, 0): dB = dC^T A with A^T given as it is
     a_mode = TR if ta else BLK
+    b_mode = TR if tb else BLK
     a_bytes = transposed_bytes(n, n) if ta else blocked_bytes(n, n)
-    r = T.check_contract_loads(a_mode, TR, n, n, n, a_bytes=a_bytes, b_bytes=transposed_bytes(n, n),
+    b_bytes = transposed_bytes(n, n) if tb else blocked_bytes(n, n)
+    r = T.check_contract_loads(a_mode, b_mode, n, n, n, a_bytes=a_bytes, b_bytes=b_bytes,
                                grid=min(256, tiles(n, n)), all_channels=n <= 300)
     assert_clean(r, tiles(n, n))
 

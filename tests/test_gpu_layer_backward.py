@@ -134,8 +134,9 @@ def test_layer_backward_n4096_runs_deterministic():
 @pytest.mark.parametrize("direction", ["outgoing", "incoming"])
 def test_layer_backward_from_saved_forward_is_identical(direction):
     """The saved-state entry points skip the recomputation of the forward:
-    from the stage calls' A, B, C, and from the regions the full call leaves
-    in its workspace (offsets 0, P, 2 P), the results equal the recomputing
+    from the stage calls' operands transposed (the projection with the
+    opposite direction) and C, and from the regions the full call leaves in
+    its workspace (offsets 0, P, 2 P), the results equal the recomputing
     backward bit for bit."""
     N = 300
     say(f"layer backward from saved forward {direction} N={N}")
@@ -146,8 +147,9 @@ def test_layer_backward_from_saved_forward_is_identical(direction):
     g = torch.Generator(device="cuda").manual_seed(9)
     dout = torch.randn((N, N, 128), generator=g, device="cuda")
     dz0, g0 = layer.backward(z, dout, mask, direction)
-    A, B = layer.project(z, mask, direction)
-    C = layer.contract(A, B, N)
+    other = "incoming" if direction == "outgoing" else "outgoing"
+    A, B = layer.project(z, mask, other)
+    C = layer.contract_transposed(A, B, N)
     dz1, g1 = layer.backward(z, dout, mask, direction, saved=(A, B, C))
     layer(z, mask, direction)                                   # the full call, workspace kept by the wrapper
     ws, _ = layer.workspace(N)

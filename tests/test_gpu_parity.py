@@ -33,6 +33,63 @@ def test_contract_exact_on_integers(dtype, N):
     np.testing.assert_array_equal(host(T.result_to_dense(C, N)).transpose(1, 2, 0), ref)
 
 
+@pytest.mark.parametrize("N", [64, 300, 520])
+def test_contract_transposed_exact_on_integers(N):
+    """tri_mul_contract_transposed takes the operands transposed (A_c^T,
+    B_c^T in the panel layout): on small integers it must give the fp64
+    contraction of A and B bit for bit."""
+    say(f"contract transposed exact N={N}")
+    layer, _ = make_layer("bf16")
+    g = torch.Generator().manual_seed(N + 1)
+    A = torch.randint(-4, 5, (128, N, N), generator=g).to(torch.bfloat16)
+    B = torch.randint(-4, 5, (128, N, N), generator=g).to(torch.bfloat16)
+    AT = T.dense_to_panel(A.transpose(1, 2).contiguous()).cuda()
+    BT = T.dense_to_panel(B.transpose(1, 2).contiguous()).cuda()
+    C = layer.contract_transposed(AT, BT, N)
+    torch.cuda.synchronize()
+    ref = oracle.block_contract([host(A)], [host(B)], [np.ones(N)])    # [i][j][c]
+    np.testing.assert_array_equal(host(T.result_to_dense(C, N)).transpose(1, 2, 0), ref)
+
+
+@pytest.mark.parametrize("N", [65, 300, 1000])
+@pytest.mark.parametrize("direction", DIRS)
+def test_contract_transposed_from_opposite_projection_is_bitwise_plain(N, direction):
+    """The projection with the opposite direction writes the direction's
+    operands transposed; contracting those with tri_mul_contract_transposed
+    (the full calls' order) equals tri_mul_contract of the direction's own
+    panels bit for bit, and the full call's output equals the stage calls'."""
+    say(f"contract transposed == plain N={N} {direction}")
+    layer, _ = make_layer("bf16", affine=True, seed=5)
+    z = synth.pair_tensor(N, dtype="bf16", seed=5, device="cuda")
+    mask = synth.random_mask(N, 0.9, sub=2).cuda()
+    other = "incoming" if direction == "outgoing" else "outgoing"
+    A, B = layer.project(z, mask, direction)
+    AT, BT = layer.project(z, mask, other)
+    C = layer.contract(A, B, N)
+    CT = layer.contract_transposed(AT, BT, N)
+    out_stage = layer.epilogue(CT, z, mask)
+    out_full = layer(z, mask, direction)
+    torch.cuda.synchronize()
+    assert torch.equal(T.result_to_dense(C, N), T.result_to_dense(CT, N))
+    assert torch.equal(T.panel_to_dense(AT, N), T.panel_to_dense(A, N).transpose(1, 2))
+    assert torch.equal(out_stage, out_full)
+
+
+def test_contract_transposed_errors():
+    layer, _ = make_layer("bf16")
+    N = 64
+    buf = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    L = T.lib()
+    s = torch.cuda.current_stream().cuda_stream
+    assert L.tri_mul_contract_transposed(layer.h, None, buf.data_ptr(), N, buf.data_ptr(), s) == T.TRI_MUL_EINVAL
+    assert L.tri_mul_contract_transposed(layer.h, buf.data_ptr() + 4, buf.data_ptr(), N, buf.data_ptr(), s) == T.TRI_MUL_EINVAL
+    assert L.tri_mul_contract_transposed(layer.h, buf.data_ptr(), buf.data_ptr(), 0, buf.data_ptr(), s) == T.TRI_MUL_EINVAL
+    f32, _ = make_layer("f32")
+    assert L.tri_mul_contract_transposed(f32.h, buf.data_ptr(), buf.data_ptr(), N, buf.data_ptr(), s) == T.TRI_MUL_EUNSUPPORTED
+    assert "bf16" in T.last_error()
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("dtype,use_ws", [("bf16", False), ("bf16", True), ("f32", False), ("f32", True)])
 def test_block_accumulate_kmask_exact(dtype, use_ws):
     """Two k-panels with a token mask over k, ragged tile (300 x 200) and
