@@ -564,13 +564,18 @@ def main():
         # contributes to the ring) and contracts the eight panel pairs as they
         # arrive, with no repack; the other seven pairs alternate between two
         # projected tiles (made before the timed calls, as a ring delivers them)
+        # The same ring in the transposed operand order (every device projects
+        # its tile with the opposite direction's pair indexing, the steps read
+        # both panels transposed: bitwise the same sums, the faster order) is
+        # the timed one; the plain order is reported beside it.
         n_bp = layer.block_panel_size(bb, bb) // 2
         own = [torch.empty(n_bp, dtype=torch.bfloat16, device=dev) for _ in range(2)]
-        arrived = []
+        arrived, arrived_t = [], []
         for p in range(2):
             zt = synth.pair_tensor(0, dtype="bf16", device=dev, name="z_tile", seed=synth.SEED + 1 + p,
                                    shape=(bb, bb, 128))
             arrived.append(layer.block_project(zt, bmask, bn, brow, p * bb, "outgoing"))
+            arrived_t.append(layer.block_project(zt, bmask, bn, brow, p * bb, "incoming"))
             del zt
 
         def ring_tile_blocked():
@@ -579,6 +584,13 @@ def main():
             for p in range(bg):
                 a_, b_ = own if p == bg - 1 else arrived[p & 1]
                 layer.block_accumulate_blocked(bviews[p], a_, b_, pacc, bmask, bz, bout, stream=stream)
+
+        def ring_tile_transposed():
+            T.tri_mul_block_project(layer.h, bz, bb, bmask, bn, brow, brow, bb, bb, T.TRI_MUL_INCOMING,
+                                    own[0], own[1], stream)
+            for p in range(bg):
+                a_, b_ = own if p == bg - 1 else arrived_t[p & 1]
+                layer.block_accumulate_transposed(bviews[p], a_, b_, pacc, bmask, bz, bout, stream=stream)
 
         def time_ring(fn):
             fn()
@@ -590,12 +602,14 @@ def main():
             torch.cuda.synchronize()
             return t0e.elapsed_time(t1e) / 2
 
-        tile_ms = time_ring(ring_tile_blocked)
+        tile_ms = time_ring(ring_tile_transposed)
+        tile_plain_ms = time_ring(ring_tile_blocked)
         tile_pk_ms = time_ring(ring_tile)
         tile_ws_ms = time_ring(ring_tile_ws)
-        del bpa, bpb, bz, bacc, bout, tws, tws2, pacc, own, arrived
+        del bpa, bpb, bz, bacc, bout, tws, tws2, pacc, own, arrived, arrived_t
         torch.cuda.empty_cache()
-        print(f"[bench] ring tile {tile_ms:.3f} ms (row-major panels: pipelined repack {tile_pk_ms:.3f} ms, "
+        print(f"[bench] ring tile {tile_ms:.3f} ms (plain operand order {tile_plain_ms:.3f} ms; "
+              f"row-major panels: pipelined repack {tile_pk_ms:.3f} ms, "
               f"one-stream repacking entry point {tile_ws_ms:.3f} ms)", file=sys.stderr, flush=True)
 
     fl = perf.flops(N)
@@ -676,14 +690,18 @@ def main():
         "ring_tile": None if tile_ms is None else {"ms": round(tile_ms, 4),
                       "TFLOP_per_s": round(tile_flops / (tile_ms * 1e-3) / 1e12, 2),
                       "roofline": mfma_roof(tile_flops, tile_ms),
+                      "ms_blocked_plain_order": round(tile_plain_ms, 4),
                       "ms_rowmajor_pipelined": round(tile_pk_ms, 4),
                       "ms_one_stream_ws": round(tile_ws_ms, 4),
                       "what": "one device's share of a layer on an 8x8 grid at N=30000, tile (7,7): the projection "
-                              "of its 3750x3750 z tile into blocked a, b panels (tri_mul_block_project), 8 ring "
-                              "steps on blocked panels (tri_mul_block_accumulate_blocked: 3750x3750 outputs, "
+                              "of its 3750x3750 z tile into blocked a, b panels written transposed "
+                              "(tri_mul_block_project with the opposite direction), 8 ring steps reading them "
+                              "transposed (tri_mul_block_accumulate_transposed: 3750x3750 outputs, "
                               "3750-token k-panels, 128 channels, 108.0 TFLOP contraction, packed fp32 "
                               "accumulator) and the tile epilogue on the last step, fp32 output; TFLOP/s counts "
-                              "the contraction only.  With row-major panels instead (no projection): "
+                              "the contraction only.  ms_blocked_plain_order: the same ring on panels in the "
+                              "direction's own order (tri_mul_block_accumulate_blocked).  With row-major panels "
+                              "instead (no projection): "
                               "ms_rowmajor_pipelined = tri_mul_block_repack of panel p + 1 on a second stream while "
                               "panel p is contracted on 224 CUs (tri_mul_block_accumulate_packed), "
                               "ms_one_stream_ws = tri_mul_block_accumulate_ws on one stream; not part of "

@@ -288,7 +288,15 @@ int tri_mul_block_accumulate_packed(tri_mul_handle_t h, const tri_mul_block_view
  *   runs the epilogue into out_tile.  reserve_cus as for
  *   tri_mul_block_accumulate_packed.  Given the panels that
  *   tri_mul_block_repack writes for the same values, the results are
- *   identical to tri_mul_block_accumulate_packed's. */
+ *   identical to tri_mul_block_accumulate_packed's.
+ * tri_mul_block_accumulate_transposed: the same ring step from the two
+ *   panels transposed -- at_panel holds A^T (m = klen rows, rows
+ *   contraction indices), bt_panel B^T (m = klen, cols), i.e. what
+ *   tri_mul_block_project writes from the same z tiles with the OPPOSITE
+ *   direction; other arguments, accumulator, epilogue and errors as
+ *   tri_mul_block_accumulate_blocked, and the sums are bitwise the same.
+ *   On gfx950 this operand order is the faster one (as for the full
+ *   update, see tri_mul_contract_transposed). */
 int tri_mul_block_panel_size(tri_mul_handle_t h, int64_t rows, int64_t klen, size_t* bytes);
 int tri_mul_block_project(tri_mul_handle_t h, const void* z_tile, int64_t ld_z, const uint8_t* mask, int64_t n_total,
                           int64_t row0, int64_t col0, int64_t rows, int64_t cols, int32_t direction, void* a_panel,
@@ -296,6 +304,9 @@ int tri_mul_block_project(tri_mul_handle_t h, const void* z_tile, int64_t ld_z, 
 int tri_mul_block_accumulate_blocked(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* a_panel,
                                      const void* b_panel, float* acc, const uint8_t* mask, const void* z_tile,
                                      void* out_tile, int32_t reserve_cus, void* stream);
+int tri_mul_block_accumulate_transposed(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* at_panel,
+                                        const void* bt_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                                        void* out_tile, int32_t reserve_cus, void* stream);
 
 /* The three stages of tri_mul_outgoing / tri_mul_incoming, exposed so that
  * callers can time or check them one by one.

@@ -907,6 +907,30 @@ int tri_mul_block_accumulate_blocked(tri_mul_handle_t h, const tri_mul_block_vie
     return ok();
 }
 
+int tri_mul_block_accumulate_transposed(tri_mul_handle_t h, const tri_mul_block_view_t* v, const void* at_panel,
+                                        const void* bt_panel, float* acc, const uint8_t* mask, const void* z_tile,
+                                        void* out_tile, int32_t reserve_cus, void* stream) {
+    if (int rc = check_handle(h)) return rc;
+    if (h->dtype != TRI_MUL_BF16) return fail(TRI_MUL_EUNSUPPORTED, "blocked panels exist for the bf16 storage path only");
+    if (!v) return fail(TRI_MUL_EINVAL, "null view");
+    tri_mul_block_view_t w = *v;   // the strides of row-major panels do not apply
+    w.ld_a = w.ld_b = (v->klen + 7) / 8 * 8;
+    if (int rc = check_block(h, &w, at_panel, bt_panel, acc, z_tile, out_tile)) return rc;
+    if (reserve_cus < 0 || reserve_cus > h->w.cus - 8)
+        return fail(TRI_MUL_EINVAL, "reserve_cus = %d outside [0, %d]", reserve_cus, h->w.cus - 8);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int cus = (h->w.cus - reserve_cus) & ~7;   // whole XCD groups
+    hipError_t e = trimul::launch_contract_transposed(1, 1, at_panel, bt_panel, acc, v->rows, v->cols, v->klen, h->c,
+                                                      cus, s, v->k_index > 0);
+    if (e != hipSuccess) return hip_fail(e, "contraction kernel launch");
+    if (v->k_index == v->k_count - 1) {
+        trimul::EpilogueArgs ea{acc, 1, 0, 0, z_tile, mask, v->row0, v->col0, v->rows, v->cols, out_tile};
+        e = trimul::launch_epilogue(h->dtype, h->out_dtype, h->w, ea, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue kernel launch");
+    }
+    return ok();
+}
+
 int tri_mul_backward_workspace_size(tri_mul_handle_t h, int64_t N, size_t* bytes) {
     if (int rc = check_handle(h)) return rc;
     if (int rc = check_n(N)) return rc;

@@ -609,7 +609,7 @@ hipError_t launch_contract_blocked_packed(const void* A, const void* B, float* C
 }
 
 hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void* B, float* C, int64_t M, int64_t N,
-                                      int64_t K, int batch, int cus, hipStream_t s) {
+                                      int64_t K, int batch, int cus, hipStream_t s, int accumulate) {
     constexpr int BM = 256;
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     const int total = tm * tn * batch;
@@ -619,7 +619,7 @@ hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void*
 #define K2_TR(TA_, TB_)                                                                                             \
     hipLaunchKernelGGL((k2_contract_ws<true, false, true, TA_, TB_>), dim3(grid), dim3(768), 0, s, (const bf16_t*)A, \
                        (const bf16_t*)B, C, (int)M, (int)N, (int)K, 0, 0, (int64_t)0, (int64_t)0, (int64_t)0,     \
-                       (int64_t)0, tm, tn, total, 0, (const uint8_t*)nullptr, pace)
+                       (int64_t)0, tm, tn, total, accumulate, (const uint8_t*)nullptr, pace)
     if (!ta && tb) K2_TR(false, true);
     else if (ta && tb) K2_TR(true, true);
     else K2_TR(true, false);

@@ -67,9 +67,9 @@ hipError_t launch_contract_blocked_packed(const void* A, const void* B, float* C
 // bf16 contraction of blocked operands, either given as its transpose in the
 // panel layout (ta: A[c][i][k] = X[c][k][i], X with K rows and M columns; tb
 // likewise with N columns), into the pair-blocked fp32 result layout.
-// Supported: (ta, tb) = (0, 1), (1, 1) and (1, 0).
+// Supported: (ta, tb) = (0, 1), (1, 1) and (1, 0); accumulate adds into C.
 hipError_t launch_contract_transposed(int ta, int tb, const void* A, const void* B, float* C, int64_t M, int64_t N,
-                                      int64_t K, int batch, int cus, hipStream_t s);
+                                      int64_t K, int batch, int cus, hipStream_t s, int accumulate = 0);
 
 // Host-side check of the contraction kernel's loads (contract.hip): counts of
 // tiles, loads and needed elements visited, and of violations.

@@ -92,6 +92,8 @@ SIGNATURES = {
     "tri_mul_block_project": (ctypes.c_int, [_vp, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_block_accumulate_blocked": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp, _vp,
                                                          _vp, _i32, _vp]),
+    "tri_mul_block_accumulate_transposed": (ctypes.c_int, [_vp, ctypes.POINTER(BlockView), _vp, _vp, _vp, _vp,
+                                                            _vp, _vp, _i32, _vp]),
     "tri_mul_project": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "tri_mul_contract": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
     "tri_mul_contract_transposed": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp, _vp]),
@@ -264,6 +266,13 @@ def tri_mul_block_accumulate_blocked(h, view, a_panel, b_panel, acc, mask, z_til
     _check(lib().tri_mul_block_accumulate_blocked(h, ctypes.byref(view), _ptr(a_panel), _ptr(b_panel), _ptr(acc),
                                                   _ptr(mask), _ptr(z_tile), _ptr(out_tile), reserve_cus,
                                                   _stream(stream)))
+
+
+def tri_mul_block_accumulate_transposed(h, view, at_panel, bt_panel, acc, mask, z_tile, out_tile, reserve_cus=0,
+                                        stream=None):
+    _check(lib().tri_mul_block_accumulate_transposed(h, ctypes.byref(view), _ptr(at_panel), _ptr(bt_panel),
+                                                     _ptr(acc), _ptr(mask), _ptr(z_tile), _ptr(out_tile),
+                                                     reserve_cus, _stream(stream)))
 
 
 def tri_mul_project(h, z, mask, N, direction, a_panels, b_panels, stream=None):
@@ -484,6 +493,13 @@ class TriMul:
                                  reserve_cus=0, stream=None):
         tri_mul_block_accumulate_blocked(self.h, view, a_panel, b_panel, acc, mask, z_tile, out_tile, reserve_cus,
                                          stream)
+
+    def block_accumulate_transposed(self, view, at_panel, bt_panel, acc, mask=None, z_tile=None, out_tile=None,
+                                    reserve_cus=0, stream=None):
+        """The ring step from the panels block_project writes with the
+        opposite direction (the operands transposed)."""
+        tri_mul_block_accumulate_transposed(self.h, view, at_panel, bt_panel, acc, mask, z_tile, out_tile,
+                                            reserve_cus, stream)
 
 
 # ------------------------------------------------------ panel layout views

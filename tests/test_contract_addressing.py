@@ -93,6 +93,17 @@ def test_block_call_repacked_panels(view):
     assert_clean(r, tiles(rows, cols))
 
 
+@pytest.mark.parametrize("view", VIEWS)
+def test_block_call_transposed_panels(view):
+    # the ring step from the panels projected with the opposite direction:
+    # A^T with klen rows and `rows` columns, B^T with klen rows and `cols`
+    rows, cols, klen, _ = view
+    r = T.check_contract_loads(TR, TR, rows, cols, klen, a_bytes=transposed_bytes(rows, klen),
+                               b_bytes=transposed_bytes(cols, klen), grid=min(256, tiles(rows, cols)),
+                               all_channels=rows * cols < 1e5)
+    assert_clean(r, tiles(rows, cols))
+
+
 @pytest.mark.parametrize("shape", [(1024, 1024, 4096), (100, 257, 37), (3, 5, 1)])
 def test_outer_product_mean_launches(shape):
     # sums: rows (token, c) = ntok * 32, K = sequences; counts: rows = tokens

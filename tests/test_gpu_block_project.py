@@ -30,6 +30,56 @@ def ring_blocked(layer, views, aps, bps, mask, z_tile, out, pacc, reserve_cus=0)
                                        reserve_cus=reserve_cus if v.k_index + 1 < v.k_count else 0)
 
 
+def ring_transposed(layer, views, atps, btps, mask, z_tile, out, pacc, reserve_cus=0):
+    for v, a, b in zip(views, atps, btps):
+        layer.block_accumulate_transposed(v, a, b, pacc, mask, z_tile, out,
+                                          reserve_cus=reserve_cus if v.k_index + 1 < v.k_count else 0)
+
+
+@pytest.mark.parametrize("direction", DIRS)
+@pytest.mark.parametrize("N,cuts", [(1000, (0, 100, 356, 700, 1000)), (77, (0, 33, 77)), (1024, (0, 512, 1024))])
+def test_transposed_ring_is_bitwise_the_blocked_ring(direction, N, cuts):
+    """Every device projecting its own z tile with the opposite direction
+    writes the transposed panels; the ring steps on those
+    (tri_mul_block_accumulate_transposed) give the blocked ring's
+    accumulator and output bit for bit, for tiles of every shape."""
+    say(f"transposed ring: N={N} cuts={cuts} {direction}")
+    layer, _ = make_layer("bf16")
+    z = synth.pair_tensor(N, dtype="bf16", device="cuda")
+    mask = synth.random_mask(N, 0.9, sub=len(cuts)).cuda()
+    bl = blocks(cuts)
+    g = len(bl)
+    inc = direction == "incoming"
+    other = "outgoing" if inc else "incoming"
+    proj, projt = {}, {}
+    for x, (r0, nr) in enumerate(bl):
+        for y, (c0, nc) in enumerate(bl):
+            zt = z[r0:r0 + nr, c0:c0 + nc].contiguous()
+            proj[(x, y)] = layer.block_project(zt, mask, N, r0, c0, direction)
+            projt[(x, y)] = layer.block_project(zt, mask, N, r0, c0, other)
+    for p, (r0, nr) in enumerate(bl):
+        for q, (c0, nc) in enumerate(bl):
+            z_tile = z[r0:r0 + nr, c0:c0 + nc].contiguous()
+            views, aps, bps, atps, btps = [], [], [], [], []
+            for r, (k0, nk) in enumerate(bl):
+                ld = (nk + 7) // 8 * 8
+                views.append(T.BlockView(N, r0, c0, nr, nc, k0, nk, ld, ld, r, g))
+                ka, kb = ((r, p), (r, q)) if inc else ((p, r), (q, r))
+                aps.append(proj[ka][0]), bps.append(proj[kb][1])
+                atps.append(projt[ka][0]), btps.append(projt[kb][1])
+            nacc = layer.block_accumulator_size(views[0]) // 4
+            o1 = torch.full((nr, nc, 128), float("nan"), device="cuda")
+            o2 = torch.full((nr, nc, 128), float("nan"), device="cuda")
+            p1 = torch.full((nacc,), float("nan"), device="cuda")
+            p2 = torch.full((nacc,), float("nan"), device="cuda")
+            ring_blocked(layer, views, aps, bps, mask, z_tile, o1, p1)
+            ring_transposed(layer, views, atps, btps, mask, z_tile, o2, p2, reserve_cus=16)
+            torch.cuda.synchronize()
+            assert torch.equal(T.result_to_dense(p1, nr, cols=nc), T.result_to_dense(p2, nr, cols=nc)), (p, q)
+            assert torch.equal(o1, o2), (p, q)
+            assert torch.isfinite(o2).all()
+
+
 @pytest.mark.parametrize("direction", DIRS)
 @pytest.mark.parametrize("N,cuts", [(1000, (0, 600, 1000)), (1000, (0, 100, 356, 700, 1000)),
                                     (1024, (0, 512, 1024)), (77, (0, 33, 77))])
