@@ -7,7 +7,8 @@
  *   incoming:  C[i][j][c] = sum_k a[k][i][c] * b[k][j][c]
  *
  * where a and b are gated projections of the pair representation z
- * (Section 3.3: "projections" of z with "element-wise gating").  For every
+ * (Section 3.3 names the projections and their element-wise gate without
+ * spelling out the layer; the layer below is the usual one).  For every
  * pair (i, j), with pair mask m_ij = m_i * m_j:
  *
  *   x_ij   = LN_in(z_ij)                              over c_z channels

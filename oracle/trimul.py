@@ -10,9 +10,9 @@ What it computes (Fold-CP, Section 3.3, Eq. 2 and Eq. 3):
     incoming:  C[n, m, c] = sum_k a[k, n, c] * b[k, m, c]
 
 where a and b are gated projections of the pair representation
-z in R^{N x N x c_z} (Section 3.3 says only "projections" with "element-wise
-gating"; the concrete layer is the usual AlphaFold-family triangle update that
-the paper's Boltz models use, written out as mathematics below).  For a pair
+z in R^{N x N x c_z} (Section 3.3 names only projections of z and an
+element-wise gate; the concrete layer is the usual AlphaFold-family triangle
+update that the paper's Boltz models use, written out as mathematics below).  For a pair
 (i, j) with pair mask m_ij = m_i * m_j:
 
     x_ij   = LN_in(z_ij)                               (over c_z, biased var)
