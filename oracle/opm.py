@@ -14,8 +14,8 @@ c * D + d) and linearly projected to c_z channels:
     o_ijcd = (1 / n_ij) sum_s m_si m_sj a_sic b_sjd  (o_ij = 0 where n_ij = 0)
     out_ij = W_o vec(o_ij) + b_o                     (W_o: [c_z][D * D], b_o: [c_z])
 
-Readings (the paper writes the mean as 1/|S| and says a single all-reduce
-finalises "the mask count"): the count is taken per pair, over the sequences
+Readings (the paper writes the mean as 1/|S| and has a single all-reduce
+finish a count of the mask): the count is taken per pair, over the sequences
 in which both tokens are present (m_si = 1, uint8 MSA mask [S][N]); with every
 token present it is |S|, the paper's normalisation.  The projection is a
 linear map with bias, applied after the mean.  a and b enter as given; the
