@@ -73,7 +73,9 @@ int opm_destroy(opm_handle_t h);
 int opm_accumulator_size(opm_handle_t h, int64_t rows, int64_t cols, size_t* bytes);
 
 /* Bytes of the per-call workspace of opm_block_accumulate (the step's
- * operands in the contraction's blocked layout). */
+ * operands in the contraction's blocked layout: those of the sums
+ * transposed, slen rows of tokens * 32 columns each, those of the pair
+ * counts plain). */
 int opm_workspace_size(opm_handle_t h, int64_t rows, int64_t cols, int64_t slen, size_t* bytes);
 
 /* One step (see opm_block_view_t).  a, b: [s_total][n_total][d] bf16, the

@@ -1064,7 +1064,8 @@ int opm_workspace_size(opm_handle_t h, int64_t rows, int64_t cols, int64_t slen,
     if (rows < 1 || cols < 1 || rows > kOpmMaxTile || cols > kOpmMaxTile)
         return fail(TRI_MUL_EINVAL, "tile %lld x %lld outside [1, %lld]^2", (long long)rows, (long long)cols, (long long)kOpmMaxTile);
     if (slen < 1 || slen > kOpmMaxSeq) return fail(TRI_MUL_EINVAL, "slen = %lld outside [1, %lld]", (long long)slen, (long long)kOpmMaxSeq);
-    *bytes = opm_panel_bytes(rows * 32, slen) + opm_panel_bytes(cols * 32, slen) + opm_panel_bytes(rows, slen) +
+    // the sums' operands transposed (slen rows, tokens * 32 columns), the counts' plain
+    *bytes = opm_panel_bytes(slen, rows * 32) + opm_panel_bytes(slen, cols * 32) + opm_panel_bytes(rows, slen) +
              opm_panel_bytes(cols, slen);
     return ok();
 }
@@ -1088,9 +1089,9 @@ int opm_block_accumulate(opm_handle_t h, const opm_block_view_t* v, const void* 
     if (last && (!out_tile || !aligned16(out_tile))) return fail(TRI_MUL_EINVAL, "the last step needs a 16-byte aligned out_tile");
     char* p = static_cast<char*>(ws);
     void* PA = p;
-    p += opm_panel_bytes(v->rows * 32, v->slen);
+    p += opm_panel_bytes(v->slen, v->rows * 32);
     void* PB = p;
-    p += opm_panel_bytes(v->cols * 32, v->slen);
+    p += opm_panel_bytes(v->slen, v->cols * 32);
     void* MA = p;
     p += opm_panel_bytes(v->rows, v->slen);
     void* MB = p;
@@ -1101,8 +1102,8 @@ int opm_block_accumulate(opm_handle_t h, const opm_block_view_t* v, const void* 
     if (e == hipSuccess) e = trimul::launch_opm_pack(b, mask, v->n_total, v->col0, v->cols, v->s0, v->slen, PB, MB, s);
     if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
     const int accumulate = v->k_index > 0;
-    e = trimul::launch_contract(TRI_MUL_BF16, 1, PA, PB, sums, v->rows * 32, v->cols * 32, v->slen, 0, 0, 0, 0, 0, 0,
-                                1, accumulate, nullptr, h->cus, s);
+    e = trimul::launch_contract_transposed(1, 1, PA, PB, sums, v->rows * 32, v->cols * 32, v->slen, 1, h->cus, s,
+                                           accumulate);
     if (e == hipSuccess)
         e = trimul::launch_contract(TRI_MUL_BF16, 1, MA, MB, cnt, v->rows, v->cols, v->slen, 0, 0, 0, 0, 0, 0, 1,
                                     accumulate, nullptr, h->cus, s);

@@ -155,8 +155,9 @@ hipError_t launch_sum_parts(const float* in, int parts, int64_t stride, int n, f
 
 // Outer product mean (opm.hip).  Pack: tokens [tok0, tok0 + ntok) and
 // sequences [s0, s0 + slen) of a [S][n_total][32] bf16 tensor, masked, into
-// the blocked panel of ntok * 32 rows and K = slen (row token * 32 + c), and
-// the 0/1 mask into the blocked panel of ntok rows.  Epilogue: out[rows][cols][128]
+// the transposed operand of the sums -- the blocked panel of slen rows and
+// ntok * 32 columns, X[s][token * 32 + c] -- and the 0/1 mask into the
+// (plain) blocked panel of ntok rows and K = slen.  Epilogue: out[rows][cols][128]
 // from the sums O (result layout, [rows * 32][cols * 32]) and the counts
 // (result layout, [rows][32 * ceil(cols / 32)]).
 hipError_t launch_opm_pack(const void* a, const uint8_t* mask, int64_t n_total, int64_t tok0, int64_t ntok,

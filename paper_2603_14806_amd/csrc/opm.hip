@@ -4,7 +4,8 @@
 //
 //     O[(i, c)][(j, d)] = sum_s m_si m_sj a_sic b_sjd,
 //
-// is one NT product with M = rows * D, N = cols * D, K = slen, and the pair
+// is one NT product with M = rows * D, N = cols * D, K = slen (both operands
+// given transposed, which is the input's own order), and the pair
 // counts n_ij = sum_s m_si m_sj another with M = rows, N = cols (0/1
 // operands: exact in fp32 up to 2^24); both run on the contraction kernel
 // (k2_contract_ws), accumulating over the steps of a tile.
@@ -19,27 +20,27 @@ constexpr int kOz = 128;       // output channels
 
 // ---------------------------------------------------------------- pack
 //
-// One work-group per (8 tokens, 32 sequences): reads a[s][tok][0:32] for the
-// 8 tokens of 32 sequences (512 contiguous bytes per sequence), multiplies
-// by the mask, and writes the 256 x 32 block of the blocked panel
-// (row R = token * 32 + c, k = s) plus the 8 x 32 block of the 0/1 mask
-// panel (row = token).  Tokens past ntok and sequences past slen are zeros.
-// Thread t: token part t / 32, sequence t % 32 for the reads; row t for the
-// panel writes.
-constexpr int kTr = 40;        // LDS row stride (bf16) of the [256][32] transpose tile
-
+// The sums' operands are given to the contraction transposed: X[s][(tok, c)]
+// = m_s,tok a_s,tok,c in the panel layout of slen rows and ntok * 32 columns,
+// where the 32-column block of token tok and the 256-row block of sequences
+// s / 256 is one contiguous 16 KB block holding, for each sequence, the 64
+// bytes a[s][tok][0:32] as they are in the input.  So the pack is a masked
+// copy, no transpose.  One work-group per (8 tokens, 32 sequences): thread t
+// takes token part t % 8 (eight consecutive tokens of one sequence read 512
+// contiguous bytes) and sequence t / 8 (the eight sequences of a wave and
+// token write 512 contiguous bytes).  Sequences from slen up to the panel's
+// 256-row boundary get zeros; tokens past ntok have no columns and write
+// nothing.  The pair counts' operands keep the plain blocked layout (row =
+// token, k = s, bf16 0/1), written for k below the panel's 32-step boundary.
 __global__ __launch_bounds__(256) void k_opm_pack(const bf16_t* __restrict__ a, const uint8_t* __restrict__ mask,
                                                   int64_t n_total, int64_t tok0, int ntok, int64_t s0, int slen,
                                                   bf16_t* __restrict__ P, bf16_t* __restrict__ Mp) {
-    __shared__ __align__(16) bf16_t tile[256 * kTr];
     const int t = threadIdx.x;
-    const int kb = blockIdx.x, rb = blockIdx.y;
-    const int part = t >> 5, sl = t & 31;
-    const int tok = rb * 8 + part, s = kb * 32 + sl;
-    const bool valid = tok < ntok && s < slen;
+    const int part = t & 7, sl = t >> 3;
+    const int tok = blockIdx.y * 8 + part, s = blockIdx.x * 32 + sl;
     uint4 v[4] = {};
     bf16_t m = 0;
-    if (valid) {
+    if (tok < ntok && s < slen) {
         const int64_t src = ((s0 + s) * n_total + tok0 + tok);
         const uint8_t mk = mask ? mask[src] : (uint8_t)1;
         if (mk) {
@@ -49,24 +50,14 @@ __global__ __launch_bounds__(256) void k_opm_pack(const bf16_t* __restrict__ a, 
             m = 0x3f80;   // bf16 1.0
         }
     }
-    const uint32_t w[16] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w,
-                            v[2].x, v[2].y, v[2].z, v[2].w, v[3].x, v[3].y, v[3].z, v[3].w};
+    if (tok < ntok) {
+        const PanelGeom xg = panel_geom(slen, (int64_t)ntok * kD);
+        uint4* dst = reinterpret_cast<uint4*>(P + panel_off(xg, 0, s, (int64_t)tok * kD));
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        tile[(part * kD + 2 * q) * kTr + sl] = (bf16_t)(w[q] & 0xffffu);
-        tile[(part * kD + 2 * q + 1) * kTr + sl] = (bf16_t)(w[q] >> 16);
+        for (int q = 0; q < 4; ++q) dst[q] = v[q];
     }
-    // mask panel: rows = tokens, same k geometry (block of 256 rows x 32 k)
-    {
-        const PanelGeom mg = panel_geom(ntok, slen);
-        Mp[panel_off(mg, 0, rb * 8 + part, kb * 32 + sl)] = m;
-    }
-    __syncthreads();
-    const PanelGeom pg = panel_geom((int64_t)ntok * kD, slen);
-    uint4* dst = reinterpret_cast<uint4*>(P + panel_off(pg, 0, (int64_t)rb * 256 + t, (int64_t)kb * 32));
-    const uint4* srow = reinterpret_cast<const uint4*>(&tile[t * kTr]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) dst[q] = srow[q];
+    const PanelGeom mg = panel_geom(ntok, slen);
+    if (s < mg.ksteps * 32) Mp[panel_off(mg, 0, tok, s)] = m;
 }
 
 // ---------------------------------------------------------------- epilogue
@@ -211,7 +202,7 @@ __global__ __launch_bounds__(kEt) void k_opm_epilogue(const float* __restrict__ 
 
 hipError_t launch_opm_pack(const void* a, const uint8_t* mask, int64_t n_total, int64_t tok0, int64_t ntok,
                            int64_t s0, int64_t slen, void* P, void* Mp, hipStream_t s) {
-    const dim3 grid((unsigned)((slen + 31) / 32), (unsigned)((ntok + 7) / 8));
+    const dim3 grid((unsigned)((slen + 255) / 256 * 8), (unsigned)((ntok + 7) / 8));
     hipLaunchKernelGGL(k_opm_pack, grid, dim3(256), 0, s, (const bf16_t*)a, mask, n_total, tok0, (int)ntok, s0,
                        (int)slen, (bf16_t*)P, (bf16_t*)Mp);
     return hipGetLastError();

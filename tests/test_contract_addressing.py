@@ -104,12 +104,13 @@ def test_block_call_transposed_panels(view):
     assert_clean(r, tiles(rows, cols))
 
 
-@pytest.mark.parametrize("shape", [(1024, 1024, 4096), (100, 257, 37), (3, 5, 1)])
+@pytest.mark.parametrize("shape", [(1024, 1024, 4096), (100, 257, 37), (3, 5, 1), (9, 2048, 300), (64, 257, 65536)])
 def test_outer_product_mean_launches(shape):
-    # sums: rows (token, c) = ntok * 32, K = sequences; counts: rows = tokens
+    # sums: rows (token, c) = ntok * 32, K = sequences, both operands given
+    # transposed (X[s][(token, c)]); counts: rows = tokens, plain panels
     rows, cols, S = shape
-    r = T.check_contract_loads(BLK, BLK, 32 * rows, 32 * cols, S, batch=1, a_bytes=blocked_bytes(32 * rows, S, 1),
-                               b_bytes=blocked_bytes(32 * cols, S, 1), grid=min(256, tiles(32 * rows, 32 * cols, 1)))
+    r = T.check_contract_loads(TR, TR, 32 * rows, 32 * cols, S, batch=1, a_bytes=transposed_bytes(32 * rows, S, 1),
+                               b_bytes=transposed_bytes(32 * cols, S, 1), grid=min(256, tiles(32 * rows, 32 * cols, 1)))
     assert_clean(r, tiles(32 * rows, 32 * cols, 1))
     r = T.check_contract_loads(BLK, BLK, rows, cols, S, batch=1, a_bytes=blocked_bytes(rows, S, 1),
                                b_bytes=blocked_bytes(cols, S, 1), grid=min(256, tiles(rows, cols, 1)))
