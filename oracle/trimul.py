@@ -9,7 +9,7 @@ What it computes (Fold-CP, Section 3.3, Eq. 2 and Eq. 3):
     outgoing:  C[n, m, c] = sum_k a[n, k, c] * b[m, k, c]
     incoming:  C[n, m, c] = sum_k a[k, n, c] * b[k, m, c]
 
-where a and b are gated projections of the pair representation
+where a and b are gated linear maps of the pair tensor
 z in R^{N x N x c_z} (Section 3.3 names only projections of z and an
 element-wise gate; the concrete layer is the usual AlphaFold-family triangle
 update that the paper's Boltz models use, written out as mathematics below).  For a pair
