@@ -6,7 +6,7 @@
  *   outgoing:  C[i][j][c] = sum_k a[i][k][c] * b[j][k][c]
  *   incoming:  C[i][j][c] = sum_k a[k][i][c] * b[k][j][c]
  *
- * where a and b are gated projections of the pair representation z
+ * where a and b are gated linear maps of the pair tensor z
  * (Section 3.3 names the projections and their element-wise gate without
  * spelling out the layer; the layer below is the usual one).  For every
  * pair (i, j), with pair mask m_ij = m_i * m_j:

@@ -5,7 +5,7 @@ this module; only the tests, the smoke check and the benchmark's CPU-baseline
 leg use it.  It shares no code, constants or helpers with the HIP library.
 
 What it computes (Section 3.5, the equation for z_ijcd): a and b are
-projections of the MSA representation, shape [S][N][D] (sequences, tokens,
+linear maps of the MSA features, shape [S][N][D] (sequences, tokens,
 channels).  The pair feature of tokens (i, j) is the mean over sequences of
 the outer product a_si (x) b_sj, a D x D matrix, which is flattened (index
 c * D + d) and linearly projected to c_z channels:
