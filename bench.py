@@ -503,8 +503,17 @@ def main():
         a1.record(stream)
         torch.cuda.synchronize()
         ta_ms = a0.elapsed_time(a1) / 3
-        del tq, tk, tv, tb, tout
-        print(f"[bench] triangle attention {ta_ms:.3f} ms", file=sys.stderr, flush=True)
+        # the same with bf16 output (the probabilities enter the PV product as bf16 alone)
+        tout16 = torch.empty((tn, tn, tH, 32), dtype=torch.bfloat16, device=dev)
+        T.tri_attn_forward(tq, tk, tv, tb, None, tn, tn, tH, tn, "bf16", tout16, stream)
+        a0.record(stream)
+        for _ in range(3):
+            T.tri_attn_forward(tq, tk, tv, tb, None, tn, tn, tH, tn, "bf16", tout16, stream)
+        a1.record(stream)
+        torch.cuda.synchronize()
+        ta16_ms = a0.elapsed_time(a1) / 3
+        del tq, tk, tv, tb, tout, tout16
+        print(f"[bench] triangle attention {ta_ms:.3f} ms (bf16 output {ta16_ms:.3f} ms)", file=sys.stderr, flush=True)
 
         # one device's share of the paper's 2-D ring, outside the timed region:
         # tile (7, 7) of an 8 x 8 grid at N = 30000 (3750 x 3750 pairs, the last
@@ -675,7 +684,7 @@ def main():
                                "what": "opm_forward, S=4096 sequences x N=1024 tokens, D=32, c_z=128, bf16 in, "
                                        "fp32 out: 2*S*(N*D)^2 = 8.80 TFLOP contraction + counts + projection; "
                                        "not part of ms_per_step"},
-        "triangle_attention": None if ta_ms is None else {"ms": round(ta_ms, 4),
+        "triangle_attention": None if ta_ms is None else {"ms": round(ta_ms, 4), "ms_bf16_out": round(ta16_ms, 4),
                                "G_scores_per_s": round(ta_scores / (ta_ms * 1e-3) / 1e9, 1),
                                "TFLOP_per_s": round(4 * 32 * ta_scores / (ta_ms * 1e-3) / 1e12, 2),
                                "roofline": {"bound": "alu", "achieved": round(ta_scores / (ta_ms * 1e-3) / 1e12, 3),
@@ -685,8 +694,8 @@ def main():
                                                                                          / perf.TRIATTN_SLOTS), 4),
                                             "peak_basis": perf.TRIATTN_BASIS},
                                "what": "tri_attn_forward, rows = n = 2048, 4 heads of 32, bf16 in, fp32 out: "
-                                       "rows*H*n^2 = 34.4e9 scores (QK and PV 128 flop each); not part of "
-                                       "ms_per_step"},
+                                       "rows*H*n^2 = 34.4e9 scores (QK and PV 128 flop each); ms_bf16_out: the "
+                                       "same call with bf16 output; not part of ms_per_step"},
         "ring_tile": None if tile_ms is None else {"ms": round(tile_ms, 4),
                       "TFLOP_per_s": round(tile_flops / (tile_ms * 1e-3) / 1e12, 2),
                       "roofline": mfma_roof(tile_flops, tile_ms),

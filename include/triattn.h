@@ -16,6 +16,9 @@
  * (head dimension 32); bias [heads][n][ld_bias] (ld_bias % 8 == 0,
  * ld_bias >= n); mask uint8 [n] or NULL (all present); out
  * [rows][n][heads][32] of out_dtype (TRI_MUL_F32 or TRI_MUL_BF16).
+ * Precision: with fp32 output the softmax weights enter the weighted sum
+ * of v with ~16 mantissa bits; with bf16 output with 8 (bf16), an error of
+ * the same order as the output's own rounding.
  * Status codes and the error message as in tri_mul.h; asynchronous on
  * `stream` (hipStream_t, NULL = default); validation before any launch.
  */

@@ -51,6 +51,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
     __shared__ __align__(16) char vs[2][kKc * 64];            // V chunks [64 keys][32 d], row-major
     __shared__ __align__(16) bf16_t bt[2][kQt * kBRow];       // bias tiles
     __shared__ float mb[2][kKc];                              // 0 or -inf per key
+    constexpr bool kHiLo = sizeof(TO) == 4;                   // P enters the PV product as hi + lo
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const int ql = lane & 31, hi = lane >> 5;
     const int qtiles = (N + kQt - 1) / kQt;
@@ -211,15 +212,20 @@ __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_pe
                 const uint2 v0 = lds_read_tr4(vr);
                 const uint2 v1 = lds_read_tr4(vr + 8 * 64);
                 const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+                // P as bf16 hi + lo for fp32 output (~16 mantissa bits of p); with
+                // bf16 output the hi part alone (its 2^-9 rounding averages over the
+                // keys, below the output's own rounding)
                 uint32_t ph[4], pl[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float x0 = s[b][8 * t2 + 2 * e], x1 = s[b][8 * t2 + 2 * e + 1];
                     ph[e] = pack_bf16x2(x0, x1);
-                    pl[e] = pack_bf16x2(x0 - __uint_as_float(ph[e] << 16), x1 - __uint_as_float(ph[e] & 0xffff0000u));
+                    if constexpr (kHiLo)
+                        pl[e] = pack_bf16x2(x0 - __uint_as_float(ph[e] << 16), x1 - __uint_as_float(ph[e] & 0xffff0000u));
                 }
                 o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, __builtin_bit_cast(bf16x8_t, make_uint4(ph[0], ph[1], ph[2], ph[3])), o, 0, 0, 0);
-                o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, __builtin_bit_cast(bf16x8_t, make_uint4(pl[0], pl[1], pl[2], pl[3])), o, 0, 0, 0);
+                if constexpr (kHiLo)
+                    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, __builtin_bit_cast(bf16x8_t, make_uint4(pl[0], pl[1], pl[2], pl[3])), o, 0, 0, 0);
             }
         // no barrier here: the next chunk stages into the other buffer, and the
         // one after that only once every wave has passed the next barrier

@@ -8,7 +8,11 @@ bias are added in fp32; exp is v_exp_f32 (about 1 ulp) of an fp32 argument,
 so each weight carries ~|s| 2^-24 relative error; the weights enter the
 P V product as bf16 hi + lo (relative truncation <= 2^-17 ~ 7.6e-6) against
 bf16 values (exact), fp32 accumulation and normalisation.  With bf16 output
-one more rounding (<= 2^-9 relative): relative Frobenius <= 3e-3."""
+the weights enter the product as bf16 alone (<= 2^-9 relative each; since
+the output is itself a weighted mean, these roundings are of the same
+relative size in it as in the weights, ~1.1e-3 RMS) and the output is
+rounded once more (<= 2^-9): ~1.6e-3 in quadrature, measured 2.0e-3 (1.7e-3
+with hi + lo weights); relative Frobenius <= 3e-3."""
 import numpy as np
 import pytest
 import torch
