@@ -129,3 +129,23 @@ def test_triangle_attention_errors():
     with pytest.raises(T.TriMulError) as e:          # a chunked attention without a state
         T.tri_attn_chunk(T.TriAttnView(rows, n, H, T.TRI_MUL_F32, n, 0, 32, 0, 2), qd, kd, vd, bd, None, None, out)
     assert e.value.code == T.TRI_MUL_EINVAL
+
+
+@pytest.mark.parametrize("cuts", [[0, 64, 128, 200], [0, 8, 200]])
+def test_chunked_steps_bf16_output(cuts):
+    """The ring's chunk merge with bf16 output (the weights enter the PV
+    product as bf16 alone in every chunk; the merge state stays fp32): the
+    bf16 bar of a single call."""
+    rows, n, H = 2, 200, 4
+    q, k, v, bfull, mask = inputs(rows, n, H, seed=13, masked=True)
+    mask[130:180] = 0
+    qd, kd, vd, bd, md = dev(q, k, v, bfull, mask)
+    view = T.TriAttnView(rows, n, H, T.TRI_MUL_BF16, bfull.shape[2], 0, n, 0, 1)
+    state = torch.full((T.tri_attn_state_size(view) // 4,), float("nan"), device="cuda")
+    out = torch.empty((rows, n, H, 32), dtype=torch.bfloat16, device="cuda")
+    for t, (k0, k1) in enumerate(zip(cuts[:-1], cuts[1:])):
+        v_t = T.TriAttnView(rows, n, H, T.TRI_MUL_BF16, bfull.shape[2], k0, k1 - k0, t, len(cuts) - 1)
+        T.tri_attn_chunk(v_t, qd, kd, vd, bd, md, state, out)
+    torch.cuda.synchronize()
+    ref = oracle.triangle_attention(host(q), host(k), host(v), host(bfull[:, :, :n]), mask.numpy())
+    check(host(out), ref, f"bf16 chunks {cuts}", rel_tol=3e-3, max_rel=1e-2)
